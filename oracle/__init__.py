@@ -1,0 +1,155 @@
+"""CPU oracle for the tile-major GEMM path -- TEST INFRASTRUCTURE ONLY.
+
+Only tests/, ``__graft_entry__.smoke()`` and bench.py's ``cpu_baseline`` leg
+may import this package.  The product library (``paper_2607_04031_amd``) never
+imports it, and it imports nothing from the product library.
+
+The arithmetic lives in ``tl_oracle.c`` (plain C, fp64, '/' and '%' only);
+this module is argument marshalling over ctypes plus numpy buffers.
+
+What each function follows (TileLens, arxiv 2607.04031):
+  tm_offset      Eq. 1 and Eq. 2, Section 3.2
+  repack/unpack  Section 3.2 (the permutation Eq. 2 defines); Section 5.1
+                 (weights are written in this order once, at load time)
+  gemm_f64       Section 2.3 (C = A W^T over the K dimension), fp64
+  round_bf16     round-to-nearest-even to 8 significant bits
+  read_amp       Sections 1, 2.5 and 6.4 (requests per compute tile at
+                 granularity G; weights only, Section 5.1)
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+NK_ROW, KN_ROW, TILE = 0, 1, 2
+
+
+class Amp(ctypes.Structure):
+    _fields_ = [("compute_tiles", ctypes.c_int64),
+                ("requests", ctypes.c_int64),
+                ("fetched_bytes", ctypes.c_int64),
+                ("useful_bytes", ctypes.c_int64),
+                ("unique_blocks", ctypes.c_int64),
+                ("min_blocks_per_tile", ctypes.c_int64),
+                ("max_blocks_per_tile", ctypes.c_int64),
+                ("amp", ctypes.c_double)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    i64, p = ctypes.c_int64, ctypes.c_void_p
+    lib.orc_tm_offset.restype = i64
+    lib.orc_tm_offset.argtypes = [i64] * 6
+    lib.orc_elem_offset.restype = i64
+    lib.orc_elem_offset.argtypes = [ctypes.c_int] + [i64] * 7
+    lib.orc_repack.restype = None
+    lib.orc_repack.argtypes = [p, p] + [i64] * 5
+    lib.orc_unpack.restype = None
+    lib.orc_unpack.argtypes = [p, p] + [i64] * 5
+    lib.orc_gemm_f64.restype = None
+    lib.orc_gemm_f64.argtypes = [p, p, p, i64, i64, i64]
+    lib.orc_gemm_f64_points.restype = None
+    lib.orc_gemm_f64_points.argtypes = [p, p, p, p, p, i64, i64]
+    lib.orc_round_bf16.restype = ctypes.c_uint16
+    lib.orc_round_bf16.argtypes = [ctypes.c_double]
+    lib.orc_round_bf16_array.restype = None
+    lib.orc_round_bf16_array.argtypes = [p, p, i64]
+    lib.orc_read_amp.restype = ctypes.c_int
+    lib.orc_read_amp.argtypes = [i64] * 6 + [ctypes.c_int] + [i64] * 4 + [
+        ctypes.c_int, ctypes.POINTER(Amp)]
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray) -> int:
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data
+
+
+def tm_offset(r: int, c: int, cols: int, s: int, G: int, block_rows: int) -> int:
+    """Eq. 2 byte offset of stored element (r, c); c is the contiguous index."""
+    return _load().orc_tm_offset(r, c, cols, s, G, block_rows)
+
+
+def elem_offset(kind: int, n: int, k: int, N: int, K: int, s: int,
+                layout_G: int = 4096, block_rows: int = 32) -> int:
+    return _load().orc_elem_offset(kind, n, k, N, K, s, layout_G, block_rows)
+
+
+def _as_bytes(x: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(x).view(np.uint8).reshape(-1)
+
+
+def repack(src: np.ndarray, G: int, block_rows: int) -> np.ndarray:
+    """Row-major [rows, cols] -> tile-major bytes, same dtype and shape."""
+    rows, cols = src.shape
+    s = src.dtype.itemsize
+    out = np.empty_like(src)
+    _load().orc_repack(_ptr(_as_bytes(src)), _ptr(out), rows, cols, s, G, block_rows)
+    return out
+
+
+def unpack(src_tm: np.ndarray, G: int, block_rows: int) -> np.ndarray:
+    rows, cols = src_tm.shape
+    s = src_tm.dtype.itemsize
+    out = np.empty_like(src_tm)
+    _load().orc_unpack(_ptr(_as_bytes(src_tm)), _ptr(out), rows, cols, s, G, block_rows)
+    return out
+
+
+def gemm_f64(A_bf16: np.ndarray, W_bf16: np.ndarray) -> np.ndarray:
+    """A: uint16 bf16 bits [M,K]; W: uint16 bf16 bits [N,K] ROW-MAJOR -> fp64 [M,N]."""
+    A = np.ascontiguousarray(A_bf16, dtype=np.uint16)
+    W = np.ascontiguousarray(W_bf16, dtype=np.uint16)
+    M, K = A.shape
+    N, K2 = W.shape
+    assert K == K2
+    Y = np.empty((M, N), dtype=np.float64)
+    _load().orc_gemm_f64(_ptr(A), _ptr(W), _ptr(Y), M, N, K)
+    return Y
+
+
+def gemm_f64_points(A_bf16: np.ndarray, W_bf16: np.ndarray, ms, ns) -> np.ndarray:
+    A = np.ascontiguousarray(A_bf16, dtype=np.uint16)
+    W = np.ascontiguousarray(W_bf16, dtype=np.uint16)
+    ms = np.ascontiguousarray(ms, dtype=np.int64)
+    ns = np.ascontiguousarray(ns, dtype=np.int64)
+    assert ms.shape == ns.shape
+    y = np.empty(ms.shape, dtype=np.float64)
+    _load().orc_gemm_f64_points(_ptr(A), _ptr(W), _ptr(ms), _ptr(ns), _ptr(y),
+                                ms.size, A.shape[1])
+    return y
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty(x.shape, dtype=np.uint16)
+    _load().orc_round_bf16_array(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+def read_amp(M: int, N: int, K: int, tm: int, tn: int, tk: int, kind: int,
+             G: int, s: int = 2, layout_G: int = 4096, block_rows: int = 32,
+             brute_m: bool = False) -> dict:
+    """Brute-force read amplification (see tl_oracle.c for the model)."""
+    out = Amp()
+    rc = _load().orc_read_amp(M, N, K, tm, tn, tk, kind, s, layout_G, block_rows, G,
+                              1 if brute_m else 0, ctypes.byref(out))
+    if rc != 0:
+        raise ValueError("orc_read_amp: bad arguments")
+    return out.as_dict()

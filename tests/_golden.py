@@ -1,0 +1,19 @@
+"""Reader for the small key = value fixtures under tests/golden/."""
+import os
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def load(name: str) -> dict:
+    out = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            key, val = (x.strip() for x in line.split("=", 1))
+            try:
+                out[key] = int(val)
+            except ValueError:
+                out[key] = val
+    return out

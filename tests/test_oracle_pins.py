@@ -1,0 +1,372 @@
+"""Pins for the CPU oracle: each test checks the oracle against something other
+than itself -- a value the paper prints, a numpy library routine, a closed form,
+or an invariant -- so that a dropped term, a wrong sign or index, or a transposed
+operand in the oracle fails at least one of them.  CPU only."""
+import itertools
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import NK_ROW, KN_ROW, TILE
+from paper_2607_04031_amd import synth
+from tests._golden import load
+
+
+# ---------------------------------------------------------------------------
+# Repack / Eq. 2
+# ---------------------------------------------------------------------------
+
+REPACK_CASES = [
+    # rows, cols, elem_bytes, G, block_rows
+    (64, 128, 2, 4096, 32),      # the evaluated (64, 32) BF16 tile
+    (128, 256, 2, 4096, 8),
+    (128, 64, 2, 4096, 32),      # one block column
+    (256, 512, 1, 4096, 64),     # FP8 64 x 64
+    (96, 320, 2, 512, 16),       # non power-of-two block counts
+    (64, 512, 4, 1024, 4),       # 4-byte elements
+    (32, 4096, 2, 16384, 4),
+]
+
+
+@pytest.mark.parametrize("rows,cols,s,G,br", REPACK_CASES)
+def test_repack_equals_numpy_reshape_transpose(rows, cols, s, G, br):
+    """Eq. 2 == the block reshape: [R/br, br, C/bc, bc] -> swap axes 1 and 2."""
+    bc = G // (s * br)
+    dt = {1: np.uint8, 2: np.uint16, 4: np.uint32}[s]
+    src = synth.random_bytes(rows * cols * s, seed=rows + cols + G).view(dt).reshape(rows, cols)
+    got = oracle.repack(src, G, br).reshape(-1)
+    want = src.reshape(rows // br, br, cols // bc, bc).transpose(0, 2, 1, 3).reshape(-1)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("rows,cols,s,G,br", REPACK_CASES)
+def test_repack_roundtrip_and_bijection(rows, cols, s, G, br):
+    dt = {1: np.uint8, 2: np.uint16, 4: np.uint32}[s]
+    src = synth.random_bytes(rows * cols * s, seed=7).view(dt).reshape(rows, cols)
+    tm = oracle.repack(src, G, br)
+    assert np.array_equal(oracle.unpack(tm, G, br), src)
+    # every destination element slot is hit exactly once
+    offs = np.array([oracle.tm_offset(r, c, cols, s, G, br)
+                     for r in range(0, rows, max(1, rows // 16))
+                     for c in range(cols)])
+    assert len(set(offs.tolist())) == offs.size
+    assert offs.min() >= 0 and offs.max() < rows * cols * s
+    assert np.all(offs % s == 0)
+
+
+def test_eq3_four_d_strides_view():
+    """Eq. 3: the tile-major buffer viewed with shape (a, b, K/a, N/b) and
+    element strides (1, a, ab, Kb) returns element (i, j) of the K x N matrix
+    at coordinates (i mod a, j mod b, i / a, j / b).  Built with numpy's
+    stride machinery, not with the oracle's offset function."""
+    K, N, s, G, b = 512, 128, 2, 4096, 32
+    a = G // (s * b)
+    W = synth.random_bytes(N * K * s, seed=3).view(np.uint16).reshape(N, K)   # W[j][i]
+    tm = oracle.repack(W, G, b).reshape(-1)
+    view = np.lib.stride_tricks.as_strided(
+        tm, shape=(a, b, K // a, N // b),
+        strides=(1 * s, a * s, a * b * s, K * b * s))
+    for i, j in itertools.product(range(0, K, 37), range(0, N, 11)):
+        assert view[i % a, j % b, i // a, j // b] == W[j, i]
+
+
+def test_eq4_tilebase_at_aligned_points():
+    """Eq. 4: at memory-tile-aligned (i, j), offset = (K j + i b) s."""
+    for (K, N, s, G, b) in [(512, 128, 2, 4096, 32), (1024, 256, 1, 4096, 64),
+                            (256, 64, 2, 1024, 8)]:
+        a = G // (s * b)
+        for i in range(0, K, a):
+            for j in range(0, N, b):
+                assert oracle.tm_offset(j, i, K, s, G, b) == (K * j + i * b) * s
+
+
+def test_case2_bit_permutation_example():
+    """Section 4.3 Case 2: FP8 128 x 32 memory tile, 32 x 32 TMA tile.  The
+    actual intra-tile offset has fields (col | sub | row); the sub-tile view
+    assumed (sub | col | row)."""
+    g = load("paper_case2_bitperm.txt")
+    a, b, u = g["memory_tile_a"], g["memory_tile_b"], g["tma_tile_u"]
+    s, G = g["elem_bytes"], g["granularity"]
+    assert a * b * s == G
+
+    def pack(fields, vals):
+        out = 0
+        for name_w in fields.split():
+            name, w = name_w.split(":")
+            w = int(w)
+            assert 0 <= vals[name] < (1 << w)
+            out = (out << w) | vals[name]
+        return out
+
+    K = 4 * a  # four memory tiles along the contiguous dim, one strip of b
+    for sub, col, row in itertools.product(range(a // u), range(b), range(u)):
+        i = sub * u + row       # contiguous index inside the memory tile
+        j = col
+        off = oracle.tm_offset(j, i, K, s, G, b) % G
+        vals = {"sub": sub, "col": col, "row": row}
+        assert off == pack(g["actual_fields"], vals)
+        # the assumed sub-tile offset differs exactly by the field permutation
+        assumed = pack(g["assumed_fields"], vals)
+        assert assumed == sub * (u * b) + col * u + row
+
+
+def test_view_example_addresses_same_elements():
+    """Section 4.3: the 2-D, 3-D and 4-D descriptors of one FP8 384 x 128
+    column-major matrix address the same 128 x 64 tile.  The leading-stride
+    rule (strides below K feed the contiguous index i, the rest feed K*j)
+    recovers (i, j), and the tile-major offsets of the three views agree."""
+    g = load("paper_view_example.txt")
+    K, N = g["K"], g["N"]
+
+    def parse(v):
+        return [list(map(int, p.split(","))) for p in v.split(";")]
+
+    views = {name: parse(g[name]) for name in ("view2d", "view3d", "view4d")}
+    # element strides of each view: the first dimension is contiguous; the
+    # others follow from how each view tiles the K x N column-major matrix
+    strides = {
+        "view2d": [1, K],
+        "view3d": [1, K, 128],
+        "view4d": [1, K, 128, 64 * K],
+    }
+    sets = {}
+    for name, (dims, coords, tile) in views.items():
+        st = strides[name]
+        offs = set()
+        for idx in itertools.product(*[range(t) for t in tile]):
+            lin = sum((c + x) * s_ for c, x, s_ in zip(coords, idx, st))
+            i = sum((c + x) * s_ for c, x, s_ in zip(coords, idx, st) if s_ < K)
+            kj = sum((c + x) * s_ for c, x, s_ in zip(coords, idx, st) if s_ >= K)
+            assert kj % K == 0 and i + kj == lin
+            j = kj // K
+            assert 0 <= i < K and 0 <= j < N
+            offs.add(oracle.tm_offset(j, i, K, 1, 4096, 64))
+        sets[name] = offs
+    logical = {oracle.tm_offset(j, i, K, 1, 4096, 64)
+               for i in range(256, 384) for j in range(64, 128)}
+    assert sets["view2d"] == sets["view3d"] == sets["view4d"] == logical
+    assert len(logical) == 128 * 64
+
+
+def test_memory_tile_shapes_and_identity_extremes():
+    """Section 3.1: shapes multiply to G; the (contiguous = G/s, other = 1)
+    extreme is the plain row-major order, so the repack is the identity;
+    a block as wide as the whole row is also the identity."""
+    g = load("paper_memory_tiles.txt")
+    for key in ("fp8_square_tile", "fp8_row_major_extreme", "bf16_eval_tile"):
+        a, b, s, G = map(int, g[key].split(","))
+        assert a * b * s == G
+    a, b, s, G = map(int, g["fp8_row_major_extreme"].split(","))
+    src = synth.random_bytes(8 * 8192, seed=1).reshape(8, 8192)
+    assert np.array_equal(oracle.repack(src, G, b), src)
+    # bc == cols: one block column per strip
+    src16 = synth.random_bytes(64 * 64 * 2, seed=2).view(np.uint16).reshape(64, 64)
+    assert np.array_equal(oracle.repack(src16, 4096, 32), src16)
+
+
+# ---------------------------------------------------------------------------
+# GEMM
+# ---------------------------------------------------------------------------
+
+def test_gemm_matches_numpy_float64():
+    A = synth.normal_bf16((7, 96), seed=1)
+    W = synth.normal_bf16((40, 96), seed=2, sigma=0.02)
+    Af, Wf = synth.bf16_bits_to_f32(A).astype(np.float64), synth.bf16_bits_to_f32(W).astype(np.float64)
+    want = Af @ Wf.T
+    got = oracle.gemm_f64(A, W)
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-14)
+
+
+def test_gemm_orientation_not_transposed():
+    """A non-square, asymmetric case where A W^T and A W (or W A^T) differ."""
+    A = synth.small_int_bf16((3, 5), seed=4)
+    W = synth.small_int_bf16((2, 5), seed=5)
+    Af, Wf = synth.bf16_bits_to_f32(A), synth.bf16_bits_to_f32(W)
+    got = oracle.gemm_f64(A, W)
+    assert got.shape == (3, 2)
+    for m in range(3):
+        for n in range(2):
+            assert got[m, n] == sum(float(Af[m, k]) * float(Wf[n, k]) for k in range(5))
+
+
+def test_gemm_one_hot_selects_weight_column():
+    K = 256
+    A, ks = synth.one_hot_bf16(9, K, seed=3)
+    W = synth.normal_bf16((33, K), seed=4, sigma=0.02)
+    got = oracle.gemm_f64(A, W)
+    Wf = synth.bf16_bits_to_f32(W).astype(np.float64)
+    assert np.array_equal(got, Wf[:, ks].T)
+
+
+def test_gemm_small_integers_exact_and_zero_weight():
+    A = synth.small_int_bf16((5, 300), seed=8)
+    W = synth.small_int_bf16((17, 300), seed=9)
+    Ai = synth.bf16_bits_to_f32(A).astype(np.int64)
+    Wi = synth.bf16_bits_to_f32(W).astype(np.int64)
+    assert np.array_equal(oracle.gemm_f64(A, W), (Ai @ Wi.T).astype(np.float64))
+    Z = np.zeros_like(W)
+    assert np.all(oracle.gemm_f64(A, Z) == 0.0)
+
+
+def test_gemm_points_equal_full():
+    A = synth.normal_bf16((4, 64), seed=1)
+    W = synth.normal_bf16((20, 64), seed=2, sigma=0.02)
+    full = oracle.gemm_f64(A, W)
+    ms = np.array([0, 3, 2, 1]); ns = np.array([19, 0, 7, 7])
+    assert np.array_equal(oracle.gemm_f64_points(A, W, ms, ns), full[ms, ns])
+
+
+def test_round_bf16_against_float32_bit_rounding():
+    """The oracle's bf16 rounding of doubles equals numpy float32 -> bf16 RNE
+    on values that are exactly float32, and breaks ties to even."""
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal(4096).astype(np.float32) * np.float32(3.0)
+    assert np.array_equal(oracle.round_bf16(x.astype(np.float64)), synth.f32_to_bf16_bits(x))
+    one = 1.0
+    ties = np.array([one + 2.0 ** -8, one + 3 * 2.0 ** -8, -(one + 2.0 ** -8), 0.0])
+    got = synth.bf16_bits_to_f32(oracle.round_bf16(ties))
+    assert got[0] == 1.0 and got[1] == 1.0 + 2.0 ** -6 and got[2] == -1.0 and got[3] == 0.0
+
+
+# ---------------------------------------------------------------------------
+# Read amplification
+# ---------------------------------------------------------------------------
+
+def test_requests_per_tile_section_6_4():
+    """128 (row-major, 512 B strips) vs 16 (tile-major (64, 32)) 4 KB requests
+    per 128 x 256 BF16 compute tile; the contiguous side is 256 wide."""
+    g = load("paper_requests_per_tile.txt")
+    G, s = g["granularity"], g["elem_bytes"]
+    N = K = 2048
+    # paper "row-major": N contiguous (KN_ROW); 256 along N, 128 along K
+    r = oracle.read_amp(1, N, K, 1, g["tile_contiguous_elems"], g["tile_other_elems"],
+                        KN_ROW, G, s=s)
+    assert r["min_blocks_per_tile"] == r["max_blocks_per_tile"] == g["requests_row_major"]
+    assert g["tile_contiguous_elems"] * s == g["strip_bytes"]
+    # tile-major: memory tile (a, b) = (64, 32), a along the contiguous dim
+    t = oracle.read_amp(1, N, K, 1, 256, 128, TILE, G, s=s,
+                        layout_G=G, block_rows=g["memory_tile_b"])
+    assert G // (s * g["memory_tile_b"]) == g["memory_tile_a"]
+    assert t["min_blocks_per_tile"] == t["max_blocks_per_tile"] == g["requests_tile_major"]
+    extra = g["requests_row_major"] - g["requests_tile_major"]
+    assert extra == g["extra_requests"] and extra * G == g["extra_bytes"]
+
+
+def test_amp_32x_for_128B_wide_tile():
+    g = load("paper_memory_tiles.txt")
+    r = oracle.read_amp(4, 256, 4096, 4, 64, 64, NK_ROW, 4096)
+    assert r["amp"] == g["amp_128B_wide_tile"]
+
+
+def _closed_form_amp(kind, N, K, tn, tk, s, G, layout_G, br):
+    """Closed forms for power-of-two tiles/blocks with no tile row segment
+    straddling a block boundary (derived by hand, independent of the
+    enumeration)."""
+    if kind == TILE:
+        bc = layout_G // (s * br)
+        assert layout_G == G
+        return max(1, br // tn) * max(1, bc // tk)
+    if kind == KN_ROW:
+        N, K, tn, tk = K, N, tk, tn     # same formula with roles swapped
+    if K * s >= G:
+        return max(1, G // (tk * s))
+    R = G // (K * s)                    # whole rows per block
+    return math.ceil(tn / R) * G / (tn * tk * s)
+
+
+@pytest.mark.parametrize("kind", [NK_ROW, KN_ROW, TILE])
+@pytest.mark.parametrize("G", [512, 1024, 4096, 16384])
+def test_read_amp_closed_forms(kind, G):
+    N, K, s = 256, 2048, 2
+    for tn, tk in itertools.product([16, 64, 128], [32, 64, 256]):
+        for br in ([8, 32, 64] if kind == TILE else [32]):
+            if kind == TILE and (G // (s * br)) < 1:
+                continue
+            if kind == TILE and (N % br or K % (G // (s * br))):
+                continue
+            r = oracle.read_amp(3, N, K, 2, tn, tk, kind, G, s=s, layout_G=G, block_rows=br)
+            want = _closed_form_amp(kind, N, K, tn, tk, s, G, G, br)
+            assert r["amp"] == pytest.approx(want, rel=0, abs=1e-12), (kind, G, tn, tk, br)
+            assert r["useful_bytes"] == 2 * N * K * s      # two m-tiles of M = 3, tm = 2
+            assert r["fetched_bytes"] == r["requests"] * G
+
+
+def test_fit_rule_gives_no_amplification():
+    """Sections 1 and 3.1: compute tile dims that are multiples of the memory
+    tile dims eliminate amplification."""
+    rng = np.random.default_rng(5)
+    for _ in range(40):
+        s = int(rng.choice([1, 2]))
+        G = int(rng.choice([512, 1024, 4096]))
+        br = int(rng.choice([1, 2, 4, 8, 16, 32]))
+        bc = G // (s * br)
+        if bc < 1:
+            continue
+        tn, tk = br * int(rng.integers(1, 4)), bc * int(rng.integers(1, 3))
+        N, K = tn * int(rng.integers(1, 4)), tk * int(rng.integers(1, 4))
+        r = oracle.read_amp(5, N, K, 5, tn, tk, TILE, G, s=s, layout_G=G, block_rows=br)
+        assert r["amp"] == 1.0 and r["unique_blocks"] * G == N * K * s
+
+
+def test_tiny_config_amplification():
+    """W[1024, 1024] bf16, 64 x 64 compute tile, 4 KB: the K-contiguous and
+    N-contiguous layouts both fetch 16x; tile-major (32 x 64) fetches 1x."""
+    assert oracle.read_amp(16, 1024, 1024, 64, 64, 64, NK_ROW, 4096)["amp"] == 16.0
+    assert oracle.read_amp(16, 1024, 1024, 64, 64, 64, KN_ROW, 4096)["amp"] == 16.0
+    assert oracle.read_amp(16, 1024, 1024, 64, 64, 64, TILE, 4096,
+                           layout_G=4096, block_rows=32)["amp"] == 1.0
+
+
+def test_hand_counted_small_case():
+    """W[4, 8] bf16 row-major, G = 8 B (4 elements per block), 2 x 2 tiles:
+    each tile row segment sits in one block, two rows -> 2 blocks per tile,
+    8 tiles -> 16 requests, 128 B fetched for 64 useful bytes."""
+    r = oracle.read_amp(1, 4, 8, 1, 2, 2, NK_ROW, 8)
+    assert (r["compute_tiles"], r["requests"], r["fetched_bytes"], r["useful_bytes"]) == (8, 16, 128, 64)
+    assert r["unique_blocks"] == 8 and r["amp"] == 2.0
+    # KN_ROW: stored [8][4]; 4 elements per block = one stored row;
+    # a 2 x 2 tile covers 2 stored rows -> 2 blocks
+    r = oracle.read_amp(1, 4, 8, 1, 2, 2, KN_ROW, 8)
+    assert r["requests"] == 16
+
+
+def test_brute_force_over_m_tiles_matches_multiplied_count():
+    for kind in (NK_ROW, KN_ROW, TILE):
+        a = oracle.read_amp(37, 96, 320, 8, 32, 64, kind, 1024, layout_G=1024, block_rows=8)
+        b = oracle.read_amp(37, 96, 320, 8, 32, 64, kind, 1024, layout_G=1024, block_rows=8,
+                            brute_m=True)
+        assert a == b
+
+
+def test_ragged_tiles_against_python_sets():
+    """Ragged edges: tiles are clipped, useful bytes count in-matrix elements
+    only, a partial block still costs G.  Cross-check with Python sets on
+    tiny shapes."""
+    for (N, K, tn, tk, G, kind) in [(10, 24, 4, 7, 16, NK_ROW), (9, 13, 5, 4, 8, KN_ROW),
+                                    (12, 40, 8, 16, 16, NK_ROW)]:
+        s = 2
+        req = useful = 0
+        for n0 in range(0, N, tn):
+            for k0 in range(0, K, tk):
+                blocks = set()
+                for n in range(n0, min(n0 + tn, N)):
+                    for k in range(k0, min(k0 + tk, K)):
+                        off = (n * K + k) * s if kind == NK_ROW else (k * N + n) * s
+                        blocks.add(off // G)
+                req += len(blocks)
+                useful += (min(n0 + tn, N) - n0) * (min(k0 + tk, K) - k0) * s
+        r = oracle.read_amp(1, N, K, 1, tn, tk, kind, G)
+        assert r["requests"] == req and r["useful_bytes"] == useful == N * K * s
+
+
+def test_granularity_sweep_expectations_on_slice():
+    """Down-projection [8192, 28672] on a 256-row slice (the slice does not
+    change per-tile counts: every tile row is the same distance from block
+    boundaries).  NK_ROW: tk = 64 gives 4/8/32/128x for G = 512 B .. 16 KB."""
+    N, K = 256, 28672
+    for G, want in [(512, 4), (1024, 8), (4096, 32), (16384, 128)]:
+        assert oracle.read_amp(32, N, K, 32, 64, 64, NK_ROW, G)["amp"] == want
+    # tile-major (G = 4 KB, br = 8 -> bc = 256): 4x at tk = 64
+    assert oracle.read_amp(32, N, K, 32, 64, 64, TILE, 4096, layout_G=4096, block_rows=8)["amp"] == 4.0
