@@ -1,0 +1,203 @@
+/*
+ * tl.h -- C ABI of libtl: GEMMs over weights stored in a tile-major layout,
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * Method: TileLens (arxiv 2607.04031).  A large-granularity memory returns a
+ * whole G-byte block (e.g. 4 KB) per request.  In a row- or column-major
+ * weight each block is a 1-D strip that mostly falls outside the 2-D compute
+ * tile that asked for it: read amplification (Sections 1 and 2.5).  The
+ * tile-major layout reshapes every contiguous G-byte block into a 2-D
+ * "memory tile" of block_rows x block_cols elements (Section 3.1) so that a
+ * compute tile whose sides are multiples of the memory tile's sides uses
+ * every byte it fetches.  Kernels that compute their own addresses adopt the
+ * layout by replacing their address arithmetic with the shifts and masks of
+ * Eq. 1 and Eq. 2 (Sections 3.2 and 4.4); the kernels behind this ABI do so.
+ *
+ * Conventions (every entry point):
+ *  - A GEMM weight is logically W[N][K] (outputs x inputs, the orientation of
+ *    a linear layer's weight).  The paper's "column-major K x N" weight is
+ *    this matrix stored row-major (TL_LAYOUT_NK_ROW); its "row-major" weight
+ *    is TL_LAYOUT_KN_ROW (Section 2.4).
+ *  - Sizes are element counts unless the name says bytes; G is in bytes.
+ *  - Device pointers are allocated and owned by the caller, must be 16-byte
+ *    aligned, and must stay valid until the work enqueued on 'stream' has
+ *    finished.  The library never frees caller memory.
+ *  - 'stream' is a hipStream_t passed as void*; NULL is the null stream.
+ *  - Every call returns a tl_status.  All arguments are checked on the host
+ *    before anything is enqueued; on an error nothing is enqueued.  A fault
+ *    inside a kernel surfaces at the caller's next synchronisation.
+ *  - Calls are thread-safe.  The library owns, per (device, stream), a split-K
+ *    workspace and a fetch counter; concurrent calls on the SAME stream from
+ *    several host threads are serialised by the stream, as usual.
+ */
+#ifndef TL_H_
+#define TL_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TL_OK = 0,
+    TL_EINVAL = -1,        /* an argument violates the contract below */
+    TL_EUNSUPPORTED = -2,  /* valid, but no kernel implements this combination */
+    TL_EHIP = -3,          /* a HIP runtime call or a launch failed */
+    TL_ENOMEM = -4         /* the library could not allocate its workspace */
+} tl_status;
+
+/* Storage layout of a weight that is logically W[N][K]. */
+typedef enum {
+    TL_LAYOUT_NK_ROW = 0,  /* W[N][K] row-major: K contiguous (paper: column-major) */
+    TL_LAYOUT_KN_ROW = 1,  /* stored as [K][N] row-major: N contiguous (paper: row-major) */
+    TL_LAYOUT_TILE = 2     /* tile-major, the output of tl_repack(W, rows=N, cols=K) */
+} tl_layout_kind;
+
+typedef enum { TL_OUT_F32 = 0, TL_OUT_BF16 = 1 } tl_out_dtype;
+
+/* fetch_mode of tl_gemm. */
+enum {
+    TL_FETCH_NATIVE = 0,   /* load what the compute tile needs, 16 B per lane */
+    TL_FETCH_BLOCK = 1,    /* whenever a byte of an aligned G-byte block (aligned
+                              relative to the weight's base) is needed, load the
+                              whole block: emulates a large-granularity memory
+                              on HBM (Sections 2.2 and 2.5) */
+    TL_FETCH_COUNT = 0x100 /* OR-able: tally the weight bytes the kernel issues
+                              into this stream's fetch counter */
+};
+
+/* Layout descriptor: the memory-tile shape travels as a runtime argument, so
+ * one library binary serves every memory-tile shape (Sections 1 and 4.3). */
+typedef struct tl_layout_desc {
+    int32_t kind;        /* tl_layout_kind */
+    int32_t elem_bytes;  /* element size s in bytes; tl_gemm needs 2 (bf16) */
+    int64_t G;           /* TL_LAYOUT_TILE: memory-tile size in bytes (power of
+                            two).  *_ROW with TL_FETCH_BLOCK: the emulated fetch
+                            block.  Otherwise ignored. */
+    int32_t block_rows;  /* TL_LAYOUT_TILE: rows of W (along N) per memory tile,
+                            paper b, a power of two.  block_cols (paper a, along
+                            K) = G / (elem_bytes * block_rows). */
+    int32_t out_dtype;   /* tl_gemm: tl_out_dtype of C */
+    int32_t tile_m;      /* tl_gemm: requested compute tile, 0 = library's */
+    int32_t tile_n;      /*   choice; see tl_gemm_plan for what is accepted */
+    int32_t tile_k;
+    int32_t split_k;     /* tl_gemm: K-splits across workgroups, 0 = library's
+                            choice; partial sums are reduced in a fixed order,
+                            so results are bitwise reproducible */
+} tl_layout_desc;
+
+/* Read-amplification report (tl_read_amp). */
+typedef struct tl_amp {
+    int64_t compute_tiles;        /* (m-tile, n-tile, k-step) triples */
+    int64_t requests;             /* G-byte block fetches, summed over all of them */
+    int64_t fetched_bytes;        /* requests * G */
+    int64_t useful_bytes;         /* weight bytes the tiles need (ceil(M/tile_m) * N*K*s) */
+    int64_t unique_blocks;        /* distinct blocks touched by the whole GEMM */
+    int64_t min_blocks_per_tile;  /* fewest / most blocks one (n-tile, k-step) touches */
+    int64_t max_blocks_per_tile;
+    double amp;                   /* fetched_bytes / useful_bytes */
+} tl_amp;
+
+/* What tl_gemm will launch for given arguments (tl_gemm_plan). */
+typedef struct tl_plan {
+    int32_t kernel;      /* 1 = decode (skinny, M <= 64), 2 = prefill (MFMA tiles) */
+    int32_t tile_m;      /* compute tile used by the kernel; with tile_k it is  */
+    int32_t tile_n;      /* the tile to pass to tl_read_amp to account for the  */
+    int32_t tile_k;      /* kernel's fetches                                     */
+    int32_t split_k;     /* workgroups per output tile along K */
+    int32_t reserved;
+    int64_t workgroups;  /* grid size */
+    int64_t workspace_bytes;  /* split-K partials the call needs from the library */
+} tl_plan;
+
+/*
+ * tl_repack -- row-major -> tile-major (Eq. 2, Section 3.2).
+ *
+ * src: device, rows x cols elements of elem_bytes each, row-major (cols
+ *      contiguous).  For a GEMM weight rows = N and cols = K.
+ * dst: device, the same number of bytes, written in tile-major order: element
+ *      (r, c) goes to byte
+ *        ((r / br) * (cols / bc) + c / bc) * G + ((r % br) * bc + c % bc) * s
+ *      with br = block_rows, bc = G / (s * br), s = elem_bytes.  Memory tiles
+ *      follow one another along cols inside each strip of br rows.
+ * The copy moves bytes only (dtype-agnostic); weights are repacked once, when
+ * they are loaded (Section 5.1).
+ * Errors: TL_EINVAL unless elem_bytes in {1,2,4,8}; G and block_rows powers of
+ * two with elem_bytes * block_rows <= G; rows % br == 0; cols % bc == 0;
+ * src, dst non-NULL, 16-byte aligned, and not overlapping.  Empty matrices
+ * (rows == 0 or cols == 0) are a no-op.
+ */
+int tl_repack(const void* src, void* dst, int64_t rows, int64_t cols, int32_t elem_bytes,
+              int64_t G, int32_t block_rows, void* stream);
+
+/* tl_unpack -- the inverse permutation of tl_repack, same contract. */
+int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t elem_bytes,
+              int64_t G, int32_t block_rows, void* stream);
+
+/*
+ * tl_gemm -- C[M][N] = A[M][K] * W^T, fp32 accumulation (Section 2.3: a tiled
+ * GEMM whose workgroups iterate along K, loading a weight tile per step).
+ *
+ * A:   device bf16, row-major [M][K] (lda = K).  Activations are read from HBM
+ *      as usual; only the weight lives in the large-granularity layout
+ *      (Section 5.1).
+ * W:   device bf16 weight in the layout layout->kind describes.
+ * C:   device, row-major [M][N] (ldc = N), fp32 or bf16 (round to nearest
+ *      even) per layout->out_dtype.  C must not overlap A or W.
+ * fetch_mode: TL_FETCH_NATIVE or TL_FETCH_BLOCK, optionally | TL_FETCH_COUNT.
+ *      For TL_LAYOUT_TILE both modes load whole memory tiles (the compute tile
+ *      is a whole number of memory tiles).
+ * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound); larger M runs the
+ * prefill kernel (bf16 MFMA tiles 128x128x64 or 256x128x64, MFMA-bound).
+ * Errors: TL_EINVAL for M, N, K < 1, NULL or misaligned pointers, a bad
+ * descriptor (see tl_repack) or N % block_rows / K % block_cols != 0 for
+ * TL_LAYOUT_TILE; TL_EUNSUPPORTED for elem_bytes != 2, K % 64 != 0,
+ * N % 32 != 0, block_cols < 8, a TILE/BLOCK combination of layout, fetch mode
+ * and tile that no kernel implements, or TL_LAYOUT_KN_ROW.  TL_ENOMEM if the
+ * split-K workspace cannot be allocated; TL_EHIP if the launch fails.
+ */
+int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
+            const tl_layout_desc* layout, int32_t fetch_mode, void* stream);
+
+/* tl_gemm_plan -- host only: fill *out with what tl_gemm would launch for the
+ * same arguments (no device work).  Same error rules as tl_gemm. */
+int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout,
+                 int32_t fetch_mode, tl_plan* out);
+
+/*
+ * tl_read_amp -- host only, exact integer count of the bytes a tiled GEMM
+ * fetches at granularity G (Sections 1, 2.5; the per-tile request counts of
+ * Section 6.4).  Model: the grid has ceil(M/tile_m) x ceil(N/tile_n) tiles,
+ * each iterating ceil(K/tile_k) K-steps; at each step a tile fetches every
+ * G-byte block (aligned relative to the weight's base) holding at least one
+ * element of its weight sub-tile (clipped at the matrix edge); nothing is
+ * reused across tiles, steps or m-tiles; only the weight is counted
+ * (Section 5.1).  layout->kind, elem_bytes and, for TILE, layout->G and
+ * block_rows define byte offsets; G here is the memory system's granularity
+ * and may differ from layout->G.  Other descriptor fields are ignored.
+ * Errors: TL_EINVAL for non-positive sizes or tiles, G < 1, a bad TILE
+ * descriptor, or NULL pointers.
+ */
+int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
+                int32_t tile_k, const tl_layout_desc* layout, int64_t G, tl_amp* out);
+
+/* tl_fetch_counter_read -- synchronises 'stream', stores the weight bytes
+ * tallied by tl_gemm calls made on it with TL_FETCH_COUNT since the last read
+ * into *bytes, and resets the tally to zero.  Errors: TL_EINVAL for NULL
+ * bytes; TL_EHIP if a HIP call fails. */
+int tl_fetch_counter_read(void* stream, int64_t* bytes);
+
+/* tl_release -- frees every workspace and counter the library holds (all
+ * devices, all streams).  The caller must ensure no library work is still in
+ * flight.  Always TL_OK. */
+int tl_release(void);
+
+/* tl_strerror -- static, NUL-terminated description of a tl_status. */
+const char* tl_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TL_H_ */

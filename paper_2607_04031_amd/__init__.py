@@ -1,1 +1,244 @@
-"""Tile-major GEMM for MI355X (gfx950): binding over the libtl C ABI."""
+"""Tile-major GEMM for AMD MI355X (gfx950): Python binding over libtl's C ABI.
+
+Every step of the path runs in libtl's HIP kernels; this module only marshals
+arguments (torch tensors -> device pointers, the current torch stream -> a
+hipStream_t) and turns status codes into exceptions.  The entry points carry
+the C names and argument order of ``include/tl.h``:
+
+    tl_repack(src, dst, rows, cols, elem_bytes, G, block_rows, stream=None)
+    tl_unpack(src_tm, dst, rows, cols, elem_bytes, G, block_rows, stream=None)
+    tl_gemm(A, W, C, M, N, K, layout, fetch_mode, stream=None)
+    tl_gemm_plan(M, N, K, layout, fetch_mode) -> dict
+    tl_read_amp(M, N, K, tile_m, tile_n, tile_k, layout, G) -> dict
+    tl_fetch_counter_read(stream=None) -> int
+    tl_release()
+    tl_strerror(status) -> str
+
+Pointer arguments accept a torch CUDA tensor or a raw integer address.
+``layout`` is a :class:`LayoutDesc` (or a dict of its fields).  A few helpers
+(``repack``, ``gemm``, ``layout``) build outputs and descriptors for callers
+that just hold tensors.
+
+If libtl.so has not been built the first call raises ``ImportError``; there is
+no fallback path of any kind.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtl.so")
+
+TL_OK, TL_EINVAL, TL_EUNSUPPORTED, TL_EHIP, TL_ENOMEM = 0, -1, -2, -3, -4
+TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE = 0, 1, 2
+TL_OUT_F32, TL_OUT_BF16 = 0, 1
+TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
+
+EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_plan", "tl_read_amp",
+            "tl_fetch_counter_read", "tl_release", "tl_strerror")
+
+
+class LayoutDesc(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32),
+                ("elem_bytes", ctypes.c_int32),
+                ("G", ctypes.c_int64),
+                ("block_rows", ctypes.c_int32),
+                ("out_dtype", ctypes.c_int32),
+                ("tile_m", ctypes.c_int32),
+                ("tile_n", ctypes.c_int32),
+                ("tile_k", ctypes.c_int32),
+                ("split_k", ctypes.c_int32)]
+
+
+class Amp(ctypes.Structure):
+    _fields_ = [("compute_tiles", ctypes.c_int64),
+                ("requests", ctypes.c_int64),
+                ("fetched_bytes", ctypes.c_int64),
+                ("useful_bytes", ctypes.c_int64),
+                ("unique_blocks", ctypes.c_int64),
+                ("min_blocks_per_tile", ctypes.c_int64),
+                ("max_blocks_per_tile", ctypes.c_int64),
+                ("amp", ctypes.c_double)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32),
+                ("tile_m", ctypes.c_int32),
+                ("tile_n", ctypes.c_int32),
+                ("tile_k", ctypes.c_int32),
+                ("split_k", ctypes.c_int32),
+                ("reserved", ctypes.c_int32),
+                ("workgroups", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_int64)]
+
+
+def _struct_dict(s):
+    return {name: getattr(s, name) for name, _ in s._fields_ if name != "reserved"}
+
+
+class TLError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {tl_strerror(status)} ({status})")
+
+
+_lib = None
+
+
+def load_library():
+    """Load libtl.so (after torch, so both share torch's HIP runtime)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libtl.so is not built ({LIB_PATH}); run python -m paper_2607_04031_amd.build")
+    import torch  # noqa: F401  (binds libtl to torch's libamdhip64)
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, i64, p = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+    lib.tl_repack.restype = ctypes.c_int
+    lib.tl_repack.argtypes = [p, p, i64, i64, i32, i64, i32, p]
+    lib.tl_unpack.restype = ctypes.c_int
+    lib.tl_unpack.argtypes = [p, p, i64, i64, i32, i64, i32, p]
+    lib.tl_gemm.restype = ctypes.c_int
+    lib.tl_gemm.argtypes = [p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, p]
+    lib.tl_gemm_plan.restype = ctypes.c_int
+    lib.tl_gemm_plan.argtypes = [i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, ctypes.POINTER(Plan)]
+    lib.tl_read_amp.restype = ctypes.c_int
+    lib.tl_read_amp.argtypes = [i64, i64, i64, i32, i32, i32, ctypes.POINTER(LayoutDesc), i64,
+                                ctypes.POINTER(Amp)]
+    lib.tl_fetch_counter_read.restype = ctypes.c_int
+    lib.tl_fetch_counter_read.argtypes = [p, ctypes.POINTER(i64)]
+    lib.tl_release.restype = ctypes.c_int
+    lib.tl_release.argtypes = []
+    lib.tl_strerror.restype = ctypes.c_char_p
+    lib.tl_strerror.argtypes = [ctypes.c_int]
+    _lib = lib
+    return lib
+
+
+def _ptr(x) -> int | None:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        if not x.is_cuda:
+            raise ValueError("libtl needs device tensors")
+        if not x.is_contiguous():
+            raise ValueError("libtl needs contiguous tensors")
+        return x.data_ptr()
+    raise TypeError(f"cannot pass {type(x)!r} as a device pointer")
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _desc(layout) -> LayoutDesc:
+    if isinstance(layout, LayoutDesc):
+        return layout
+    d = LayoutDesc()
+    d.kind, d.elem_bytes, d.G, d.block_rows = TL_LAYOUT_TILE, 2, 4096, 32
+    for k, v in dict(layout).items():
+        setattr(d, k, v)
+    return d
+
+
+def _check(rc: int, where: str):
+    if rc != TL_OK:
+        raise TLError(rc, where)
+
+
+# ---------------------------------------------------------------------------
+# C ABI, same names and argument order
+# ---------------------------------------------------------------------------
+
+def tl_repack(src, dst, rows, cols, elem_bytes, G, block_rows, stream=None):
+    _check(load_library().tl_repack(_ptr(src), _ptr(dst), rows, cols, elem_bytes, G, block_rows,
+                                    _stream(stream)), "tl_repack")
+
+
+def tl_unpack(src_tm, dst, rows, cols, elem_bytes, G, block_rows, stream=None):
+    _check(load_library().tl_unpack(_ptr(src_tm), _ptr(dst), rows, cols, elem_bytes, G, block_rows,
+                                    _stream(stream)), "tl_unpack")
+
+
+def tl_gemm(A, W, C, M, N, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):
+    d = _desc(layout)
+    _check(load_library().tl_gemm(_ptr(A), _ptr(W), _ptr(C), M, N, K, ctypes.byref(d), fetch_mode,
+                                  _stream(stream)), "tl_gemm")
+
+
+def tl_gemm_plan(M, N, K, layout, fetch_mode=TL_FETCH_BLOCK) -> dict:
+    d = _desc(layout)
+    out = Plan()
+    _check(load_library().tl_gemm_plan(M, N, K, ctypes.byref(d), fetch_mode, ctypes.byref(out)),
+           "tl_gemm_plan")
+    return _struct_dict(out)
+
+
+def tl_read_amp(M, N, K, tile_m, tile_n, tile_k, layout, G) -> dict:
+    d = _desc(layout)
+    out = Amp()
+    _check(load_library().tl_read_amp(M, N, K, tile_m, tile_n, tile_k, ctypes.byref(d), G,
+                                      ctypes.byref(out)), "tl_read_amp")
+    return _struct_dict(out)
+
+
+def tl_fetch_counter_read(stream=None) -> int:
+    v = ctypes.c_int64(0)
+    _check(load_library().tl_fetch_counter_read(_stream(stream), ctypes.byref(v)),
+           "tl_fetch_counter_read")
+    return v.value
+
+
+def tl_release():
+    _check(load_library().tl_release(), "tl_release")
+
+
+def tl_strerror(status: int) -> str:
+    return load_library().tl_strerror(status).decode()
+
+
+# ---------------------------------------------------------------------------
+# Tensor helpers (allocation + the calls above)
+# ---------------------------------------------------------------------------
+
+def layout(kind=TL_LAYOUT_TILE, G=4096, block_rows=32, out_dtype=TL_OUT_F32, elem_bytes=2,
+           tile_m=0, tile_n=0, tile_k=0, split_k=0) -> LayoutDesc:
+    return _desc(dict(kind=kind, G=G, block_rows=block_rows, out_dtype=out_dtype,
+                      elem_bytes=elem_bytes, tile_m=tile_m, tile_n=tile_n, tile_k=tile_k,
+                      split_k=split_k))
+
+
+def repack(w, G=4096, block_rows=32, out=None, stream=None):
+    """Tile-major copy of a 2-D device tensor (same dtype and shape)."""
+    import torch
+    out = torch.empty_like(w) if out is None else out
+    rows, cols = w.shape
+    tl_repack(w, out, rows, cols, w.element_size(), G, block_rows, stream)
+    return out
+
+
+def unpack(w_tm, G=4096, block_rows=32, out=None, stream=None):
+    import torch
+    out = torch.empty_like(w_tm) if out is None else out
+    rows, cols = w_tm.shape
+    tl_unpack(w_tm, out, rows, cols, w_tm.element_size(), G, block_rows, stream)
+    return out
+
+
+def gemm(A, W, N, desc: LayoutDesc, fetch_mode=TL_FETCH_BLOCK, out=None, stream=None):
+    """C = A @ W^T for bf16 A [M, K] and a bf16 weight of logical shape [N, K]."""
+    import torch
+    M, K = A.shape
+    dt = torch.bfloat16 if desc.out_dtype == TL_OUT_BF16 else torch.float32
+    C = torch.empty((M, N), dtype=dt, device=A.device) if out is None else out
+    tl_gemm(A, W, C, M, N, K, desc, fetch_mode, stream)
+    return C

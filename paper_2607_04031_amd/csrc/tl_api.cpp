@@ -1,0 +1,337 @@
+// libtl C ABI: argument validation, kernel planning, per-(device, stream)
+// library state, dispatch.  Nothing is enqueued unless every check passes.
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "tl_internal.h"
+
+namespace tl {
+
+int make_tile_layout(int64_t s, int64_t G, int64_t br, Layout* out) {
+    if (!(s == 1 || s == 2 || s == 4 || s == 8)) return TL_EINVAL;
+    if (!is_pow2(G) || !is_pow2(br)) return TL_EINVAL;
+    if (s * br > G) return TL_EINVAL;
+    if (G > (int64_t(1) << 30)) return TL_EINVAL;
+    Layout L;
+    L.kind = TL_LAYOUT_TILE;
+    L.s = s;
+    L.G = G;
+    L.br = br;
+    L.bc = G / (s * br);
+    L.log2_br = ilog2(br);
+    L.log2_bc = ilog2(L.bc);
+    L.log2_G = ilog2(G);
+    *out = L;
+    return TL_OK;
+}
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Library state: split-K workspace, tile counters and the fetch tally, one set
+// per (device, stream).
+// ---------------------------------------------------------------------------
+struct StreamState {
+    float* ws = nullptr;
+    size_t ws_bytes = 0;
+    int* counters = nullptr;
+    size_t n_counters = 0;
+    unsigned long long* fetch = nullptr;
+};
+
+std::mutex g_mu;
+std::map<std::pair<int, void*>, StreamState> g_state;
+
+int current_device(int* dev) {
+    return hipGetDevice(dev) == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+// Returns the state for (current device, stream), growing its buffers.  New
+// counters and the tally are cleared on 'stream' so the clear is ordered
+// before any kernel that uses them.
+int get_state(hipStream_t stream, size_t ws_bytes, size_t n_counters, StreamState** out) {
+    int dev = 0;
+    if (current_device(&dev) != TL_OK) return TL_EHIP;
+    std::lock_guard<std::mutex> lock(g_mu);
+    StreamState& st = g_state[{dev, (void*)stream}];
+    if (!st.fetch) {
+        if (hipMalloc(&st.fetch, sizeof(unsigned long long)) != hipSuccess) { st.fetch = nullptr; return TL_ENOMEM; }
+        if (hipMemsetAsync(st.fetch, 0, sizeof(unsigned long long), stream) != hipSuccess) return TL_EHIP;
+    }
+    if (ws_bytes > st.ws_bytes) {
+        if (st.ws) {
+            // the old buffer may still be read by work in flight on this stream
+            if (hipStreamSynchronize(stream) != hipSuccess) return TL_EHIP;
+            (void)hipFree(st.ws);
+            st.ws = nullptr;
+            st.ws_bytes = 0;
+        }
+        size_t bytes = std::max<size_t>(ws_bytes, size_t(1) << 20);
+        if (hipMalloc(&st.ws, bytes) != hipSuccess) { st.ws = nullptr; return TL_ENOMEM; }
+        st.ws_bytes = bytes;
+    }
+    if (n_counters > st.n_counters) {
+        if (st.counters) {
+            if (hipStreamSynchronize(stream) != hipSuccess) return TL_EHIP;
+            (void)hipFree(st.counters);
+            st.counters = nullptr;
+            st.n_counters = 0;
+        }
+        size_t n = std::max<size_t>(n_counters, 4096);
+        if (hipMalloc(&st.counters, n * sizeof(int)) != hipSuccess) { st.counters = nullptr; return TL_ENOMEM; }
+        if (hipMemsetAsync(st.counters, 0, n * sizeof(int), stream) != hipSuccess) return TL_EHIP;
+        st.n_counters = n;
+    }
+    *out = &st;
+    return TL_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlap(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
+    auto x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + uintptr_t(b_bytes) && y < x + uintptr_t(a_bytes);
+}
+
+int check_repack_args(const void* src, const void* dst, int64_t rows, int64_t cols, int32_t s,
+                      int64_t G, int32_t br, Layout* L) {
+    if (rows < 0 || cols < 0) return TL_EINVAL;
+    if (make_tile_layout(s, G, br, L) != TL_OK) return TL_EINVAL;
+    if (rows % L->br || cols % L->bc) return TL_EINVAL;
+    if (rows == 0 || cols == 0) return TL_OK;
+    if (!src || !dst || !aligned16(src) || !aligned16(dst)) return TL_EINVAL;
+    if (rows > (int64_t(1) << 40) / std::max<int64_t>(cols, 1)) return TL_EINVAL;
+    const int64_t bytes = rows * cols * s;
+    if (overlap(src, bytes, dst, bytes)) return TL_EINVAL;
+    return TL_OK;
+}
+
+int do_repack(const void* src, void* dst, int64_t rows, int64_t cols, int32_t s, int64_t G,
+              int32_t br, void* stream, bool inverse) {
+    Layout L;
+    int rc = check_repack_args(src, dst, rows, cols, s, G, br, &L);
+    if (rc != TL_OK) return rc;
+    if (rows == 0 || cols == 0) return TL_OK;
+    if ((rows * cols * s) / L.G >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;  // 32-bit block index
+    hipError_t e = launch_repack(src, dst, rows, cols, L, inverse, (hipStream_t)stream);
+    return e == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+// ---------------------------------------------------------------------------
+// GEMM planning
+// ---------------------------------------------------------------------------
+struct Plan {
+    tl_plan pub;
+    Layout L;
+    bool out_bf16 = false;
+    bool count = false;
+    int m_tiles16 = 1;
+    int64_t k_unit = 64;
+    int64_t n_counters = 0;
+};
+
+constexpr int kDecodeMaxM = 64;
+constexpr int kTargetWorkgroups = 1024;   // 4 per CU on 256 CUs
+
+int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t fetch_mode,
+              Plan* P) {
+    if (!d) return TL_EINVAL;
+    if (M < 1 || N < 1 || K < 1) return TL_EINVAL;
+    if (fetch_mode & ~(TL_FETCH_BLOCK | TL_FETCH_COUNT)) return TL_EINVAL;
+    if (d->out_dtype != TL_OUT_F32 && d->out_dtype != TL_OUT_BF16) return TL_EINVAL;
+    if (d->tile_m < 0 || d->tile_n < 0 || d->tile_k < 0 || d->split_k < 0) return TL_EINVAL;
+    if (d->kind != TL_LAYOUT_NK_ROW && d->kind != TL_LAYOUT_KN_ROW && d->kind != TL_LAYOUT_TILE)
+        return TL_EINVAL;
+    if (d->elem_bytes != 2) return d->elem_bytes < 1 ? TL_EINVAL : TL_EUNSUPPORTED;
+    if (M > (int64_t(1) << 31) || N > (int64_t(1) << 31) || K > (int64_t(1) << 31)) return TL_EINVAL;
+
+    Plan p;
+    std::memset(&p.pub, 0, sizeof p.pub);
+    p.out_bf16 = d->out_dtype == TL_OUT_BF16;
+    p.count = (fetch_mode & TL_FETCH_COUNT) != 0;
+    const bool block = (fetch_mode & TL_FETCH_BLOCK) != 0;
+
+    if (d->kind == TL_LAYOUT_TILE) {
+        if (make_tile_layout(2, d->G, d->block_rows, &p.L) != TL_OK) return TL_EINVAL;
+        if (N % p.L.br || K % p.L.bc) return TL_EINVAL;
+        if (p.L.bc < 8) return TL_EUNSUPPORTED;
+    } else if (d->kind == TL_LAYOUT_NK_ROW) {
+        p.L.kind = TL_LAYOUT_NK_ROW;
+        if (block) return TL_EUNSUPPORTED;
+    } else {
+        return TL_EUNSUPPORTED;
+    }
+    if (K % 64 || N % 32) return TL_EUNSUPPORTED;
+
+    const bool tile = d->kind == TL_LAYOUT_TILE;
+    p.k_unit = tile ? std::max<int64_t>(64, p.L.bc) : 64;
+
+    if (M <= kDecodeMaxM && d->tile_m <= 64) {
+        p.pub.kernel = 1;
+        p.m_tiles16 = int((M + 15) / 16);
+        if (p.m_tiles16 == 3) p.m_tiles16 = 4;
+        int tn = d->tile_n ? d->tile_n : int(tile ? std::max<int64_t>(32, p.L.br) : 32);
+        if (tn != 32 && tn != 64) return TL_EUNSUPPORTED;
+        if (tile && tn % p.L.br) return TL_EUNSUPPORTED;
+        if (N % tn) return TL_EUNSUPPORTED;
+        if (d->tile_k && (d->tile_k != p.k_unit)) return TL_EUNSUPPORTED;
+        const int64_t n_tiles = N / tn;
+        const int64_t units = K / p.k_unit;
+        int64_t S = d->split_k;
+        if (S == 0) {
+            const int64_t min_units = std::max<int64_t>(1, 1024 / p.k_unit);  // >= 1024 K per split
+            S = (kTargetWorkgroups + n_tiles - 1) / n_tiles;
+            S = std::max<int64_t>(1, std::min<int64_t>(S, units / min_units));
+        }
+        if (S < 1 || S > units || S > 4096) return TL_EUNSUPPORTED;
+        p.pub.tile_m = 16 * p.m_tiles16;
+        p.pub.tile_n = tn;
+        p.pub.tile_k = int(p.k_unit);
+        p.pub.split_k = int(S);
+        p.pub.workgroups = n_tiles * S;
+        p.pub.workspace_bytes = S > 1 ? S * M * N * 4 : 0;
+        p.n_counters = S > 1 ? n_tiles : 0;
+    } else {
+        p.pub.kernel = 2;
+        int tm = d->tile_m ? d->tile_m : (M >= 1024 ? 256 : 128);
+        if (tm != 128 && tm != 256) return TL_EUNSUPPORTED;
+        int tn = d->tile_n ? d->tile_n : 128;
+        if (tn != 128) return TL_EUNSUPPORTED;
+        if (tile && tn % p.L.br) return TL_EUNSUPPORTED;
+        if (d->tile_k && d->tile_k != p.k_unit) return TL_EUNSUPPORTED;
+        if (d->split_k > 1) return TL_EUNSUPPORTED;
+        p.pub.tile_m = tm;
+        p.pub.tile_n = tn;
+        p.pub.tile_k = int(p.k_unit);
+        p.pub.split_k = 1;
+        p.pub.workgroups = ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
+        p.pub.workspace_bytes = 0;
+    }
+    *P = p;
+    return TL_OK;
+}
+
+}  // namespace
+}  // namespace tl
+
+using namespace tl;
+
+extern "C" {
+
+int tl_repack(const void* src, void* dst, int64_t rows, int64_t cols, int32_t elem_bytes,
+              int64_t G, int32_t block_rows, void* stream) {
+    return do_repack(src, dst, rows, cols, elem_bytes, G, block_rows, stream, false);
+}
+
+int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t elem_bytes,
+              int64_t G, int32_t block_rows, void* stream) {
+    return do_repack(src_tm, dst, rows, cols, elem_bytes, G, block_rows, stream, true);
+}
+
+int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout, int32_t fetch_mode,
+                 tl_plan* out) {
+    if (!out) return TL_EINVAL;
+    Plan p;
+    int rc = plan_gemm(M, N, K, layout, fetch_mode, &p);
+    if (rc != TL_OK) return rc;
+    *out = p.pub;
+    return TL_OK;
+}
+
+int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
+            const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
+    Plan p;
+    int rc = plan_gemm(M, N, K, layout, fetch_mode, &p);
+    if (rc != TL_OK) return rc;
+    if (!A || !W || !C || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
+    const int64_t c_bytes = M * N * (p.out_bf16 ? 2 : 4);
+    if (overlap(C, c_bytes, A, M * K * 2) || overlap(C, c_bytes, W, N * K * 2)) return TL_EINVAL;
+
+    hipStream_t s = (hipStream_t)stream;
+    StreamState* st = nullptr;
+    rc = get_state(s, size_t(p.pub.workspace_bytes), size_t(p.n_counters), &st);
+    if (rc != TL_OK) return rc;
+
+    hipError_t e;
+    if (p.pub.kernel == 1) {
+        DecodeLaunch d;
+        d.A = static_cast<const uint16_t*>(A);
+        d.W = static_cast<const uint8_t*>(W);
+        d.C = C;
+        d.ws = st->ws;
+        d.counters = st->counters;
+        d.fetch = p.count ? st->fetch : nullptr;
+        d.M = M;
+        d.N = N;
+        d.K = K;
+        d.L = p.L;
+        d.tile_n = p.pub.tile_n;
+        d.m_tiles16 = p.m_tiles16;
+        d.split_k = p.pub.split_k;
+        d.k_unit = p.k_unit;
+        d.out_bf16 = p.out_bf16;
+        e = launch_decode(d, s);
+    } else {
+        PrefillLaunch q;
+        q.A = static_cast<const uint16_t*>(A);
+        q.W = static_cast<const uint8_t*>(W);
+        q.C = C;
+        q.fetch = p.count ? st->fetch : nullptr;
+        q.M = M;
+        q.N = N;
+        q.K = K;
+        q.L = p.L;
+        q.tile_m = p.pub.tile_m;
+        q.out_bf16 = p.out_bf16;
+        e = launch_prefill(q, s);
+    }
+    return e == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+int tl_fetch_counter_read(void* stream, int64_t* bytes) {
+    if (!bytes) return TL_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    StreamState* st = nullptr;
+    int rc = get_state(s, 0, 0, &st);
+    if (rc != TL_OK) return rc;
+    unsigned long long v = 0;
+    if (hipStreamSynchronize(s) != hipSuccess) return TL_EHIP;
+    if (hipMemcpy(&v, st->fetch, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return TL_EHIP;
+    if (hipMemsetAsync(st->fetch, 0, sizeof v, s) != hipSuccess) return TL_EHIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return TL_EHIP;
+    *bytes = int64_t(v);
+    return TL_OK;
+}
+
+int tl_release(void) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    int dev0 = 0;
+    (void)hipGetDevice(&dev0);
+    for (auto& kv : g_state) {
+        (void)hipSetDevice(kv.first.first);
+        if (kv.second.ws) (void)hipFree(kv.second.ws);
+        if (kv.second.counters) (void)hipFree(kv.second.counters);
+        if (kv.second.fetch) (void)hipFree(kv.second.fetch);
+    }
+    g_state.clear();
+    (void)hipSetDevice(dev0);
+    return TL_OK;
+}
+
+const char* tl_strerror(int status) {
+    switch (status) {
+        case TL_OK: return "TL_OK: success";
+        case TL_EINVAL: return "TL_EINVAL: invalid argument";
+        case TL_EUNSUPPORTED: return "TL_EUNSUPPORTED: no kernel implements this combination";
+        case TL_EHIP: return "TL_EHIP: HIP runtime or launch failure";
+        case TL_ENOMEM: return "TL_ENOMEM: workspace allocation failed";
+        default: return "unknown tl_status";
+    }
+}
+
+}  // extern "C"

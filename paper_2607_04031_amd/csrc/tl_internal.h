@@ -1,0 +1,74 @@
+// Internal declarations shared by the libtl translation units (host side).
+#pragma once
+
+#include <cstdint>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/tl.h"
+
+namespace tl {
+
+inline bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+inline int ilog2(int64_t x) {
+    int r = 0;
+    while ((int64_t(1) << r) < x) ++r;
+    return r;
+}
+
+// A validated tile-major (or linear) weight layout with the shift amounts the
+// kernels use in place of Eq. 1's divisions (Section 3.2: a and b are powers
+// of two, so the tile indices are shifts and masks).
+struct Layout {
+    int kind = TL_LAYOUT_TILE;
+    int64_t s = 2;        // element bytes
+    int64_t G = 4096;     // memory-tile bytes
+    int64_t br = 32;      // paper b (rows along N)
+    int64_t bc = 64;      // paper a (elements along K)
+    int log2_br = 5, log2_bc = 6, log2_G = 12;
+};
+
+// Checks a tile-major description; fills 'out' on success.
+int make_tile_layout(int64_t s, int64_t G, int64_t br, Layout* out);
+
+// ---------------------------------------------------------------------------
+// Kernel launchers (defined in the .hip files).  Arguments are validated by
+// the callers; these only enqueue.
+// ---------------------------------------------------------------------------
+
+hipError_t launch_repack(const void* src, void* dst, int64_t rows, int64_t cols,
+                         const Layout& L, bool inverse, hipStream_t stream);
+
+struct DecodeLaunch {
+    const uint16_t* A;
+    const uint8_t* W;
+    void* C;
+    float* ws;                  // [split_k][M][N] partials (split_k > 1)
+    int* counters;              // one per n-tile, zero on entry, left zero on exit
+    unsigned long long* fetch;  // fetch tally (TL_FETCH_COUNT) or nullptr
+    int64_t M, N, K;
+    Layout L;
+    int tile_n;                 // 32 or 64
+    int m_tiles16;              // ceil(M / 16): 1, 2 or 4
+    int split_k;
+    int64_t k_unit;             // K granularity of a split, in elements
+    bool out_bf16;
+};
+
+hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream);
+
+struct PrefillLaunch {
+    const uint16_t* A;
+    const uint8_t* W;
+    void* C;
+    unsigned long long* fetch;
+    int64_t M, N, K;
+    Layout L;
+    int tile_m;                 // 128 or 256
+    bool out_bf16;
+};
+
+hipError_t launch_prefill(const PrefillLaunch& p, hipStream_t stream);
+
+}  // namespace tl

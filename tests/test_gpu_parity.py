@@ -1,0 +1,340 @@
+"""GPU parity: libtl's HIP kernels, called through the C ABI, against the CPU
+oracle on the same seeded inputs.  Repack and amplification counts must be
+bit-exact; GEMMs meet relative L2 <= 1e-3 and max abs <= 5e-3 * max|y_ref|,
+and are bit-exact where the exact result is representable (one-hot and
+small-integer inputs)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_04031_amd as tl
+from paper_2607_04031_amd import synth
+from tests._gpu import banner, dev_bf16, dev_u8, host_bits, host_f32, parity, parity_bf16_out
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+    assert torch.cuda.is_available()
+    tl.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------------------
+# Repack
+# ---------------------------------------------------------------------------
+
+REPACK_SMALL = [
+    # rows, cols, elem_bytes, G, block_rows
+    (1024, 1024, 2, 4096, 32),       # tiny config
+    (256, 2048, 2, 512, 8), (256, 2048, 2, 512, 16), (256, 2048, 2, 512, 32), (256, 2048, 2, 512, 64),
+    (256, 2048, 2, 1024, 8), (256, 2048, 2, 1024, 64),
+    (256, 2048, 2, 4096, 8), (256, 2048, 2, 4096, 16), (256, 2048, 2, 4096, 64),
+    (256, 2048, 2, 16384, 8), (256, 2048, 2, 16384, 16), (256, 2048, 2, 16384, 32), (256, 2048, 2, 16384, 64),
+    (192, 768, 1, 4096, 64),         # FP8-sized elements, 64 x 64 memory tile
+    (64, 4096, 4, 4096, 8),
+    (32, 64, 2, 4096, 32),           # a single memory tile
+]
+
+
+@pytest.mark.parametrize("rows,cols,s,G,br", REPACK_SMALL)
+def test_repack_bit_exact_small(rows, cols, s, G, br):
+    banner(f"repack rows={rows} cols={cols} s={s} G={G} br={br}")
+    src = synth.random_bytes(rows * cols * s, seed=rows * 7 + cols + G + br).reshape(rows, cols * s)
+    want = oracle.repack(src.view({1: np.uint8, 2: np.uint16, 4: np.uint32}[s]).reshape(rows, cols),
+                         G, br).view(np.uint8).reshape(rows, cols * s)
+    d_src = dev_u8(src)
+    d_dst = dev_u8(np.zeros_like(src))
+    tl.tl_repack(d_src, d_dst, rows, cols, s, G, br)
+    got = host_bits(d_dst)
+    assert np.array_equal(got, want)
+    d_back = dev_u8(np.zeros_like(src))
+    tl.tl_unpack(d_dst, d_back, rows, cols, s, G, br)
+    assert np.array_equal(host_bits(d_back), src)
+
+
+@pytest.mark.parametrize("name,N,K", synth.LLAMA70B)
+def test_repack_full_size_llama(name, N, K):
+    """Full Llama-70B weight shapes: exact round trip, plus 4096 sampled
+    elements placed where the oracle's Eq. 2 offset says."""
+    import torch
+    banner(f"repack full {name} [{N},{K}]")
+    W = torch.randint(-32768, 32767, (N, K), dtype=torch.int16, device="cuda",
+                      generator=torch.Generator(device="cuda").manual_seed(5))
+    Wt = torch.empty_like(W)
+    tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
+    back = torch.empty_like(W)
+    tl.tl_unpack(Wt, back, N, K, 2, 4096, 32)
+    assert torch.equal(back, W)
+    rng = np.random.default_rng(1)
+    rs = rng.integers(0, N, 4096)
+    cs = rng.integers(0, K, 4096)
+    offs = np.array([oracle.tm_offset(int(r), int(c), K, 2, 4096, 32) // 2 for r, c in zip(rs, cs)])
+    flat = Wt.view(-1)
+    got = flat[torch.from_numpy(offs).cuda()].cpu().numpy()
+    want = W[torch.from_numpy(rs).cuda(), torch.from_numpy(cs).cuda()].cpu().numpy()
+    assert np.array_equal(got, want)
+
+
+# ---------------------------------------------------------------------------
+# GEMM helpers
+# ---------------------------------------------------------------------------
+
+def run_gemm(A_bits, W_bits, desc, fetch=tl.TL_FETCH_BLOCK, tile_major=True):
+    """Upload, (repack), run tl_gemm; returns the output tensor."""
+    import torch
+    M, K = A_bits.shape
+    N = W_bits.shape[0]
+    A = dev_bf16(A_bits)
+    W = dev_bf16(W_bits)
+    if tile_major:
+        Wt = torch.empty_like(W)
+        tl.tl_repack(W, Wt, N, K, 2, desc.G, desc.block_rows)
+        W = Wt
+    out_dt = torch.bfloat16 if desc.out_dtype == tl.TL_OUT_BF16 else torch.float32
+    C = torch.full((M, N), float("nan"), dtype=out_dt, device="cuda")
+    tl.tl_gemm(A, W, C, M, N, K, desc, fetch)
+    _sync()
+    return C
+
+
+DECODE_SHAPES = [
+    # M, N, K
+    (16, 1024, 1024),     # tiny config
+    (1, 1024, 1024), (5, 512, 2048), (8, 1024, 1024), (17, 256, 1024), (32, 512, 1024),
+    (33, 256, 512), (48, 128, 4096), (64, 256, 1024),
+]
+
+
+@pytest.mark.parametrize("M,N,K", DECODE_SHAPES)
+def test_decode_tile_major_parity(M, N, K):
+    banner(f"decode tile-major M={M} N={N} K={K}")
+    A = synth.normal_bf16((M, K), seed=1 + M)
+    W = synth.normal_bf16((N, K), seed=2 + N, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    C = run_gemm(A, W, tl.layout())
+    parity(host_f32(C), y_ref, f"decode M={M}")
+
+
+@pytest.mark.parametrize("split_k", [1, 2, 3, 7, 16])
+def test_decode_split_k_parity_and_reproducible(split_k):
+    M, N, K = 8, 512, 4096
+    banner(f"decode split_k={split_k}")
+    A = synth.normal_bf16((M, K), seed=3)
+    W = synth.normal_bf16((N, K), seed=4, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    d = tl.layout(split_k=split_k)
+    C1 = host_f32(run_gemm(A, W, d))
+    C2 = host_f32(run_gemm(A, W, d))
+    parity(C1, y_ref, f"split_k={split_k}")
+    assert np.array_equal(C1, C2)    # fixed-order reduction: bitwise reproducible
+
+
+@pytest.mark.parametrize("M", [1, 8, 32, 64])
+def test_decode_one_hot_exact(M):
+    """A[m] = e_{k_m}: every output is one weight element, exact in any order."""
+    K, N = 2048, 512
+    banner(f"decode one-hot M={M}")
+    A, ks = synth.one_hot_bf16(M, K, seed=M)
+    W = synth.normal_bf16((N, K), seed=9, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    for split_k in (1, 4):
+        C = host_f32(run_gemm(A, W, tl.layout(split_k=split_k)))
+        assert np.array_equal(C.astype(np.float64), y_ref)
+
+
+@pytest.mark.parametrize("split_k", [1, 5])
+def test_decode_small_integers_exact(split_k):
+    """Integers in [-4, 4]: every partial sum is an exact fp32 integer."""
+    M, N, K = 24, 256, 4096
+    banner(f"decode small-int split_k={split_k}")
+    A = synth.small_int_bf16((M, K), seed=5)
+    W = synth.small_int_bf16((N, K), seed=6)
+    y_ref = oracle.gemm_f64(A, W)
+    C = host_f32(run_gemm(A, W, tl.layout(split_k=split_k)))
+    assert np.array_equal(C.astype(np.float64), y_ref)
+
+
+def test_decode_zero_weight():
+    banner("decode zero weight")
+    A = synth.normal_bf16((8, 1024), seed=7)
+    W = np.zeros((256, 1024), dtype=np.uint16)
+    C = host_f32(run_gemm(A, W, tl.layout(split_k=2)))
+    assert np.all(C == 0.0)
+
+
+@pytest.mark.parametrize("M", [1, 8, 32])
+def test_decode_bf16_output(M):
+    N, K = 1024, 2048
+    banner(f"decode bf16-out M={M}")
+    A = synth.normal_bf16((M, K), seed=11)
+    W = synth.normal_bf16((N, K), seed=12, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    for split_k in (1, 4):
+        C = run_gemm(A, W, tl.layout(out_dtype=tl.TL_OUT_BF16, split_k=split_k))
+        parity_bf16_out(host_bits(C), y_ref, f"bf16 M={M}")
+
+
+@pytest.mark.parametrize("G", [512, 1024, 4096, 16384])
+@pytest.mark.parametrize("br", [8, 16, 32, 64])
+def test_decode_memory_tile_shapes(G, br):
+    """One library binary for every memory-tile shape (runtime descriptor)."""
+    if G // (2 * br) < 8:
+        pytest.skip("block_cols < 8 is rejected by tl_gemm (TL_EUNSUPPORTED)")
+    M, N, K = 8, 256, 4096
+    banner(f"decode G={G} br={br}")
+    A = synth.normal_bf16((M, K), seed=13)
+    W = synth.normal_bf16((N, K), seed=14, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    C = host_f32(run_gemm(A, W, tl.layout(G=G, block_rows=br)))
+    parity(C, y_ref, f"G={G} br={br}")
+
+
+@pytest.mark.parametrize("M", [1, 8, 32])
+def test_decode_row_major_native(M):
+    N, K = 1024, 2048
+    banner(f"decode NK_ROW native M={M}")
+    A = synth.normal_bf16((M, K), seed=15)
+    W = synth.normal_bf16((N, K), seed=16, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    C = host_f32(run_gemm(A, W, tl.layout(kind=tl.TL_LAYOUT_NK_ROW), fetch=tl.TL_FETCH_NATIVE,
+                          tile_major=False))
+    parity(C, y_ref, f"NK_ROW M={M}")
+
+
+def test_decode_fetch_counter_equals_read_amp():
+    """TL_FETCH_COUNT tally == tl_read_amp fetched bytes for the plan's tile."""
+    M, N, K = 8, 1024, 2048
+    banner("decode fetch counter")
+    A = synth.normal_bf16((M, K), seed=17)
+    W = synth.normal_bf16((N, K), seed=18, sigma=synth.W_SIGMA)
+    d = tl.layout()
+    tl.tl_fetch_counter_read()   # reset
+    run_gemm(A, W, d, fetch=tl.TL_FETCH_BLOCK | tl.TL_FETCH_COUNT)
+    got = tl.tl_fetch_counter_read()
+    p = tl.tl_gemm_plan(M, N, K, d, tl.TL_FETCH_BLOCK)
+    amp = tl.tl_read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, 4096)
+    assert got == amp["fetched_bytes"] == N * K * 2
+
+
+# ---------------------------------------------------------------------------
+# Prefill
+# ---------------------------------------------------------------------------
+
+PREFILL_SHAPES = [
+    # M, N, K, tile_m
+    (256, 1024, 1024, 128), (256, 1024, 1024, 256),
+    (300, 512, 2048, 128), (300, 512, 2048, 256),    # ragged M tail
+    (65, 256, 512, 128),                              # just above the decode limit
+    (512, 1056, 512, 256),                            # ragged N tail (N % 128 = 32)
+]
+
+
+@pytest.mark.parametrize("M,N,K,tm", PREFILL_SHAPES)
+def test_prefill_tile_major_parity(M, N, K, tm):
+    banner(f"prefill M={M} N={N} K={K} tile_m={tm}")
+    A = synth.normal_bf16((M, K), seed=21)
+    W = synth.normal_bf16((N, K), seed=22, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    C = host_f32(run_gemm(A, W, tl.layout(tile_m=tm)))
+    parity(C, y_ref, f"prefill tm={tm}")
+    Cb = run_gemm(A, W, tl.layout(tile_m=tm, out_dtype=tl.TL_OUT_BF16))
+    parity_bf16_out(host_bits(Cb), y_ref, "prefill bf16")
+
+
+def test_prefill_exact_inputs():
+    M, N, K = 256, 256, 1024
+    banner("prefill one-hot / small-int")
+    A, _ = synth.one_hot_bf16(M, K, seed=23)
+    W = synth.normal_bf16((N, K), seed=24, sigma=synth.W_SIGMA)
+    assert np.array_equal(host_f32(run_gemm(A, W, tl.layout(tile_m=128))).astype(np.float64),
+                          oracle.gemm_f64(A, W))
+    A = synth.small_int_bf16((M, K), seed=25)
+    W = synth.small_int_bf16((N, K), seed=26)
+    assert np.array_equal(host_f32(run_gemm(A, W, tl.layout(tile_m=256))).astype(np.float64),
+                          oracle.gemm_f64(A, W))
+
+
+@pytest.mark.parametrize("G,br", [(4096, 8), (16384, 32), (1024, 16), (512, 32)])
+def test_prefill_memory_tile_shapes(G, br):
+    M, N, K = 256, 256, 2048
+    banner(f"prefill G={G} br={br}")
+    A = synth.normal_bf16((M, K), seed=27)
+    W = synth.normal_bf16((N, K), seed=28, sigma=synth.W_SIGMA)
+    parity(host_f32(run_gemm(A, W, tl.layout(G=G, block_rows=br))), oracle.gemm_f64(A, W),
+           f"prefill G={G} br={br}")
+
+
+def test_prefill_row_major_native():
+    M, N, K = 256, 512, 1024
+    banner("prefill NK_ROW")
+    A = synth.normal_bf16((M, K), seed=29)
+    W = synth.normal_bf16((N, K), seed=30, sigma=synth.W_SIGMA)
+    C = host_f32(run_gemm(A, W, tl.layout(kind=tl.TL_LAYOUT_NK_ROW), fetch=tl.TL_FETCH_NATIVE,
+                          tile_major=False))
+    parity(C, oracle.gemm_f64(A, W), "prefill NK_ROW")
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, sampled outputs
+# ---------------------------------------------------------------------------
+
+def _sampled_check(A_bits, W_bits, C, n_samples, seed, bf16_out=False):
+    M, N = C.shape
+    rng = np.random.default_rng(seed)
+    ms = rng.integers(0, M, n_samples)
+    ns = rng.integers(0, N, n_samples)
+    y_ref = oracle.gemm_f64_points(A_bits, W_bits, ms, ns)
+    import torch
+    got = C[torch.from_numpy(ms).cuda(), torch.from_numpy(ns).cuda()]
+    if bf16_out:
+        parity_bf16_out(host_bits(got), y_ref, "sampled bf16")
+    else:
+        parity(host_f32(got), y_ref, "sampled")
+
+
+@pytest.mark.parametrize("i,name,N,K", [(i, *s) for i, s in enumerate(synth.LLAMA70B)])
+def test_llama_decode_full_size_sampled(i, name, N, K):
+    """The bench workload (Llama-70B shapes, M = 1, 8, 32, tile-major G = 4 KB,
+    br = 32, block fetch), in the launch configuration the bench uses."""
+    banner(f"llama decode full {name}")
+    import torch
+    W_bits = synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA)
+    W = dev_bf16(W_bits)
+    Wt = torch.empty_like(W)
+    tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
+    del W
+    for M in synth.LLAMA_DECODE_M:
+        A_bits = synth.normal_bf16((M, K), seed=synth.llama_decode_act_seed(i, M))
+        A = dev_bf16(A_bits)
+        C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(), tl.TL_FETCH_BLOCK)
+        _sync()
+        _sampled_check(A_bits, W_bits, C, 512, seed=M + i)
+
+
+@pytest.mark.parametrize("i,name,N,K", [(i, *s) for i, s in enumerate(synth.LLAMA70B)])
+def test_llama_prefill_full_size_sampled(i, name, N, K):
+    banner(f"llama prefill full {name}")
+    import torch
+    W_bits = synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA)
+    W = dev_bf16(W_bits)
+    Wt = torch.empty_like(W)
+    tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
+    del W
+    M = synth.LLAMA_PREFILL_M
+    A_bits = synth.normal_bf16((M, K), seed=synth.llama_prefill_act_seed(i))
+    A = dev_bf16(A_bits)
+    for tm in (128, 256):
+        C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(tile_m=tm, out_dtype=tl.TL_OUT_BF16), tl.TL_FETCH_BLOCK)
+        _sync()
+        _sampled_check(A_bits, W_bits, C, 512, seed=tm + i, bf16_out=True)

@@ -1,0 +1,174 @@
+"""Host-side tests of libtl (no GPU): the library loads and exports every
+symbol include/tl.h declares; tl_read_amp equals the brute-force oracle;
+tl_gemm_plan; argument validation returns the documented status before any
+device work."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_04031_amd as tl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+KIND = {oracle.NK_ROW: tl.TL_LAYOUT_NK_ROW, oracle.KN_ROW: tl.TL_LAYOUT_KN_ROW,
+        oracle.TILE: tl.TL_LAYOUT_TILE}
+
+
+def header_symbols():
+    text = open(os.path.join(ROOT, "include", "tl.h")).read()
+    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(tl_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = tl.load_library()
+    syms = header_symbols()
+    assert set(syms) == set(tl.EXPORTED)
+    for s in syms:
+        assert hasattr(lib, s), s
+    # and the binding exposes the same names
+    for s in syms:
+        assert callable(getattr(tl, s))
+
+
+def test_strerror_strings():
+    for st in (tl.TL_OK, tl.TL_EINVAL, tl.TL_EUNSUPPORTED, tl.TL_EHIP, tl.TL_ENOMEM):
+        assert tl.tl_strerror(st).startswith("TL_")
+    assert "unknown" in tl.tl_strerror(12345)
+
+
+def _lib_amp(M, N, K, tm, tn, tk, kind, G, layout_G=4096, br=32):
+    d = tl.layout(kind=KIND[kind], G=layout_G, block_rows=br)
+    return tl.tl_read_amp(M, N, K, tm, tn, tk, d, G)
+
+
+def test_read_amp_matches_oracle_random_shapes():
+    """Random shapes including ragged tiles, G != memory-tile size, all layouts."""
+    rng = np.random.default_rng(11)
+    for _ in range(120):
+        kind = int(rng.choice([oracle.NK_ROW, oracle.KN_ROW, oracle.TILE]))
+        s = 2
+        layout_G = int(rng.choice([256, 512, 1024, 4096]))
+        br = int(rng.choice([1, 2, 4, 8, 16, 32]))
+        if s * br > layout_G:
+            continue
+        bc = layout_G // (s * br)
+        if kind == oracle.TILE:
+            N = br * int(rng.integers(1, 5)) * (1 if br > 8 else 4)
+            K = bc * int(rng.integers(1, 5))
+        else:
+            N = int(rng.integers(1, 70))
+            K = int(rng.integers(1, 300))
+        G = int(rng.choice([64, 256, 512, 1024, 4096])) if rng.random() < 0.5 else layout_G
+        M = int(rng.integers(1, 40))
+        tm = int(rng.integers(1, 20))
+        tn = int(rng.choice([1, 3, 8, 16, 32, 64]))
+        tk = int(rng.choice([1, 5, 16, 64, 128, 256]))
+        want = oracle.read_amp(M, N, K, tm, tn, tk, kind, G, s=s, layout_G=layout_G, block_rows=br)
+        got = _lib_amp(M, N, K, tm, tn, tk, kind, G, layout_G, br)
+        for key in want:
+            if key == "amp":
+                assert got[key] == pytest.approx(want[key], rel=1e-15)
+            else:
+                assert got[key] == want[key], (key, kind, M, N, K, tm, tn, tk, G, layout_G, br)
+
+
+@pytest.mark.parametrize("G", [512, 1024, 4096, 16384])
+@pytest.mark.parametrize("br", [8, 16, 32, 64])
+def test_read_amp_granularity_sweep_slice_matches_oracle(G, br):
+    """Down-projection [8192, 28672] (256-row slice), tiles 64..256: the
+    library's closed forms equal the oracle's enumeration exactly."""
+    N, K, s = 256, 28672, 2
+    for tn in (64, 128, 256):
+        for tk in (64, 128, 256):
+            for kind in (oracle.NK_ROW, oracle.TILE):
+                want = oracle.read_amp(32, N, K, 32, tn, tk, kind, G, s=s, layout_G=G, block_rows=br)
+                got = _lib_amp(32, N, K, 32, tn, tk, kind, G, G, br)
+                assert got == {k: (pytest.approx(v) if k == "amp" else v) for k, v in want.items()}
+
+
+def test_read_amp_tiny_config():
+    assert _lib_amp(16, 1024, 1024, 64, 64, 64, oracle.NK_ROW, 4096)["amp"] == 16.0
+    assert _lib_amp(16, 1024, 1024, 64, 64, 64, oracle.KN_ROW, 4096)["amp"] == 16.0
+    assert _lib_amp(16, 1024, 1024, 64, 64, 64, oracle.TILE, 4096)["amp"] == 1.0
+
+
+def test_read_amp_rejects_bad_arguments():
+    d = tl.layout()
+    for args in [(0, 8, 8, 1, 1, 1), (1, 8, 8, 0, 1, 1), (1, 8, 8, 1, 1, -1)]:
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_read_amp(*args, d, 4096)
+        assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError):
+        tl.tl_read_amp(1, 8, 8, 1, 1, 1, d, 0)
+    bad = tl.layout(G=3000)
+    with pytest.raises(tl.TLError):
+        tl.tl_read_amp(1, 64, 64, 1, 1, 1, bad, 4096)
+    # TILE requires N % br == 0 and K % bc == 0
+    with pytest.raises(tl.TLError):
+        tl.tl_read_amp(1, 48, 64, 1, 1, 1, tl.layout(block_rows=32), 4096)
+
+
+def test_gemm_plan_decode_and_prefill_shapes():
+    d = tl.layout()
+    # Llama-70B-shaped decode at M = 8: whole memory tiles per compute tile
+    for N, K, S in [(10240, 8192, 4), (8192, 8192, 4), (57344, 8192, 1), (8192, 28672, 4)]:
+        p = tl.tl_gemm_plan(8, N, K, d)
+        assert p["kernel"] == 1 and p["tile_n"] == 32 and p["tile_k"] == 64
+        assert p["split_k"] == S
+        assert p["workgroups"] % 256 == 0
+        amp = tl.tl_read_amp(8, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, 4096)
+        assert amp["amp"] == 1.0
+    p = tl.tl_gemm_plan(2048, 57344, 8192, d)
+    assert p["kernel"] == 2 and p["tile_m"] == 256 and p["tile_n"] == 128
+    p = tl.tl_gemm_plan(2048, 57344, 8192, tl.layout(tile_m=128))
+    assert p["tile_m"] == 128
+
+
+def test_gemm_plan_error_codes():
+    d = tl.layout()
+    cases = [
+        ((0, 64, 64, d), tl.TL_EINVAL),
+        ((8, 64, 64, tl.layout(G=1000)), tl.TL_EINVAL),
+        ((8, 48, 64, d), tl.TL_EINVAL),                      # N % br
+        ((8, 64, 96, d), tl.TL_EINVAL),                      # K % bc
+        ((8, 64, 64, tl.layout(elem_bytes=1)), tl.TL_EUNSUPPORTED),
+        ((8, 64, 64, tl.layout(kind=tl.TL_LAYOUT_KN_ROW)), tl.TL_EUNSUPPORTED),
+        ((8, 64, 64, tl.layout(G=512, block_rows=64)), tl.TL_EUNSUPPORTED),   # bc = 4
+        ((8, 64, 64, tl.layout(out_dtype=7)), tl.TL_EINVAL),
+        ((8, 64, 64, tl.layout(tile_n=48)), tl.TL_EUNSUPPORTED),
+    ]
+    for (M, N, K, desc), want in cases:
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_plan(M, N, K, desc)
+        assert e.value.status == want, (M, N, K)
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm_plan(8, 64, 64, d, fetch_mode=0x8)
+    assert e.value.status == tl.TL_EINVAL
+
+
+def test_entry_points_reject_before_device_work():
+    """NULL / misaligned pointers and bad descriptors return an error status
+    and enqueue nothing; these paths make no HIP call."""
+    d = tl.layout()
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm(0, 0, 0, 8, 64, 64, d, tl.TL_FETCH_BLOCK, stream=0)
+    assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm(16, 32, 8, 8, 64, 64, d, tl.TL_FETCH_BLOCK, stream=0)   # C misaligned
+    assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_repack(0, 0, 64, 64, 2, 4096, 32, stream=0)
+    assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_repack(4096, 8192, 64, 64, 3, 4096, 32, stream=0)          # elem_bytes
+    assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_repack(4096, 8192, 48, 64, 2, 4096, 32, stream=0)          # rows % br
+    assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:                                  # overlap
+        tl.tl_repack(4096, 4096 + 1024, 64, 64, 2, 4096, 32, stream=0)
+    assert e.value.status == tl.TL_EINVAL
+    # empty matrices are a no-op
+    tl.tl_repack(0, 0, 0, 64, 2, 4096, 32, stream=0)
