@@ -6,7 +6,9 @@ the four projections (QKV 8192->10240, O 8192->8192, gate+up 8192->57344,
 down 28672->8192) through tl_gemm with bf16 weights stored tile-major
 (G = 4096 B, 32 x 64-element memory tiles), block-granular fetch, fp32 out.
 The layer holds 1.71 GB of weights, far above the 256 MB last-level cache, so
-every call streams its weight from HBM.
+every call streams its weight from HBM.  The timed region launches K steps
+eagerly on one stream; the same step captured as a HIP graph and replayed K
+times is timed too and reported beside it.
 
 value = algorithmic bytes (2NK + 2MK + 4MN summed over the four GEMMs) per
 second over the K timed steps, in GB/s.  Also reported: prefill TFLOP/s at
@@ -80,7 +82,10 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     tl.load_library()
     dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream()
+    # all work on one side stream (default priority): graphs cannot be
+    # captured on the null stream
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.set_stream(stream)
 
     # ---------------- weights: seeded, row-major, repacked on the GPU --------
     desc = tl.layout(G=G, block_rows=BR)
@@ -125,21 +130,41 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # ---------------- timed region ----------------
+    # ---------------- timed region: K eager steps ----------------
     log(f"timing {args.steps} steps")
-    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-           for _ in weights] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(ev[s])
+    for _ in range(args.steps):
+        step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     wall_s = t1 - t0
     ms_per_step = wall_s * 1e3 / args.steps
     value_gbs = step_bytes * args.steps / wall_s / 1e9
 
-    # per-launch kernel durations from HIP events on the launch stream
+    # the same step captured once as a HIP graph and replayed K times (the
+    # library's workspace already exists, so capture records kernels only);
+    # reported beside the eager number
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    graph_gbs = step_bytes * args.steps / (time.perf_counter() - t0) / 1e9
+
+    # per-launch durations from HIP events recorded on the launch stream around
+    # each tl_gemm call (a separate pass over the same launches)
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+           for _ in weights] for _ in range(args.steps)]
+    for s in range(args.steps):
+        step(ev[s])
+    torch.cuda.synchronize()
     per_shape_ms = [0.0] * len(weights)
     for s in range(args.steps):
         for j in range(len(weights)):
@@ -148,9 +173,11 @@ def main():
     launch_bytes = [2 * N * K + 2 * DECODE_M * K + 4 * DECODE_M * N for (_, N, K, _) in weights]
     achieved = sum(launch_bytes) / (sum(per_shape_ms) * 1e-3) / 1e9
     per_shape = {name: {"us": round(ms * 1e3, 2), "GB/s": round(b / (ms * 1e-3) / 1e9, 1),
-                        "frac_hbm_peak": round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-                 for (name, _, _, _), ms, b in zip(weights, per_shape_ms, launch_bytes)}
-    log(f"decode layer M={DECODE_M}: {value_gbs:.1f} GB/s wall, kernels {achieved:.1f} GB/s")
+                        "frac_hbm_peak": round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                        "split_k": tl.tl_gemm_plan(DECODE_M, N, K, desc)["split_k"]}
+                 for (name, N, K, _), ms, b in zip(weights, per_shape_ms, launch_bytes)}
+    log(f"decode layer M={DECODE_M}: eager {value_gbs:.1f} GB/s, graph replay {graph_gbs:.1f} GB/s, "
+        f"kernels {achieved:.1f} GB/s")
 
     # ---------------- read amplification ----------------
     plan = tl.tl_gemm_plan(DECODE_M, 8192, 8192, desc, tl.TL_FETCH_BLOCK)
@@ -234,7 +261,8 @@ def main():
     traffic = profiled_traffic(kernel_hash)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "decode_kernel (tile-major, M=8)", "per_shape": per_shape}
+                "kernel": "decode_kernel (tile-major, M=8; a split_k > 1 call includes its reduce kernel)",
+                "per_shape": per_shape}
 
     out = {
         "metric": METRIC,
@@ -253,6 +281,7 @@ def main():
                                "bf16 weights tile-major G=4096 B 32x64 memory tiles, block fetch, fp32 out",
                    "M": DECODE_M, "G": G, "block_rows": BR, "weight_bytes": sum(2 * N * K for (_, N, K, _) in weights)},
         "frac_hbm_peak": round(value_gbs / HBM_PEAK_GBS, 4),
+        "graph_replay_GB/s": round(graph_gbs, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "prefill": prefill,

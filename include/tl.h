@@ -82,9 +82,10 @@ typedef struct tl_layout_desc {
     int32_t tile_m;      /* tl_gemm: requested compute tile, 0 = library's */
     int32_t tile_n;      /*   choice; see tl_gemm_plan for what is accepted */
     int32_t tile_k;
-    int32_t split_k;     /* tl_gemm: K-splits across workgroups, 0 = library's
-                            choice; partial sums are reduced in a fixed order,
-                            so results are bitwise reproducible */
+    int32_t split_k;     /* tl_gemm: K-splits across workgroups (decode kernel,
+                            1..16), 0 = library's choice; partial sums are
+                            reduced in a fixed order, so results are bitwise
+                            reproducible */
 } tl_layout_desc;
 
 /* Read-amplification report (tl_read_amp). */

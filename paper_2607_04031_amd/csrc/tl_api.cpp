@@ -33,14 +33,12 @@ int make_tile_layout(int64_t s, int64_t G, int64_t br, Layout* out) {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Library state: split-K workspace, tile counters and the fetch tally, one set
-// per (device, stream).
+// Library state: split-K workspace and the fetch tally, one set per
+// (device, stream).
 // ---------------------------------------------------------------------------
 struct StreamState {
     float* ws = nullptr;
     size_t ws_bytes = 0;
-    int* counters = nullptr;
-    size_t n_counters = 0;
     unsigned long long* fetch = nullptr;
 };
 
@@ -51,10 +49,10 @@ int current_device(int* dev) {
     return hipGetDevice(dev) == hipSuccess ? TL_OK : TL_EHIP;
 }
 
-// Returns the state for (current device, stream), growing its buffers.  New
-// counters and the tally are cleared on 'stream' so the clear is ordered
-// before any kernel that uses them.
-int get_state(hipStream_t stream, size_t ws_bytes, size_t n_counters, StreamState** out) {
+// Returns the state for (current device, stream), growing the workspace.  A
+// new tally is cleared on 'stream' so the clear is ordered before any kernel
+// that uses it.
+int get_state(hipStream_t stream, size_t ws_bytes, StreamState** out) {
     int dev = 0;
     if (current_device(&dev) != TL_OK) return TL_EHIP;
     std::lock_guard<std::mutex> lock(g_mu);
@@ -74,18 +72,6 @@ int get_state(hipStream_t stream, size_t ws_bytes, size_t n_counters, StreamStat
         size_t bytes = std::max<size_t>(ws_bytes, size_t(1) << 20);
         if (hipMalloc(&st.ws, bytes) != hipSuccess) { st.ws = nullptr; return TL_ENOMEM; }
         st.ws_bytes = bytes;
-    }
-    if (n_counters > st.n_counters) {
-        if (st.counters) {
-            if (hipStreamSynchronize(stream) != hipSuccess) return TL_EHIP;
-            (void)hipFree(st.counters);
-            st.counters = nullptr;
-            st.n_counters = 0;
-        }
-        size_t n = std::max<size_t>(n_counters, 4096);
-        if (hipMalloc(&st.counters, n * sizeof(int)) != hipSuccess) { st.counters = nullptr; return TL_ENOMEM; }
-        if (hipMemsetAsync(st.counters, 0, n * sizeof(int), stream) != hipSuccess) return TL_EHIP;
-        st.n_counters = n;
     }
     *out = &st;
     return TL_OK;
@@ -132,11 +118,11 @@ struct Plan {
     bool count = false;
     int m_tiles16 = 1;
     int64_t k_unit = 64;
-    int64_t n_counters = 0;
 };
 
 constexpr int kDecodeMaxM = 64;
 constexpr int kTargetWorkgroups = 1024;   // 4 per CU on 256 CUs
+constexpr int kMaxSplitK = 16;            // partials the reduce kernel sums
 
 int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t fetch_mode,
               Plan* P) {
@@ -188,14 +174,13 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
             S = (kTargetWorkgroups + n_tiles - 1) / n_tiles;
             S = std::max<int64_t>(1, std::min<int64_t>(S, units / min_units));
         }
-        if (S < 1 || S > units || S > 4096) return TL_EUNSUPPORTED;
+        if (S < 1 || S > units || S > kMaxSplitK) return TL_EUNSUPPORTED;
         p.pub.tile_m = 16 * p.m_tiles16;
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
         p.pub.split_k = int(S);
         p.pub.workgroups = n_tiles * S;
         p.pub.workspace_bytes = S > 1 ? S * M * N * 4 : 0;
-        p.n_counters = S > 1 ? n_tiles : 0;
     } else {
         p.pub.kernel = 2;
         int tm = d->tile_m ? d->tile_m : (M >= 1024 ? 256 : 128);
@@ -254,7 +239,7 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
 
     hipStream_t s = (hipStream_t)stream;
     StreamState* st = nullptr;
-    rc = get_state(s, size_t(p.pub.workspace_bytes), size_t(p.n_counters), &st);
+    rc = get_state(s, size_t(p.pub.workspace_bytes), &st);
     if (rc != TL_OK) return rc;
 
     hipError_t e;
@@ -264,7 +249,6 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
         d.W = static_cast<const uint8_t*>(W);
         d.C = C;
         d.ws = st->ws;
-        d.counters = st->counters;
         d.fetch = p.count ? st->fetch : nullptr;
         d.M = M;
         d.N = N;
@@ -297,7 +281,7 @@ int tl_fetch_counter_read(void* stream, int64_t* bytes) {
     if (!bytes) return TL_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     StreamState* st = nullptr;
-    int rc = get_state(s, 0, 0, &st);
+    int rc = get_state(s, 0, &st);
     if (rc != TL_OK) return rc;
     unsigned long long v = 0;
     if (hipStreamSynchronize(s) != hipSuccess) return TL_EHIP;
@@ -315,7 +299,6 @@ int tl_release(void) {
     for (auto& kv : g_state) {
         (void)hipSetDevice(kv.first.first);
         if (kv.second.ws) (void)hipFree(kv.second.ws);
-        if (kv.second.counters) (void)hipFree(kv.second.counters);
         if (kv.second.fetch) (void)hipFree(kv.second.fetch);
     }
     g_state.clear();

@@ -11,17 +11,20 @@
 //   Each 64-step is two bf16 MFMA 16x16x32 K-halves per 16-row n-subtile:
 //     A operand = activations (rows m = lane % 16), zero-padded to 16 rows,
 //     B operand = weights     (cols n = lane % 16),
-//   lane l supplies 8 consecutive k (a 16-byte load) at k-slot group l / 16.
+//   lane l supplies 8 consecutive k (16 bytes) at k-slot group l / 16.
 //   The per-lane weight address is Eq. 2 evaluated with shifts and masks
 //   (Section 3.2, Eq. 1): strip = n >> log2(br), row-in-tile = n & (br - 1),
 //   memory tile along K = k >> log2(bc), column-in-tile = k & (bc - 1).
 //   With bc >= 8 each 16-byte load stays inside one memory-tile row.
+//   Weight loads are non-temporal (read once) and each load instruction reads
+//   whole 128-byte lines (see decode_kernel).
 // Reduction
-//   waves -> LDS -> fixed-order sum; K-splits -> fp32 partials in a workspace;
-//   the last workgroup of a tile to finish (atomic ticket) sums the partials in
-//   split order and writes C, then re-arms the ticket.  No float atomics, so
+//   waves -> LDS -> fixed-order sum; K-splits -> fp32 partials in a workspace,
+//   summed in split order by a second small kernel.  No float atomics, so
 //   results are bitwise reproducible.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "tl_internal.h"
 
@@ -39,7 +42,6 @@ struct DecodeParams {
     const uint8_t* W;
     void* C;
     float* ws;
-    int* counters;
     unsigned long long* fetch;
     int M, N, K;
     int split_k;
@@ -71,6 +73,31 @@ __device__ inline int64_t w_koff(const DecodeParams& p, int k) {
     return int64_t(k) << 1;
 }
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Value of 'v' held by lane l ^ 8 (DPP row_ror:8 inside each 16-lane row).
+__device__ inline bf16x8 swap8(bf16x8 v) {
+    i32x4 x = __builtin_bit_cast(i32x4, v), y;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y[i] = __builtin_amdgcn_update_dpp(0, x[i], 0x128, 0xf, 0xf, false);
+    return __builtin_bit_cast(bf16x8, y);
+}
+
+__device__ inline bf16x8 load_stream(const uint8_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
+}
+
+// Weight loads.  Lane l = 16 g + q needs, per 16-row n-subtile and 64-wide K
+// step, the MFMA B operands  B0 = W[row q][k-chunk g], B1 = W[row q][chunk 4+g]
+// (chunks of 8 elements).  Fetching those directly touches 16 rows x 64 B per
+// instruction.  Instead every lane loads
+//     x0 = W[row (q & 7)    ][chunk 4 (q >> 3) + g]
+//     x1 = W[row 8 + (q & 7)][chunk 4 (q >> 3) + g]
+// so each instruction reads 8 rows x 128 B -- whole 128 B lines for every
+// memory-tile shape with block_cols >= 8 -- and the operands are rebuilt with
+// one exchange between lanes l and l ^ 8:
+//     t = q < 8 ? x1 : x0,  s = t from lane l ^ 8,
+//     B0 = q < 8 ? x0 : s,  B1 = q < 8 ? s : x1.
 template <int MT, int NS, int U, bool TILE, bool OUT_BF16, bool COUNT>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     constexpr int TN = 16 * NS;
@@ -85,24 +112,28 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     const int st0 = u0 * p.steps_per_unit, st1 = u1 * p.steps_per_unit;
 
     const int n_base = tile * TN;
-    const int kq = (lane >> 4) * 8;     // this lane's k-slot group inside a 32-K half
+    const int g = lane >> 4, q = lane & 15;
+    const bool lo = q < 8;
+    const int kc = (((q >> 3) << 2) + g) << 3;   // k offset of this lane's weight chunk in a step
 
-    const uint8_t* wrow[NS];
+    const uint8_t* wrow[NS][2];
 #pragma unroll
-    for (int j = 0; j < NS; ++j) {
-        const int n = n_base + j * 16 + (lane & 15);
-        int64_t off;
-        if (TILE) off = int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << (p.log2_bc + 1));
-        else off = int64_t(n) * p.K * 2;
-        wrow[j] = p.W + off;
-    }
+    for (int j = 0; j < NS; ++j)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            const int n = n_base + j * 16 + hf * 8 + (q & 7);
+            int64_t off;
+            if (TILE) off = int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << (p.log2_bc + 1));
+            else off = int64_t(n) * p.K * 2;
+            wrow[j][hf] = p.W + off;
+        }
     const uint16_t* arow[MT];
     bool aok[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + (lane & 15);
+        const int m = mt * 16 + q;
         aok[mt] = m < p.M;
-        arow[mt] = p.A + int64_t(aok[mt] ? m : 0) * p.K;
+        arow[mt] = p.A + int64_t(aok[mt] ? m : 0) * p.K + g * 8;
     }
 
     f32x4 acc[MT][NS];
@@ -116,59 +147,60 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
     const int nsteps = st1 - st0 - wave > 0 ? (st1 - st0 - wave + kWaves - 1) / kWaves : 0;
     int st = st0 + wave;
     int i = 0;
+    auto compute = [&](const bf16x8 (&x)[NS][2], const bf16x8 (&a)[2][MT]) {
+#pragma unroll
+        for (int j = 0; j < NS; ++j) {
+            const bf16x8 t = lo ? x[j][1] : x[j][0];
+            const bf16x8 s = swap8(t);
+            const bf16x8 b0 = lo ? x[j][0] : s;
+            const bf16x8 b1 = lo ? s : x[j][1];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0][mt], b0, acc[mt][j], 0, 0, 0);
+                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1][mt], b1, acc[mt][j], 0, 0, 0);
+            }
+        }
+    };
     for (; i + U <= nsteps; i += U) {
-        bf16x8 w[U][2][NS];
+        bf16x8 x[U][NS][2];
         bf16x8 a[U][2][MT];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int k = (st + u * kWaves) * 64;
+            const int64_t ko = w_koff<TILE>(p, k + kc);
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int kk = k + h * 32 + kq;
-                const int64_t ko = w_koff<TILE>(p, kk);
+            for (int j = 0; j < NS; ++j)
 #pragma unroll
-                for (int j = 0; j < NS; ++j)
-                    w[u][h][j] = *reinterpret_cast<const bf16x8*>(wrow[j] + ko);
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    a[u][h][mt] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + kk) : zero8;
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
+                for (int hf = 0; hf < 2; ++hf) x[u][j][hf] = load_stream(wrow[j][hf] + ko);
 #pragma unroll
             for (int h = 0; h < 2; ++h)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
+                    a[u][h][mt] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + k + h * 32) : zero8;
+        }
 #pragma unroll
-                    for (int j = 0; j < NS; ++j)
-                        acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][h][mt], w[u][h][j],
-                                                                             acc[mt][j], 0, 0, 0);
+        for (int u = 0; u < U; ++u) compute(x[u], a[u]);
         st += U * kWaves;
     }
     for (; i < nsteps; ++i) {
         const int k = st * 64;
+        const int64_t ko = w_koff<TILE>(p, k + kc);
+        bf16x8 x[NS][2], a[2][MT];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int kk = k + h * 32 + kq;
-            const int64_t ko = w_koff<TILE>(p, kk);
-            bf16x8 w[NS], a[MT];
+        for (int j = 0; j < NS; ++j)
 #pragma unroll
-            for (int j = 0; j < NS; ++j) w[j] = *reinterpret_cast<const bf16x8*>(wrow[j] + ko);
+            for (int hf = 0; hf < 2; ++hf) x[j][hf] = load_stream(wrow[j][hf] + ko);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                a[mt] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + kk) : zero8;
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int j = 0; j < NS; ++j)
-                    acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mt], w[j], acc[mt][j], 0, 0, 0);
-        }
+                a[h][mt] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + k + h * 32) : zero8;
+        compute(x, a);
         st += kWaves;
     }
 
     if (COUNT && lane == 0 && nsteps > 0) {
-        // each step: 2 K-halves x NS loads of 64 lanes x 16 B
+        // each step: NS subtiles x 2 loads of 64 lanes x 16 B
         atomicAdd(p.fetch, (unsigned long long)nsteps * 2ull * NS * 1024ull);
     }
 
@@ -180,24 +212,10 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         for (int j = 0; j < NS; ++j) red[wave][mt][j][lane] = acc[mt][j];
     __syncthreads();
 
+    // split_k == 1: final output; otherwise this split's fp32 partial, summed
+    // in split order by splitk_reduce_kernel.
     constexpr int kEntries = MT * NS * 64;   // f32x4 entries per wave
-    if (p.split_k == 1) {
-        for (int e = threadIdx.x; e < kEntries; e += kThreads) {
-            const int mt = e / (NS * 64);
-            const int j = (e / 64) % NS;
-            const int l = e % 64;
-            const f32x4 v = red[0][mt][j][l] + red[1][mt][j][l] + red[2][mt][j][l] + red[3][mt][j][l];
-            const int n = n_base + j * 16 + (l & 15);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = mt * 16 + (l >> 4) * 4 + r;
-                if (m < p.M) store_out<OUT_BF16>(p.C, int64_t(m) * p.N + n, v[r]);
-            }
-        }
-        return;
-    }
-
-    // ---- K-split: publish this split's partial tile, last arrival reduces ----
+    const bool final_out = p.split_k == 1;
     float* part = p.ws + int64_t(split) * p.M * p.N;
     for (int e = threadIdx.x; e < kEntries; e += kThreads) {
         const int mt = e / (NS * 64);
@@ -208,26 +226,38 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int m = mt * 16 + (l >> 4) * 4 + r;
-            if (m < p.M) part[int64_t(m) * p.N + n] = v[r];
+            if (m < p.M) {
+                if (final_out) store_out<OUT_BF16>(p.C, int64_t(m) * p.N + n, v[r]);
+                else part[int64_t(m) * p.N + n] = v[r];
+            }
         }
     }
-    __threadfence();            // release the partial to every XCD
-    __syncthreads();
-    __shared__ int s_last;
-    if (threadIdx.x == 0) s_last = atomicAdd(&p.counters[tile], 1) == p.split_k - 1;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();            // acquire the other splits' partials
-    const int outs = p.M * TN;
-    for (int e = threadIdx.x; e < outs; e += kThreads) {
-        const int m = e / TN;
-        const int n = n_base + (e - m * TN);
-        const int64_t idx = int64_t(m) * p.N + n;
-        float sum = 0.f;
-        for (int s = 0; s < p.split_k; ++s) sum += __builtin_nontemporal_load(p.ws + int64_t(s) * p.M * p.N + idx);
-        store_out<OUT_BF16>(p.C, idx, sum);
+}
+
+// C[i] = sum over s = 0..S-1 (ascending) of ws[s][i]; i covers M*N/4 float4s.
+// All S partial loads are issued before the in-order sum (latency-bound
+// kernel); S <= kMaxSplitReduce.
+constexpr int kMaxSplitReduce = 16;
+template <bool OUT_BF16>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, void* C, int64_t mn4, int S) {
+    const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= mn4) return;
+    f32x4 part[kMaxSplitReduce];
+#pragma unroll
+    for (int s = 0; s < kMaxSplitReduce; ++s)
+        if (s < S) part[s] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ws + int64_t(s) * mn4 * 4) + i);
+    f32x4 acc = part[0];
+#pragma unroll
+    for (int s = 1; s < kMaxSplitReduce; ++s)
+        if (s < S) acc += part[s];
+    if (OUT_BF16) {
+        uint2 o;
+        o.x = uint32_t(f32_to_bf16_rne(acc[0])) | (uint32_t(f32_to_bf16_rne(acc[1])) << 16);
+        o.y = uint32_t(f32_to_bf16_rne(acc[2])) | (uint32_t(f32_to_bf16_rne(acc[3])) << 16);
+        reinterpret_cast<uint2*>(C)[i] = o;
+    } else {
+        reinterpret_cast<f32x4*>(C)[i] = acc;
     }
-    if (threadIdx.x == 0) atomicExch(&p.counters[tile], 0);   // re-arm for the next call
 }
 
 template <int MT, int NS, bool TILE, bool OUT_BF16, bool COUNT>
@@ -263,7 +293,6 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.W = d.W;
     p.C = d.C;
     p.ws = d.ws;
-    p.counters = d.counters;
     p.fetch = d.fetch;
     p.M = int(d.M);
     p.N = int(d.N);
@@ -279,11 +308,20 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.bc_mask = tile ? int(d.L.bc - 1) : 0;
     const int grid = int(d.N / d.tile_n) * d.split_k;
     const int ns = d.tile_n / 16;
+    hipError_t e;
     switch (d.m_tiles16) {
-        case 1: return launch_m<1>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream);
-        case 2: return launch_m<2>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream);
-        default: return launch_m<4>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream);
+        case 1: e = launch_m<1>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream); break;
+        case 2: e = launch_m<2>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream); break;
+        default: e = launch_m<4>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream); break;
     }
+    if (e != hipSuccess || d.split_k == 1) return e;
+    const int64_t mn4 = d.M * d.N / 4;
+    const int rgrid = int((mn4 + 255) / 256);
+    if (d.out_bf16)
+        hipLaunchKernelGGL((splitk_reduce_kernel<true>), dim3(rgrid), dim3(256), 0, stream, d.ws, d.C, mn4, d.split_k);
+    else
+        hipLaunchKernelGGL((splitk_reduce_kernel<false>), dim3(rgrid), dim3(256), 0, stream, d.ws, d.C, mn4, d.split_k);
+    return hipGetLastError();
 }
 
 }  // namespace tl

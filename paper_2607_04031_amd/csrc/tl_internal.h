@@ -45,7 +45,6 @@ struct DecodeLaunch {
     const uint8_t* W;
     void* C;
     float* ws;                  // [split_k][M][N] partials (split_k > 1)
-    int* counters;              // one per n-tile, zero on entry, left zero on exit
     unsigned long long* fetch;  // fetch tally (TL_FETCH_COUNT) or nullptr
     int64_t M, N, K;
     Layout L;

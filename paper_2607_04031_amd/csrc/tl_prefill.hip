@@ -23,6 +23,7 @@ namespace {
 
 typedef short bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 struct PrefillParams {
     const uint16_t* A;
@@ -83,30 +84,8 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
         else off = int64_t(n) * p.K * 2;
         w_src[i] = p.W + off;
         w_k[i] = c * 8;
-        w_lds[i] = W_BYTES * 0 + swz(row, c);
+        w_lds[i] = swz(row, c);
     }
-
-    uint4 ra[A_CH], rw[W_CH];
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_src[i] + k0);
-#pragma unroll
-        for (int i = 0; i < W_CH; ++i) {
-            const int k = k0 + w_k[i];
-            int64_t ko;
-            if (TILE) ko = (int64_t(k >> p.log2_bc) << p.log2_G) + int64_t((k & p.bc_mask) << 1);
-            else ko = int64_t(k) << 1;
-            rw[i] = *reinterpret_cast<const uint4*>(w_src[i] + ko);
-        }
-    };
-    auto sstore = [&](int buf) {
-        uint8_t* As = smem + buf * (A_BYTES + W_BYTES);
-        uint8_t* Ws = As + A_BYTES;
-#pragma unroll
-        for (int i = 0; i < A_CH; ++i) *reinterpret_cast<uint4*>(As + a_lds[i]) = ra[i];
-#pragma unroll
-        for (int i = 0; i < W_CH; ++i) *reinterpret_cast<uint4*>(Ws + w_lds[i]) = rw[i];
-    };
 
     const int lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -118,13 +97,42 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const int KT = p.K / BK;
-    gload(0);
-    sstore(0);
+    // prefetch registers for the next K step (kept in VGPRs: plain scalars
+    // indexed only by unrolled constants)
+    u32x4 ra[A_CH], rw[W_CH];
+#pragma unroll
+    for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
+#pragma unroll
+    for (int i = 0; i < W_CH; ++i) {
+        const int k = w_k[i];
+        int64_t ko;
+        if (TILE) ko = (int64_t(k >> p.log2_bc) << p.log2_G) + int64_t((k & p.bc_mask) << 1);
+        else ko = int64_t(k) << 1;
+        rw[i] = *reinterpret_cast<const u32x4*>(w_src[i] + ko);
+    }
+#pragma unroll
+    for (int i = 0; i < A_CH; ++i) *reinterpret_cast<u32x4*>(smem + a_lds[i]) = ra[i];
+#pragma unroll
+    for (int i = 0; i < W_CH; ++i) *reinterpret_cast<u32x4*>(smem + A_BYTES + w_lds[i]) = rw[i];
     __syncthreads();
+
+    const int KT = p.K / BK;
     for (int kt = 0; kt < KT; ++kt) {
         const int buf = kt & 1;
-        if (kt + 1 < KT) gload((kt + 1) * BK);
+        const bool more = kt + 1 < KT;
+        if (more) {
+            const int k0 = (kt + 1) * BK;
+#pragma unroll
+            for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + k0);
+#pragma unroll
+            for (int i = 0; i < W_CH; ++i) {
+                const int k = k0 + w_k[i];
+                int64_t ko;
+                if (TILE) ko = (int64_t(k >> p.log2_bc) << p.log2_G) + int64_t((k & p.bc_mask) << 1);
+                else ko = int64_t(k) << 1;
+                rw[i] = *reinterpret_cast<const u32x4*>(w_src[i] + ko);
+            }
+        }
         const uint8_t* As = smem + buf * (A_BYTES + W_BYTES);
         const uint8_t* Ws = As + A_BYTES;
 #pragma unroll
@@ -147,7 +155,13 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
                 for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
         }
-        if (kt + 1 < KT) sstore(buf ^ 1);
+        if (more) {
+            uint8_t* An = smem + (buf ^ 1) * (A_BYTES + W_BYTES);
+#pragma unroll
+            for (int i = 0; i < A_CH; ++i) *reinterpret_cast<u32x4*>(An + a_lds[i]) = ra[i];
+#pragma unroll
+            for (int i = 0; i < W_CH; ++i) *reinterpret_cast<u32x4*>(An + A_BYTES + w_lds[i]) = rw[i];
+        }
         __syncthreads();
     }
 

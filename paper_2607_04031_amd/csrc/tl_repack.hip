@@ -24,9 +24,14 @@ struct RepackParams {
     int inverse;            // 0: row-major -> tile-major, 1: back
 };
 
+// Native vector types (not HIP's uint4/uint2 structs) so the per-thread
+// staging arrays stay in registers.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
 template <int CH> struct Chunk;
-template <> struct Chunk<16> { using T = uint4; };
-template <> struct Chunk<8> { using T = uint2; };
+template <> struct Chunk<16> { using T = u32x4; };
+template <> struct Chunk<8> { using T = u32x2; };
 template <> struct Chunk<4> { using T = uint32_t; };
 template <> struct Chunk<2> { using T = uint16_t; };
 template <> struct Chunk<1> { using T = uint8_t; };

@@ -338,3 +338,39 @@ def test_llama_prefill_full_size_sampled(i, name, N, K):
         tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(tile_m=tm, out_dtype=tl.TL_OUT_BF16), tl.TL_FETCH_BLOCK)
         _sync()
         _sampled_check(A_bits, W_bits, C, 512, seed=tm + i, bf16_out=True)
+
+
+# ---------------------------------------------------------------------------
+# HIP graph capture: replays equal eager results, replay after replay
+# ---------------------------------------------------------------------------
+
+def test_graph_replay_matches_eager():
+    import torch
+    banner("graph capture / replay")
+    side = torch.cuda.Stream()
+    cases = [(8, 1024, 2048, 1), (8, 1024, 2048, 4), (32, 512, 4096, 3), (256, 512, 1024, 0)]
+    with torch.cuda.stream(side):
+        tensors = []
+        for i, (M, N, K, S) in enumerate(cases):
+            A = dev_bf16(synth.normal_bf16((M, K), seed=40 + i))
+            W = dev_bf16(synth.normal_bf16((N, K), seed=50 + i, sigma=synth.W_SIGMA))
+            Wt = torch.empty_like(W)
+            tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
+            C = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+            d = tl.layout(split_k=S)
+            tl.tl_gemm(A, Wt, C, M, N, K, d, tl.TL_FETCH_BLOCK)       # eager; creates the workspace
+            tensors.append((A, Wt, C, d, M, N, K))
+        side.synchronize()
+        eager = [t[2].clone() for t in tensors]
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for (A, Wt, C, d, M, N, K) in tensors:
+                tl.tl_gemm(A, Wt, C, M, N, K, d, tl.TL_FETCH_BLOCK)
+        for rep in range(4):
+            for (_, _, C, _, _, _, _) in tensors:
+                C.fill_(float("nan"))                # eager work between replays
+            side.synchronize()
+            g.replay()
+            side.synchronize()
+            for (_, _, C, _, _, _, _), want in zip(tensors, eager):
+                assert torch.equal(C, want), f"replay {rep}"
