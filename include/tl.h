@@ -107,7 +107,8 @@ typedef struct tl_plan {
     int32_t tile_n;      /* the tile to pass to tl_read_amp to account for the  */
     int32_t tile_k;      /* kernel's fetches                                     */
     int32_t split_k;     /* workgroups per output tile along K */
-    int32_t reserved;
+    int32_t waves;       /* wavefronts per workgroup (decode: 4, 8 or 16; the
+                            waves of a workgroup also split K, reduced in LDS) */
     int64_t workgroups;  /* grid size */
     int64_t workspace_bytes;  /* split-K partials the call needs from the library */
 } tl_plan;

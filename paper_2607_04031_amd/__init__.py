@@ -68,13 +68,13 @@ class Plan(ctypes.Structure):
                 ("tile_n", ctypes.c_int32),
                 ("tile_k", ctypes.c_int32),
                 ("split_k", ctypes.c_int32),
-                ("reserved", ctypes.c_int32),
+                ("waves", ctypes.c_int32),
                 ("workgroups", ctypes.c_int64),
                 ("workspace_bytes", ctypes.c_int64)]
 
 
 def _struct_dict(s):
-    return {name: getattr(s, name) for name, _ in s._fields_ if name != "reserved"}
+    return {name: getattr(s, name) for name, _ in s._fields_}
 
 
 class TLError(RuntimeError):

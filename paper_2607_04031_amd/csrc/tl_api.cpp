@@ -117,12 +117,14 @@ struct Plan {
     bool out_bf16 = false;
     bool count = false;
     int m_tiles16 = 1;
+    int waves = 4;
     int64_t k_unit = 64;
 };
 
 constexpr int kDecodeMaxM = 64;
 constexpr int kTargetWorkgroups = 1024;   // 4 per CU on 256 CUs
 constexpr int kMaxSplitK = 16;            // partials the reduce kernel sums
+constexpr int kCUs = 256;                  // MI355X compute units
 
 int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t fetch_mode,
               Plan* P) {
@@ -168,18 +170,34 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         if (d->tile_k && (d->tile_k != p.k_unit)) return TL_EUNSUPPORTED;
         const int64_t n_tiles = N / tn;
         const int64_t units = K / p.k_unit;
+        // Balance: every CU should stream the same number of bytes.  With at
+        // least 4 tiles per CU, one 4-wave workgroup per tile; with one or two
+        // tiles per CU (N = 256 or 512 tiles), one workgroup per tile whose 8
+        // or 16 waves split K among themselves (reduced in LDS, no second
+        // kernel); otherwise split K across workgroups (fp32 partials + a
+        // fixed-order reduce kernel).
         int64_t S = d->split_k;
         if (S == 0) {
-            const int64_t min_units = std::max<int64_t>(1, 1024 / p.k_unit);  // >= 1024 K per split
-            S = (kTargetWorkgroups + n_tiles - 1) / n_tiles;
-            S = std::max<int64_t>(1, std::min<int64_t>(S, units / min_units));
+            if (n_tiles >= kTargetWorkgroups || n_tiles % kCUs == 0) {
+                S = 1;
+            } else {
+                const int64_t min_units = std::max<int64_t>(1, 1024 / p.k_unit);  // >= 1024 K per split
+                S = (kTargetWorkgroups + n_tiles - 1) / n_tiles;
+                S = std::max<int64_t>(1, std::min<int64_t>(S, units / min_units));
+            }
         }
         if (S < 1 || S > units || S > kMaxSplitK) return TL_EUNSUPPORTED;
+        const int64_t wgs = n_tiles * S;
+        const int ns = tn / 16;
+        int waves = wgs <= kCUs ? 16 : (wgs <= 2 * kCUs ? 8 : 4);
+        while (waves > 4 && waves * p.m_tiles16 * ns > 64) waves /= 2;   // LDS reduction buffer <= 64 KB
+        p.waves = waves;
         p.pub.tile_m = 16 * p.m_tiles16;
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
         p.pub.split_k = int(S);
-        p.pub.workgroups = n_tiles * S;
+        p.pub.waves = waves;
+        p.pub.workgroups = wgs;
         p.pub.workspace_bytes = S > 1 ? S * M * N * 4 : 0;
     } else {
         p.pub.kernel = 2;
@@ -194,6 +212,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
         p.pub.split_k = 1;
+        p.pub.waves = 4;
         p.pub.workgroups = ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
         p.pub.workspace_bytes = 0;
     }
@@ -256,6 +275,7 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
         d.L = p.L;
         d.tile_n = p.pub.tile_n;
         d.m_tiles16 = p.m_tiles16;
+        d.waves = p.waves;
         d.split_k = p.pub.split_k;
         d.k_unit = p.k_unit;
         d.out_bf16 = p.out_bf16;

@@ -34,8 +34,6 @@ namespace {
 typedef short bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
 
 struct DecodeParams {
     const uint16_t* A;
@@ -50,6 +48,7 @@ struct DecodeParams {
     int64_t strip_bytes;     // br * K * 2 (TILE) -- bytes per strip of br rows
     int log2_br, log2_bc, log2_G;
     int bc_mask;
+    bool out_bf16;
 };
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
@@ -60,9 +59,8 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
     return uint16_t(u >> 16);
 }
 
-template <bool OUT_BF16>
-__device__ inline void store_out(void* C, int64_t idx, float v) {
-    if (OUT_BF16) static_cast<uint16_t*>(C)[idx] = f32_to_bf16_rne(v);
+__device__ inline void store_out(void* C, int64_t idx, float v, bool out_bf16) {
+    if (out_bf16) static_cast<uint16_t*>(C)[idx] = f32_to_bf16_rne(v);
     else static_cast<float*>(C)[idx] = v;
 }
 
@@ -98,8 +96,10 @@ __device__ inline bf16x8 load_stream(const uint8_t* p) {
 // one exchange between lanes l and l ^ 8:
 //     t = q < 8 ? x1 : x0,  s = t from lane l ^ 8,
 //     B0 = q < 8 ? x0 : s,  B1 = q < 8 ? s : x1.
-template <int MT, int NS, int U, bool TILE, bool OUT_BF16, bool COUNT>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
+template <int MT, int NS, int U, int WAVES, bool TILE>
+__global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
+    constexpr int kWaves = WAVES;
+    constexpr int kThreads = 64 * WAVES;
     constexpr int TN = 16 * NS;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -199,12 +199,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         st += kWaves;
     }
 
-    if (COUNT && lane == 0 && nsteps > 0) {
+    if (p.fetch && lane == 0 && nsteps > 0) {
         // each step: NS subtiles x 2 loads of 64 lanes x 16 B
         atomicAdd(p.fetch, (unsigned long long)nsteps * 2ull * NS * 1024ull);
     }
 
-    // ---- reduce the four waves in a fixed order ----
+    // ---- reduce the waves (an in-workgroup K split) in a fixed order ----
+    static_assert(WAVES * MT * NS <= 64, "reduction buffer exceeds 64 KB");
     __shared__ f32x4 red[kWaves][MT][NS][64];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -221,13 +222,15 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
         const int mt = e / (NS * 64);
         const int j = (e / 64) % NS;
         const int l = e % 64;
-        const f32x4 v = red[0][mt][j][l] + red[1][mt][j][l] + red[2][mt][j][l] + red[3][mt][j][l];
+        f32x4 v = red[0][mt][j][l];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) v += red[w][mt][j][l];
         const int n = n_base + j * 16 + (l & 15);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int m = mt * 16 + (l >> 4) * 4 + r;
             if (m < p.M) {
-                if (final_out) store_out<OUT_BF16>(p.C, int64_t(m) * p.N + n, v[r]);
+                if (final_out) store_out(p.C, int64_t(m) * p.N + n, v[r], p.out_bf16);
                 else part[int64_t(m) * p.N + n] = v[r];
             }
         }
@@ -260,29 +263,31 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, voi
     }
 }
 
-template <int MT, int NS, bool TILE, bool OUT_BF16, bool COUNT>
+template <int MT, int NS, int WAVES, bool TILE>
 hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
     constexpr int U = MT >= 4 ? 2 : 4;
-    hipLaunchKernelGGL((decode_kernel<MT, NS, U, TILE, OUT_BF16, COUNT>), dim3(grid), dim3(kThreads), 0,
-                       stream, p);
+    hipLaunchKernelGGL((decode_kernel<MT, NS, U, WAVES, TILE>), dim3(grid), dim3(64 * WAVES), 0, stream, p);
     return hipGetLastError();
 }
 
+// Instantiated (MT, NS, waves) combinations; the planner only asks for these.
 template <int MT, int NS, bool TILE>
-hipError_t launch_b(const DecodeParams& p, int grid, bool out_bf16, bool count, hipStream_t stream) {
-    if (out_bf16) return count ? launch_t<MT, NS, TILE, true, true>(p, grid, stream)
-                               : launch_t<MT, NS, TILE, true, false>(p, grid, stream);
-    return count ? launch_t<MT, NS, TILE, false, true>(p, grid, stream)
-                 : launch_t<MT, NS, TILE, false, false>(p, grid, stream);
+hipError_t launch_w(const DecodeParams& p, int grid, int waves, hipStream_t stream) {
+    if constexpr (16 * MT * NS <= 64) {
+        if (waves == 16) return launch_t<MT, NS, 16, TILE>(p, grid, stream);
+    }
+    if constexpr (8 * MT * NS <= 64) {
+        if (waves == 8) return launch_t<MT, NS, 8, TILE>(p, grid, stream);
+    }
+    return launch_t<MT, NS, 4, TILE>(p, grid, stream);
 }
 
 template <int MT>
-hipError_t launch_m(const DecodeParams& p, int grid, int ns, bool tile, bool out_bf16, bool count,
-                    hipStream_t stream) {
-    if (ns == 2) return tile ? launch_b<MT, 2, true>(p, grid, out_bf16, count, stream)
-                             : launch_b<MT, 2, false>(p, grid, out_bf16, count, stream);
-    return tile ? launch_b<MT, 4, true>(p, grid, out_bf16, count, stream)
-                : launch_b<MT, 4, false>(p, grid, out_bf16, count, stream);
+hipError_t launch_m(const DecodeParams& p, int grid, int ns, int waves, bool tile, hipStream_t stream) {
+    if (ns == 2) return tile ? launch_w<MT, 2, true>(p, grid, waves, stream)
+                             : launch_w<MT, 2, false>(p, grid, waves, stream);
+    return tile ? launch_w<MT, 4, true>(p, grid, waves, stream)
+                : launch_w<MT, 4, false>(p, grid, waves, stream);
 }
 
 }  // namespace
@@ -306,13 +311,14 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.log2_bc = tile ? d.L.log2_bc : 0;
     p.log2_G = tile ? d.L.log2_G : 0;
     p.bc_mask = tile ? int(d.L.bc - 1) : 0;
+    p.out_bf16 = d.out_bf16;
     const int grid = int(d.N / d.tile_n) * d.split_k;
     const int ns = d.tile_n / 16;
     hipError_t e;
     switch (d.m_tiles16) {
-        case 1: e = launch_m<1>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream); break;
-        case 2: e = launch_m<2>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream); break;
-        default: e = launch_m<4>(p, grid, ns, tile, d.out_bf16, d.fetch != nullptr, stream); break;
+        case 1: e = launch_m<1>(p, grid, ns, d.waves, tile, stream); break;
+        case 2: e = launch_m<2>(p, grid, ns, d.waves, tile, stream); break;
+        default: e = launch_m<4>(p, grid, ns, d.waves, tile, stream); break;
     }
     if (e != hipSuccess || d.split_k == 1) return e;
     const int64_t mn4 = d.M * d.N / 4;

@@ -50,6 +50,7 @@ struct DecodeLaunch {
     Layout L;
     int tile_n;                 // 32 or 64
     int m_tiles16;              // ceil(M / 16): 1, 2 or 4
+    int waves;                  // wavefronts per workgroup: 4, 8 or 16 (K split inside)
     int split_k;
     int64_t k_unit;             // K granularity of a split, in elements
     bool out_bf16;

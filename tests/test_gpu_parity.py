@@ -124,6 +124,23 @@ def test_decode_tile_major_parity(M, N, K):
     parity(host_f32(C), y_ref, f"decode M={M}")
 
 
+@pytest.mark.parametrize("M", [1, 8, 32, 64])
+@pytest.mark.parametrize("N", [8192, 16384])
+def test_decode_in_workgroup_k_split(M, N):
+    """256 or 512 tiles: one workgroup per tile, 16 or 8 waves splitting K."""
+    K = 1024
+    d = tl.layout()
+    p = tl.tl_gemm_plan(M, N, K, d)
+    banner(f"decode M={M} N={N} waves={p['waves']} split_k={p['split_k']}")
+    assert p["split_k"] == 1 and p["waves"] in (8, 16)
+    A = synth.normal_bf16((M, K), seed=60 + M)
+    W = synth.normal_bf16((N, K), seed=61, sigma=synth.W_SIGMA)
+    parity(host_f32(run_gemm(A, W, d)), oracle.gemm_f64(A, W), f"M={M} N={N}")
+    Ai = synth.small_int_bf16((M, K), seed=62)
+    Wi = synth.small_int_bf16((N, K), seed=63)
+    assert np.array_equal(host_f32(run_gemm(Ai, Wi, d)).astype(np.float64), oracle.gemm_f64(Ai, Wi))
+
+
 @pytest.mark.parametrize("split_k", [1, 2, 3, 7, 16])
 def test_decode_split_k_parity_and_reproducible(split_k):
     M, N, K = 8, 512, 4096

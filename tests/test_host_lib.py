@@ -113,13 +113,17 @@ def test_read_amp_rejects_bad_arguments():
 def test_gemm_plan_decode_and_prefill_shapes():
     d = tl.layout()
     # Llama-70B-shaped decode at M = 8: whole memory tiles per compute tile
-    for N, K, S in [(10240, 8192, 4), (8192, 8192, 4), (57344, 8192, 1), (8192, 28672, 4)]:
+    for N, K, S, waves in [(10240, 8192, 4, 4), (8192, 8192, 1, 16), (57344, 8192, 1, 4),
+                           (8192, 28672, 1, 16)]:
         p = tl.tl_gemm_plan(8, N, K, d)
         assert p["kernel"] == 1 and p["tile_n"] == 32 and p["tile_k"] == 64
-        assert p["split_k"] == S
+        assert p["split_k"] == S and p["waves"] == waves
         assert p["workgroups"] % 256 == 0
         amp = tl.tl_read_amp(8, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, 4096)
         assert amp["amp"] == 1.0
+    # 512 tiles -> 8 waves; the LDS reduction buffer caps waves at M = 64
+    assert tl.tl_gemm_plan(8, 16384, 1024, d)["waves"] == 8
+    assert tl.tl_gemm_plan(64, 8192, 1024, d)["waves"] == 8
     p = tl.tl_gemm_plan(2048, 57344, 8192, d)
     assert p["kernel"] == 2 and p["tile_m"] == 256 and p["tile_n"] == 128
     p = tl.tl_gemm_plan(2048, 57344, 8192, tl.layout(tile_m=128))
