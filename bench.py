@@ -12,7 +12,7 @@ times is timed too and reported beside it.
 
 value = algorithmic bytes (2NK + 2MK + 4MN summed over the four GEMMs) per
 second over the K timed steps, in GB/s.  Also reported: prefill TFLOP/s at
-M = 2048 (tiles 256x128x64 and 128x128x64, bf16 out), read amplification of
+M = 2048 (tiles 256x256x64, 256x128x64 and 128x128x64, bf16 out), read amplification of
 the decode compute tile and of the paper's 128 x 256 tile, repack GB/s, the
 decode kernel's roofline, and the CPU oracle timed on a bounded sample.
 
@@ -207,8 +207,8 @@ def main():
             pacts.append(torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev))
         pouts = [torch.empty((Mp, N), dtype=torch.bfloat16, device=dev) for (_, N, _, _) in weights]
         flops = sum(2.0 * Mp * N * K for (_, N, K, _) in weights)
-        for tm in (256, 128):
-            pd = tl.layout(G=G, block_rows=BR, tile_m=tm, out_dtype=tl.TL_OUT_BF16)
+        for tm, tn in ((256, 256), (256, 128), (128, 128)):
+            pd = tl.layout(G=G, block_rows=BR, tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16)
             for _ in range(2):
                 for (name, N, K, Wt), A, C in zip(weights, pacts, pouts):
                     tl.tl_gemm(A, Wt, C, Mp, N, K, pd, tl.TL_FETCH_BLOCK)
@@ -226,12 +226,12 @@ def main():
                     tot[j] += pev[j][0].elapsed_time(pev[j][1])
             ms = sum(tot) / reps
             tf = flops / (ms * 1e-3) / 1e12
-            prefill[f"tile_{tm}x128x64"] = {
+            prefill[f"tile_{tm}x{tn}x64"] = {
                 "TFLOP/s": round(tf, 1), "frac_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
                 "layer_ms": round(ms, 3),
                 "per_shape_TFLOP/s": {name: round(2.0 * Mp * N * K / (t / reps * 1e-3) / 1e12, 1)
                                       for (name, N, K, _), t in zip(weights, tot)}}
-            log(f"prefill tile {tm}: {tf:.1f} TFLOP/s")
+            log(f"prefill tile {tm}x{tn}: {tf:.1f} TFLOP/s")
         del pacts, pouts
 
     # ---------------- HBM copy calibration (for rocprofv3 counters) ---------

@@ -203,11 +203,13 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.pub.kernel = 2;
         int tm = d->tile_m ? d->tile_m : (M >= 1024 ? 256 : 128);
         if (tm != 128 && tm != 256) return TL_EUNSUPPORTED;
-        int tn = d->tile_n ? d->tile_n : 128;
-        if (tn != 128) return TL_EUNSUPPORTED;
+        int tn = d->tile_n ? d->tile_n : ((tm == 256 && N % 256 == 0) ? 256 : 128);
+        if (tn != 128 && !(tn == 256 && tm == 256)) return TL_EUNSUPPORTED;
         if (tile && tn % p.L.br) return TL_EUNSUPPORTED;
         if (d->tile_k && d->tile_k != p.k_unit) return TL_EUNSUPPORTED;
         if (d->split_k > 1) return TL_EUNSUPPORTED;
+        // the kernel addresses A and W with 32-bit byte offsets
+        if (M * K * 2 >= (int64_t(1) << 32) || N * K * 2 >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;
         p.pub.tile_m = tm;
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
@@ -291,6 +293,7 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
         q.K = K;
         q.L = p.L;
         q.tile_m = p.pub.tile_m;
+        q.tile_n = p.pub.tile_n;
         q.out_bf16 = p.out_bf16;
         e = launch_prefill(q, s);
     }

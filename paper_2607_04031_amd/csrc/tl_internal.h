@@ -66,6 +66,7 @@ struct PrefillLaunch {
     int64_t M, N, K;
     Layout L;
     int tile_m;                 // 128 or 256
+    int tile_n;                 // 128 or 256 (256 only with tile_m 256)
     bool out_bf16;
 };
 

@@ -3,17 +3,20 @@
 // batch (TileLens Section 6.2: the dense FFN becomes compute-bound as the batch
 // grows).
 //
-// Workgroup tile BM x 128 x 64 (BM = 128 or 256), 4 wavefronts in a 2 x 2
-// grid, each owning a (BM/2) x 64 block of C as (BM/64) x 2 MFMA 32x32 tiles.
+// Workgroup tile BM x BN x 64: 128x128 and 256x128 with 4 wavefronts in a
+// 2 x 2 grid, 256x256 with 8 wavefronts in a 2 x 4 grid (two per SIMD, so one
+// wave's MFMAs cover the other's LDS and barrier waits); each wave owns a block
+// of C as MFMA 32x32 tiles.
 // Per 64-wide K step the workgroup stages its A tile and its weight tile in
 // LDS; the weight tile of a (64, 32) BF16 memory tile layout is exactly four
 // whole 4 KB memory tiles, so each wavefront load instruction reads 1 KB of
 // one contiguous memory tile.  Per-lane weight addresses are Eq. 2 with shifts
 // and masks (Section 3.2).  The next K step's global loads are issued before
 // the current step's MFMAs (register double buffering; LDS is double buffered
-// so one barrier per step suffices).  LDS rows are 128 B; 16-byte chunks are
-// XOR-swizzled by (row mod 8) so the MFMA operand reads of 8 consecutive rows
-// hit 8 different bank groups.
+// so one barrier per step suffices); LDS operand fragments for the next
+// 16-wide sub-step are read while the current sub-step's MFMAs run.  LDS rows
+// are 128 B with 16-byte chunks XOR-swizzled (see swz) so operand reads are
+// free of bank conflicts.
 #include <hip/hip_runtime.h>
 
 #include "tl_internal.h"
@@ -35,6 +38,7 @@ struct PrefillParams {
     int64_t strip_bytes;
     int log2_br, log2_bc, log2_G;
     int br_mask, bc_mask;
+    bool out_bf16;
 };
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
@@ -44,17 +48,26 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
     return uint16_t(u >> 16);
 }
 
-__device__ inline int swz(int row, int chunk) { return row * 128 + ((chunk ^ (row & 7)) << 4); }
+// LDS byte offset of 16-byte chunk 'chunk' (0..7) of 128-byte row 'row'.
+// gfx950 serves a 16-byte-per-lane LDS read 16 lanes at a time across 64
+// four-byte banks (256 B): rows r and r + 1 fall in different halves, so the
+// chunk is XORed with (r / 2) mod 8 to give the 16 rows an MFMA operand read
+// touches 16 distinct 16-byte bank groups.
+__device__ inline int swz(int row, int chunk) { return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4); }
 
-template <int BM, bool TILE, bool OUT_BF16, bool COUNT>
-__global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
-    constexpr int BN = 128, BK = 64;
+template <int BM, int BN, int WGM, int WGN, bool TILE>
+__global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p) {
+    constexpr int NT = 64 * WGM * WGN;   // threads; waves form a WGM x WGN grid
+    constexpr int BK = 64;
     constexpr int A_BYTES = BM * BK * 2, W_BYTES = BN * BK * 2;
-    constexpr int A_CH = BM * 8 / 256;   // 16-byte chunks per thread per K step
-    constexpr int W_CH = BN * 8 / 256;
-    constexpr int FM = BM / 64;          // 32-row MFMA tiles per wave
-    constexpr int FN = 2;                // 32-col MFMA tiles per wave
-    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (A_BYTES + W_BYTES)];
+    constexpr int STAGE = A_BYTES + W_BYTES;
+    constexpr int A_CH = BM * 8 / NT;    // 16-byte chunks per thread per K step
+    constexpr int W_CH = BN * 8 / NT;
+    constexpr int ROWS = NT / 8;         // rows one pass of the workgroup stages
+    constexpr int WM = BM / WGM, WN = BN / WGN;   // wave tile
+    constexpr int FM = WM / 32;          // 32-row MFMA tiles per wave
+    constexpr int FN = WN / 32;          // 32-col MFMA tiles per wave
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
 
     // XCD-aware order: workgroup b runs on XCD (b mod 8); give each XCD a
     // contiguous range of tiles so neighbouring tiles share that XCD's L2.
@@ -63,32 +76,17 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
     const int tm = lb % p.m_tiles, tn = lb / p.m_tiles;
     const int m0 = tm * BM, n0 = tn * BN;
 
+    // Thread t stages 16-byte chunk c = t % 8 of rows r = t / 8 + ROWS i of
+    // both tiles (i < A_CH, i < W_CH).  Row addresses are rebuilt per step from
+    // one base so they cost no registers; rows past M or N are clamped (their
+    // results are never stored).
     const int t = threadIdx.x;
-    const uint16_t* a_src[A_CH];
-    int a_lds[A_CH];
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i) {
-        const int q = t + 256 * i, row = q >> 3, c = q & 7;
-        const int m = min(m0 + row, p.M - 1);
-        a_src[i] = p.A + int64_t(m) * p.K + c * 8;
-        a_lds[i] = swz(row, c);
-    }
-    const uint8_t* w_src[W_CH];
-    int w_k[W_CH], w_lds[W_CH];
-#pragma unroll
-    for (int i = 0; i < W_CH; ++i) {
-        const int q = t + 256 * i, row = q >> 3, c = q & 7;
-        const int n = min(n0 + row, p.N - 1);
-        int64_t off;
-        if (TILE) off = int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & p.br_mask) << (p.log2_bc + 1));
-        else off = int64_t(n) * p.K * 2;
-        w_src[i] = p.W + off;
-        w_k[i] = c * 8;
-        w_lds[i] = swz(row, c);
-    }
+    const int r0 = t >> 3, c0 = t & 7;
+    const int a_lds0 = swz(r0, c0);      // row r0 + ROWS i sits ROWS * 128 * i bytes further
+    const int w_k = c0 * 8;
 
     const int lane = t & 63, wave = t >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
     f32x16 acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -97,103 +95,143 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    // prefetch registers for the next K step (kept in VGPRs: plain scalars
-    // indexed only by unrolled constants)
+    // prefetch registers for the next K step (native vectors indexed only by
+    // unrolled constants, so they stay in VGPRs)
     u32x4 ra[A_CH], rw[W_CH];
+    // 32-bit byte offsets from the (uniform) base pointers: A and W are
+    // below 4 GB (checked on the host), and 32-bit offsets halve the
+    // registers the hoisted row addresses take.
+    const uint8_t* Ab = reinterpret_cast<const uint8_t*>(p.A);
+    auto a_addr = [&](int i, int k0) {
+        const uint32_t m = uint32_t(min(m0 + r0 + ROWS * i, p.M - 1));
+        return reinterpret_cast<const u32x4*>(Ab + (m * uint32_t(p.K) + uint32_t(k0 + w_k)) * 2u);
+    };
+    auto w_addr = [&](int i, uint32_t ko) {
+        const uint32_t n = uint32_t(min(n0 + r0 + ROWS * i, p.N - 1));
+        uint32_t off;
+        if (TILE) off = (n >> p.log2_br) * uint32_t(p.strip_bytes) + ((n & uint32_t(p.br_mask)) << (p.log2_bc + 1));
+        else off = n * uint32_t(p.K) * 2u;
+        return reinterpret_cast<const u32x4*>(p.W + (off + ko));
+    };
+    auto w_koff = [&](int k) -> uint32_t {
+        if (TILE) return (uint32_t(k >> p.log2_bc) << p.log2_G) + uint32_t((k & p.bc_mask) << 1);
+        return uint32_t(k) << 1;
+    };
+    const int KT = p.K / BK;
+    auto gload = [&](int kstep) {
+        const int k0 = kstep * BK;
 #pragma unroll
-    for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
+        for (int i = 0; i < A_CH; ++i) ra[i] = *a_addr(i, k0);
+        const uint32_t ko = w_koff(k0 + w_k);
 #pragma unroll
-    for (int i = 0; i < W_CH; ++i) {
-        const int k = w_k[i];
-        int64_t ko;
-        if (TILE) ko = (int64_t(k >> p.log2_bc) << p.log2_G) + int64_t((k & p.bc_mask) << 1);
-        else ko = int64_t(k) << 1;
-        rw[i] = *reinterpret_cast<const u32x4*>(w_src[i] + ko);
-    }
+        for (int i = 0; i < W_CH; ++i) rw[i] = *w_addr(i, ko);
+    };
+    auto sstore = [&](int buf) {
+        uint8_t* As = smem + buf * STAGE;
 #pragma unroll
-    for (int i = 0; i < A_CH; ++i) *reinterpret_cast<u32x4*>(smem + a_lds[i]) = ra[i];
+        for (int i = 0; i < A_CH; ++i) *reinterpret_cast<u32x4*>(As + a_lds0 + ROWS * 128 * i) = ra[i];
 #pragma unroll
-    for (int i = 0; i < W_CH; ++i) *reinterpret_cast<u32x4*>(smem + A_BYTES + w_lds[i]) = rw[i];
+        for (int i = 0; i < W_CH; ++i) *reinterpret_cast<u32x4*>(As + A_BYTES + a_lds0 + ROWS * 128 * i) = rw[i];
+    };
+    // Pipeline: LDS buffer kt % 2 holds K step kt; the registers hold step
+    // kt + 1, loaded one iteration earlier.  Each iteration first writes them
+    // to the other buffer (free: every wave passed the previous barrier), then
+    // issues the loads of step kt + 2, then runs step kt's MFMAs -- so the LDS
+    // writes overlap the MFMAs and each global load has a full iteration to
+    // arrive.
+    gload(0);
+    sstore(0);
+    if (KT > 1) gload(1);
     __syncthreads();
 
-    const int KT = p.K / BK;
+    // LDS read offsets of this lane's operand rows (chunk added per sub-step)
+    int a_row[FM], w_row[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) a_row[i] = wm * WM + i * 32 + (lane & 31);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) w_row[j] = wn * WN + j * 32 + (lane & 31);
+    const int khalf = lane >> 5;
+
     for (int kt = 0; kt < KT; ++kt) {
         const int buf = kt & 1;
-        const bool more = kt + 1 < KT;
-        if (more) {
-            const int k0 = (kt + 1) * BK;
-#pragma unroll
-            for (int i = 0; i < A_CH; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + k0);
-#pragma unroll
-            for (int i = 0; i < W_CH; ++i) {
-                const int k = k0 + w_k[i];
-                int64_t ko;
-                if (TILE) ko = (int64_t(k >> p.log2_bc) << p.log2_G) + int64_t((k & p.bc_mask) << 1);
-                else ko = int64_t(k) << 1;
-                rw[i] = *reinterpret_cast<const u32x4*>(w_src[i] + ko);
-            }
-        }
-        const uint8_t* As = smem + buf * (A_BYTES + W_BYTES);
+        if (kt + 1 < KT) sstore(buf ^ 1);
+        if (kt + 2 < KT) gload(kt + 2);
+        const uint8_t* As = smem + buf * STAGE;
         const uint8_t* Ws = As + A_BYTES;
+        // Operand fragments of the next 16-wide sub-step are read while the
+        // current one's MFMAs run (double-buffered) unless the 128x128 wave
+        // tile leaves no registers for it.
+        constexpr bool kDoubleFrag = FM * FN <= 8;
+        bf16x8 af[2][FM], bfr[2][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[0][i] = *reinterpret_cast<const bf16x8*>(As + swz(a_row[i], khalf));
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bfr[0][j] = *reinterpret_cast<const bf16x8*>(Ws + swz(w_row[j], khalf));
 #pragma unroll
         for (int s = 0; s < BK / 16; ++s) {
-            const int chunk = s * 2 + (lane >> 5);
-            bf16x8 af[FM], bfr[FN];
+            const int cur = kDoubleFrag ? (s & 1) : 0, nxt = kDoubleFrag ? (cur ^ 1) : 0;
+            if (kDoubleFrag && s + 1 < BK / 16) {
+                const int chunk = (s + 1) * 2 + khalf;
 #pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int row = wm * (BM / 2) + i * 32 + (lane & 31);
-                af[i] = *reinterpret_cast<const bf16x8*>(As + swz(row, chunk));
+                for (int i = 0; i < FM; ++i) af[nxt][i] = *reinterpret_cast<const bf16x8*>(As + swz(a_row[i], chunk));
+#pragma unroll
+                for (int j = 0; j < FN; ++j) bfr[nxt][j] = *reinterpret_cast<const bf16x8*>(Ws + swz(w_row[j], chunk));
             }
+            if (!kDoubleFrag && s > 0) {
+                const int chunk = s * 2 + khalf;
 #pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int row = wn * 64 + j * 32 + (lane & 31);
-                bfr[j] = *reinterpret_cast<const bf16x8*>(Ws + swz(row, chunk));
+                for (int i = 0; i < FM; ++i) af[0][i] = *reinterpret_cast<const bf16x8*>(As + swz(a_row[i], chunk));
+#pragma unroll
+                for (int j = 0; j < FN; ++j) bfr[0][j] = *reinterpret_cast<const bf16x8*>(Ws + swz(w_row[j], chunk));
             }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-        }
-        if (more) {
-            uint8_t* An = smem + (buf ^ 1) * (A_BYTES + W_BYTES);
-#pragma unroll
-            for (int i = 0; i < A_CH; ++i) *reinterpret_cast<u32x4*>(An + a_lds[i]) = ra[i];
-#pragma unroll
-            for (int i = 0; i < W_CH; ++i) *reinterpret_cast<u32x4*>(An + A_BYTES + w_lds[i]) = rw[i];
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
         }
         __syncthreads();
     }
 
-    if (COUNT && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)W_BYTES);
+    if (p.fetch && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)W_BYTES);
 
     // D layout of a 32x32 MFMA tile: lane l, register v holds
     // row 8*(v/4) + 4*(l/32) + v%4, column l%32.
+    const bool full = m0 + BM <= p.M && n0 + BN <= p.N;
+    const int row_base = m0 + wm * WM + 4 * (lane >> 5);
+    const int col_base = n0 + wn * WN + (lane & 31);
+    if (p.out_bf16) {
+        uint16_t* C = static_cast<uint16_t*>(p.C);
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+        for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+            for (int j = 0; j < FN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int row = m0 + wm * (BM / 2) + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-                if (row < p.M && col < p.N) {
-                    const int64_t idx = int64_t(row) * p.N + col;
-                    if (OUT_BF16) static_cast<uint16_t*>(p.C)[idx] = f32_to_bf16_rne(acc[i][j][v]);
-                    else static_cast<float*>(p.C)[idx] = acc[i][j][v];
+                for (int v = 0; v < 16; ++v) {
+                    const int row = row_base + i * 32 + 8 * (v >> 2) + (v & 3);
+                    const int col = col_base + j * 32;
+                    if (full || (row < p.M && col < p.N))
+                        C[int64_t(row) * p.N + col] = f32_to_bf16_rne(acc[i][j][v]);
                 }
-            }
+    } else {
+        float* C = static_cast<float*>(p.C);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = row_base + i * 32 + 8 * (v >> 2) + (v & 3);
+                    const int col = col_base + j * 32;
+                    if (full || (row < p.M && col < p.N)) C[int64_t(row) * p.N + col] = acc[i][j][v];
+                }
+    }
 }
 
-template <int BM, bool TILE>
-hipError_t launch_t(const PrefillParams& p, int grid, bool out_bf16, bool count, hipStream_t s) {
-    if (out_bf16) {
-        if (count) hipLaunchKernelGGL((prefill_kernel<BM, TILE, true, true>), dim3(grid), dim3(256), 0, s, p);
-        else hipLaunchKernelGGL((prefill_kernel<BM, TILE, true, false>), dim3(grid), dim3(256), 0, s, p);
-    } else {
-        if (count) hipLaunchKernelGGL((prefill_kernel<BM, TILE, false, true>), dim3(grid), dim3(256), 0, s, p);
-        else hipLaunchKernelGGL((prefill_kernel<BM, TILE, false, false>), dim3(grid), dim3(256), 0, s, p);
-    }
+template <int BM, int BN, int WGM, int WGN>
+hipError_t launch_t(const PrefillParams& p, int grid, bool tile, hipStream_t s) {
+    if (tile) hipLaunchKernelGGL((prefill_kernel<BM, BN, WGM, WGN, true>), dim3(grid), dim3(64 * WGM * WGN), 0, s, p);
+    else hipLaunchKernelGGL((prefill_kernel<BM, BN, WGM, WGN, false>), dim3(grid), dim3(64 * WGM * WGN), 0, s, p);
     return hipGetLastError();
 }
 
@@ -216,12 +254,13 @@ hipError_t launch_prefill(const PrefillLaunch& q, hipStream_t stream) {
     p.log2_G = tile ? q.L.log2_G : 0;
     p.br_mask = tile ? int(q.L.br - 1) : 0;
     p.bc_mask = tile ? int(q.L.bc - 1) : 0;
-    const int64_t n_tiles = (q.N + 127) / 128;
+    p.out_bf16 = q.out_bf16;
+    const int64_t n_tiles = (q.N + q.tile_n - 1) / q.tile_n;
     const int grid = int(p.m_tiles * n_tiles);
-    if (q.tile_m == 256) return tile ? launch_t<256, true>(p, grid, q.out_bf16, q.fetch, stream)
-                                     : launch_t<256, false>(p, grid, q.out_bf16, q.fetch, stream);
-    return tile ? launch_t<128, true>(p, grid, q.out_bf16, q.fetch, stream)
-                : launch_t<128, false>(p, grid, q.out_bf16, q.fetch, stream);
+    // 256x256: 8 waves (2 per SIMD) of 128x64; smaller tiles: 4 waves in 2 x 2
+    if (q.tile_m == 256 && q.tile_n == 256) return launch_t<256, 256, 2, 4>(p, grid, tile, stream);
+    if (q.tile_m == 256) return launch_t<256, 128, 2, 2>(p, grid, tile, stream);
+    return launch_t<128, 128, 2, 2>(p, grid, tile, stream);
 }
 
 }  // namespace tl

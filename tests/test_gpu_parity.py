@@ -247,23 +247,24 @@ def test_decode_fetch_counter_equals_read_amp():
 # ---------------------------------------------------------------------------
 
 PREFILL_SHAPES = [
-    # M, N, K, tile_m
-    (256, 1024, 1024, 128), (256, 1024, 1024, 256),
-    (300, 512, 2048, 128), (300, 512, 2048, 256),    # ragged M tail
-    (65, 256, 512, 128),                              # just above the decode limit
-    (512, 1056, 512, 256),                            # ragged N tail (N % 128 = 32)
+    # M, N, K, tile_m, tile_n
+    (256, 1024, 1024, 128, 128), (256, 1024, 1024, 256, 128), (512, 1024, 1024, 256, 256),
+    (300, 512, 2048, 128, 128), (300, 512, 2048, 256, 128),    # ragged M tail
+    (300, 768, 1024, 256, 256),
+    (65, 256, 512, 128, 128),                                  # just above the decode limit
+    (512, 1056, 512, 256, 128), (512, 1056, 512, 256, 256),    # ragged N tail (N % 128 = 32)
 ]
 
 
-@pytest.mark.parametrize("M,N,K,tm", PREFILL_SHAPES)
-def test_prefill_tile_major_parity(M, N, K, tm):
-    banner(f"prefill M={M} N={N} K={K} tile_m={tm}")
+@pytest.mark.parametrize("M,N,K,tm,tn", PREFILL_SHAPES)
+def test_prefill_tile_major_parity(M, N, K, tm, tn):
+    banner(f"prefill M={M} N={N} K={K} tile={tm}x{tn}")
     A = synth.normal_bf16((M, K), seed=21)
     W = synth.normal_bf16((N, K), seed=22, sigma=synth.W_SIGMA)
     y_ref = oracle.gemm_f64(A, W)
-    C = host_f32(run_gemm(A, W, tl.layout(tile_m=tm)))
-    parity(C, y_ref, f"prefill tm={tm}")
-    Cb = run_gemm(A, W, tl.layout(tile_m=tm, out_dtype=tl.TL_OUT_BF16))
+    C = host_f32(run_gemm(A, W, tl.layout(tile_m=tm, tile_n=tn)))
+    parity(C, y_ref, f"prefill {tm}x{tn}")
+    Cb = run_gemm(A, W, tl.layout(tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16))
     parity_bf16_out(host_bits(Cb), y_ref, "prefill bf16")
 
 
@@ -276,8 +277,9 @@ def test_prefill_exact_inputs():
                           oracle.gemm_f64(A, W))
     A = synth.small_int_bf16((M, K), seed=25)
     W = synth.small_int_bf16((N, K), seed=26)
-    assert np.array_equal(host_f32(run_gemm(A, W, tl.layout(tile_m=256))).astype(np.float64),
-                          oracle.gemm_f64(A, W))
+    for tn in (128, 256):
+        assert np.array_equal(host_f32(run_gemm(A, W, tl.layout(tile_m=256, tile_n=tn))).astype(np.float64),
+                              oracle.gemm_f64(A, W))
 
 
 @pytest.mark.parametrize("G,br", [(4096, 8), (16384, 32), (1024, 16), (512, 32)])
@@ -350,11 +352,12 @@ def test_llama_prefill_full_size_sampled(i, name, N, K):
     M = synth.LLAMA_PREFILL_M
     A_bits = synth.normal_bf16((M, K), seed=synth.llama_prefill_act_seed(i))
     A = dev_bf16(A_bits)
-    for tm in (128, 256):
+    for tm, tn in ((128, 128), (256, 128), (256, 256)):
         C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-        tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(tile_m=tm, out_dtype=tl.TL_OUT_BF16), tl.TL_FETCH_BLOCK)
+        tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16),
+                   tl.TL_FETCH_BLOCK)
         _sync()
-        _sampled_check(A_bits, W_bits, C, 512, seed=tm + i, bf16_out=True)
+        _sampled_check(A_bits, W_bits, C, 512, seed=tm + tn + i, bf16_out=True)
 
 
 # ---------------------------------------------------------------------------

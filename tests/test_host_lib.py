@@ -125,7 +125,8 @@ def test_gemm_plan_decode_and_prefill_shapes():
     assert tl.tl_gemm_plan(8, 16384, 1024, d)["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, d)["waves"] == 8
     p = tl.tl_gemm_plan(2048, 57344, 8192, d)
-    assert p["kernel"] == 2 and p["tile_m"] == 256 and p["tile_n"] == 128
+    assert p["kernel"] == 2 and p["tile_m"] == 256 and p["tile_n"] == 256
+    assert tl.tl_gemm_plan(2048, 57344 + 128, 8192, d)["tile_n"] == 128
     p = tl.tl_gemm_plan(2048, 57344, 8192, tl.layout(tile_m=128))
     assert p["tile_m"] == 128
 
