@@ -163,7 +163,11 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.pub.kernel = 1;
         p.m_tiles16 = int((M + 15) / 16);
         if (p.m_tiles16 == 3) p.m_tiles16 = 4;
-        int tn = d->tile_n ? d->tile_n : int(tile ? std::max<int64_t>(32, p.L.br) : 32);
+        // 64-row tiles halve the activation reloads per weight byte, which
+        // pays off once M exceeds one 16-row MFMA tile
+        int tn_default = p.m_tiles16 >= 2 && N % 64 == 0 ? 64 : 32;
+        if (tile) tn_default = int(std::max<int64_t>(tn_default, p.L.br));
+        int tn = d->tile_n ? d->tile_n : tn_default;
         if (tn != 32 && tn != 64) return TL_EUNSUPPORTED;
         if (tile && tn % p.L.br) return TL_EUNSUPPORTED;
         if (N % tn) return TL_EUNSUPPORTED;
@@ -190,7 +194,11 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         const int64_t wgs = n_tiles * S;
         const int ns = tn / 16;
         int waves = wgs <= kCUs ? 16 : (wgs <= 2 * kCUs ? 8 : 4);
-        while (waves > 4 && waves * p.m_tiles16 * ns > 64) waves /= 2;   // LDS reduction buffer <= 64 KB
+        // registers: 16 waves (4 per SIMD, <= 128 VGPRs) only fit one 16-row
+        // M tile x 32 rows of N; 8 waves (<= 256 VGPRs) fit up to 8 of those
+        const int mn = p.m_tiles16 * ns / 2;
+        if (waves == 16 && mn > 1) waves = 8;
+        if (waves == 8 && mn > 4) waves = 4;
         p.waves = waves;
         p.pub.tile_m = 16 * p.m_tiles16;
         p.pub.tile_n = tn;

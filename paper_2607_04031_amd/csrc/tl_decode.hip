@@ -127,14 +127,21 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
             else off = int64_t(n) * p.K * 2;
             wrow[j][hf] = p.W + off;
         }
-    const uint16_t* arow[MT];
-    bool aok[MT];
+    // Activations are loaded like the weights (8 rows x 128 B per
+    // instruction, then the lane exchange): lane (g, q) reads row
+    // 16 mt + 8 hf + (q & 7) at this lane's chunk kc.  Rows past M read zeros;
+    // a half-tile that is entirely past M is not loaded at all.
+    const uint16_t* arow[MT][2];
+    bool aok[MT][2], aany[MT][2];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + q;
-        aok[mt] = m < p.M;
-        arow[mt] = p.A + int64_t(aok[mt] ? m : 0) * p.K + g * 8;
-    }
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            const int m = mt * 16 + hf * 8 + (q & 7);
+            aok[mt][hf] = m < p.M;
+            aany[mt][hf] = mt * 16 + hf * 8 < p.M;
+            arow[mt][hf] = p.A + int64_t(aok[mt][hf] ? m : 0) * p.K + kc;
+        }
 
     f32x4 acc[MT][NS];
 #pragma unroll
@@ -147,23 +154,40 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     const int nsteps = st1 - st0 - wave > 0 ? (st1 - st0 - wave + kWaves - 1) / kWaves : 0;
     int st = st0 + wave;
     int i = 0;
-    auto compute = [&](const bf16x8 (&x)[NS][2], const bf16x8 (&a)[2][MT]) {
+    auto exchange = [&](const bf16x8& x0, const bf16x8& x1, bf16x8& o0, bf16x8& o1) {
+        const bf16x8 t = lo ? x1 : x0;
+        const bf16x8 s = swap8(t);
+        o0 = lo ? x0 : s;
+        o1 = lo ? s : x1;
+    };
+    auto compute = [&](const bf16x8 (&x)[NS][2], const bf16x8 (&xa)[MT][2]) {
+        bf16x8 a0[MT], a1[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) exchange(xa[mt][0], xa[mt][1], a0[mt], a1[mt]);
 #pragma unroll
         for (int j = 0; j < NS; ++j) {
-            const bf16x8 t = lo ? x[j][1] : x[j][0];
-            const bf16x8 s = swap8(t);
-            const bf16x8 b0 = lo ? x[j][0] : s;
-            const bf16x8 b1 = lo ? s : x[j][1];
+            bf16x8 b0, b1;
+            exchange(x[j][0], x[j][1], b0, b1);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0][mt], b0, acc[mt][j], 0, 0, 0);
-                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1][mt], b1, acc[mt][j], 0, 0, 0);
+                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[mt], b0, acc[mt][j], 0, 0, 0);
+                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[mt], b1, acc[mt][j], 0, 0, 0);
             }
         }
     };
+    auto load_a = [&](int k, bf16x8 (&xa)[MT][2]) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf)
+                if (aany[mt][hf])   // uniform: skips the load when the half-tile is past M
+                    xa[mt][hf] = aok[mt][hf] ? *reinterpret_cast<const bf16x8*>(arow[mt][hf] + k) : zero8;
+                else
+                    xa[mt][hf] = zero8;
+    };
     for (; i + U <= nsteps; i += U) {
         bf16x8 x[U][NS][2];
-        bf16x8 a[U][2][MT];
+        bf16x8 a[U][MT][2];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int k = (st + u * kWaves) * 64;
@@ -172,11 +196,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
             for (int j = 0; j < NS; ++j)
 #pragma unroll
                 for (int hf = 0; hf < 2; ++hf) x[u][j][hf] = load_stream(wrow[j][hf] + ko);
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    a[u][h][mt] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + k + h * 32) : zero8;
+            load_a(k, a[u]);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) compute(x[u], a[u]);
@@ -185,16 +205,12 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     for (; i < nsteps; ++i) {
         const int k = st * 64;
         const int64_t ko = w_koff<TILE>(p, k + kc);
-        bf16x8 x[NS][2], a[2][MT];
+        bf16x8 x[NS][2], a[MT][2];
 #pragma unroll
         for (int j = 0; j < NS; ++j)
 #pragma unroll
             for (int hf = 0; hf < 2; ++hf) x[j][hf] = load_stream(wrow[j][hf] + ko);
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                a[h][mt] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + k + h * 32) : zero8;
+        load_a(k, a);
         compute(x, a);
         st += kWaves;
     }
@@ -265,18 +281,19 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, voi
 
 template <int MT, int NS, int WAVES, bool TILE>
 hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
-    constexpr int U = MT >= 4 ? 2 : 4;
+    constexpr int U = MT >= 2 ? 2 : 4;   // steps in flight per wave; fewer for larger M (registers)
     hipLaunchKernelGGL((decode_kernel<MT, NS, U, WAVES, TILE>), dim3(grid), dim3(64 * WAVES), 0, stream, p);
     return hipGetLastError();
 }
 
-// Instantiated (MT, NS, waves) combinations; the planner only asks for these.
+// Instantiated (MT, NS, waves) combinations -- those whose registers fit
+// the waves per SIMD they need; the planner only asks for these.
 template <int MT, int NS, bool TILE>
 hipError_t launch_w(const DecodeParams& p, int grid, int waves, hipStream_t stream) {
-    if constexpr (16 * MT * NS <= 64) {
+    if constexpr (MT * NS <= 2) {
         if (waves == 16) return launch_t<MT, NS, 16, TILE>(p, grid, stream);
     }
-    if constexpr (8 * MT * NS <= 64) {
+    if constexpr (MT * NS <= 8) {
         if (waves == 8) return launch_t<MT, NS, 8, TILE>(p, grid, stream);
     }
     return launch_t<MT, NS, 4, TILE>(p, grid, stream);

@@ -167,6 +167,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
         for (int i = 0; i < FM; ++i) af[0][i] = *reinterpret_cast<const bf16x8*>(As + swz(a_row[i], khalf));
 #pragma unroll
         for (int j = 0; j < FN; ++j) bfr[0][j] = *reinterpret_cast<const bf16x8*>(Ws + swz(w_row[j], khalf));
+        // let the scheduler interleave the LDS operand reads with the MFMAs
+        __builtin_amdgcn_iglp_opt(1);
 #pragma unroll
         for (int s = 0; s < BK / 16; ++s) {
             const int cur = kDoubleFrag ? (s & 1) : 0, nxt = kDoubleFrag ? (cur ^ 1) : 0;

@@ -121,9 +121,12 @@ def test_gemm_plan_decode_and_prefill_shapes():
         assert p["workgroups"] % 256 == 0
         amp = tl.tl_read_amp(8, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, 4096)
         assert amp["amp"] == 1.0
-    # 512 tiles -> 8 waves; the LDS reduction buffer caps waves at M = 64
+    # 512 tiles -> 8 waves; registers cap waves as M and tile_n grow
     assert tl.tl_gemm_plan(8, 16384, 1024, d)["waves"] == 8
-    assert tl.tl_gemm_plan(64, 8192, 1024, d)["waves"] == 8
+    assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 64      # M > 16: 64-row tiles
+    assert tl.tl_gemm_plan(32, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
+    assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
+    assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64))["waves"] == 4
     p = tl.tl_gemm_plan(2048, 57344, 8192, d)
     assert p["kernel"] == 2 and p["tile_m"] == 256 and p["tile_n"] == 256
     assert tl.tl_gemm_plan(2048, 57344 + 128, 8192, d)["tile_n"] == 128
