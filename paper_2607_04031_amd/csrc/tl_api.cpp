@@ -119,6 +119,8 @@ struct Plan {
     int m_tiles16 = 1;
     int waves = 4;
     int64_t k_unit = 64;
+    bool block_row = false;      // block-granular emulation on a row-major weight
+    int64_t fetch_G = 0;
 };
 
 constexpr int kDecodeMaxM = 64;
@@ -150,7 +152,13 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         if (p.L.bc < 8) return TL_EUNSUPPORTED;
     } else if (d->kind == TL_LAYOUT_NK_ROW) {
         p.L.kind = TL_LAYOUT_NK_ROW;
-        if (block) return TL_EUNSUPPORTED;
+        if (block) {
+            // whole G-byte blocks of the row-major weight; G >= 128 keeps each
+            // 128-byte row segment of a K step inside one block
+            if (!is_pow2(d->G) || d->G < 128 || d->G > (int64_t(1) << 30)) return TL_EINVAL;
+            p.block_row = true;
+            p.fetch_G = d->G;
+        }
     } else {
         return TL_EUNSUPPORTED;
     }
@@ -159,6 +167,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
     const bool tile = d->kind == TL_LAYOUT_TILE;
     p.k_unit = tile ? std::max<int64_t>(64, p.L.bc) : 64;
 
+    if (p.block_row && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;   // decode kernel only
     if (M <= kDecodeMaxM && d->tile_m <= 64) {
         p.pub.kernel = 1;
         p.m_tiles16 = int((M + 15) / 16);
@@ -289,6 +298,8 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
         d.split_k = p.pub.split_k;
         d.k_unit = p.k_unit;
         d.out_bf16 = p.out_bf16;
+        d.block_fetch = p.block_row;
+        d.fetch_G = p.fetch_G;
         e = launch_decode(d, s);
     } else {
         PrefillLaunch q;

@@ -54,6 +54,8 @@ struct DecodeLaunch {
     int split_k;
     int64_t k_unit;             // K granularity of a split, in elements
     bool out_bf16;
+    bool block_fetch;           // row-major weight read in whole fetch_G-byte blocks
+    int64_t fetch_G;
 };
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream);

@@ -129,7 +129,7 @@ def test_decode_tile_major_parity(M, N, K):
 def test_decode_in_workgroup_k_split(M, N):
     """256 or 512 tiles: one workgroup per tile, 16 or 8 waves splitting K."""
     K = 1024
-    d = tl.layout()
+    d = tl.layout(tile_n=32)
     p = tl.tl_gemm_plan(M, N, K, d)
     banner(f"decode M={M} N={N} waves={p['waves']} split_k={p['split_k']}")
     assert p["split_k"] == 1 and p["waves"] in (8, 16)
@@ -225,6 +225,27 @@ def test_decode_row_major_native(M):
     C = host_f32(run_gemm(A, W, tl.layout(kind=tl.TL_LAYOUT_NK_ROW), fetch=tl.TL_FETCH_NATIVE,
                           tile_major=False))
     parity(C, y_ref, f"NK_ROW M={M}")
+
+
+@pytest.mark.parametrize("M,N,K,G", [(8, 1024, 2048, 4096), (8, 512, 2048, 512), (1, 256, 4096, 16384),
+                                     (8, 512, 1024, 4096), (32, 512, 512, 8192), (5, 256, 2048, 128)])
+def test_decode_row_major_block_fetch_emulation(M, N, K, G):
+    """Row-major weight read in whole G-byte blocks: same result, and the
+    fetch tally equals tl_read_amp's fetched bytes for the kernel's tile
+    exactly (rows share a block when K * 2 < G)."""
+    banner(f"decode NK_ROW block fetch M={M} N={N} K={K} G={G}")
+    A = synth.normal_bf16((M, K), seed=70 + M)
+    W = synth.normal_bf16((N, K), seed=71, sigma=synth.W_SIGMA)
+    d = tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=G)
+    tl.tl_fetch_counter_read()
+    C = run_gemm(A, W, d, fetch=tl.TL_FETCH_BLOCK | tl.TL_FETCH_COUNT, tile_major=False)
+    got = tl.tl_fetch_counter_read()
+    parity(host_f32(C), oracle.gemm_f64(A, W), f"block fetch G={G}")
+    p = tl.tl_gemm_plan(M, N, K, d, tl.TL_FETCH_BLOCK)
+    amp = tl.tl_read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, G)
+    assert got == amp["fetched_bytes"]
+    want = oracle.read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], oracle.NK_ROW, G)
+    assert got == want["fetched_bytes"]
 
 
 def test_decode_fetch_counter_equals_read_amp():

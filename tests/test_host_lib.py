@@ -154,6 +154,17 @@ def test_gemm_plan_error_codes():
     with pytest.raises(tl.TLError) as e:
         tl.tl_gemm_plan(8, 64, 64, d, fetch_mode=0x8)
     assert e.value.status == tl.TL_EINVAL
+    # block-granular fetch on a row-major weight: G a power of two >= 128,
+    # decode kernel only
+    rm = tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=4096)
+    assert tl.tl_gemm_plan(8, 64, 64, rm, tl.TL_FETCH_BLOCK)["kernel"] == 1
+    for bad_G in (64, 100, 0):
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_plan(8, 64, 64, tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=bad_G), tl.TL_FETCH_BLOCK)
+        assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm_plan(256, 64, 64, rm, tl.TL_FETCH_BLOCK)
+    assert e.value.status == tl.TL_EUNSUPPORTED
 
 
 def test_entry_points_reject_before_device_work():
