@@ -11,12 +11,17 @@ eagerly on one stream; the same step captured as a HIP graph and replayed K
 times is timed too and reported beside it.
 
 value = algorithmic bytes (2NK + 2MK + 4MN summed over the four GEMMs) per
-second over the K timed steps, in GB/s.  Also reported: prefill TFLOP/s at
-M = 2048 (tiles 256x256x64, 256x128x64 and 128x128x64, bf16 out), read amplification of
-the decode compute tile and of the paper's 128 x 256 tile, repack GB/s, the
-decode kernel's roofline, and the CPU oracle timed on a bounded sample.
+second over the K timed steps, in GB/s.  Also reported: the same layer at
+M = 1 and M = 32; the M = 8 layer over row-major weights read natively and
+read in whole 4 KB blocks (a large-granularity memory emulated), with the
+fetch amplification the kernel counts; prefill TFLOP/s at M = 2048 (tiles
+256x256x64, 256x128x64, 128x128x64, bf16 out); a Qwen-3-30B-A3B-shaped MoE
+layer (64 tokens, top-8 of 128 experts, plus the attention projections);
+read amplification of the decode tile and of the paper's 128 x 256 tile;
+repack GB/s; the decode kernel's roofline; the CPU oracle on a bounded sample.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
+    python bench.py --sweep      # memory-tile granularity sweep, its own JSON line
 """
 import argparse
 import hashlib
@@ -60,124 +65,351 @@ def profiled_traffic(kernel_hash):
     return d.get("hbm_bytes_per_launch")
 
 
+class Ctx:
+    """torch, library and stream handles shared by the sections."""
+
+    def __init__(self):
+        import numpy as np
+        import torch
+
+        import paper_2607_04031_amd as tl
+        from paper_2607_04031_amd import synth
+        self.np, self.torch, self.tl, self.synth = np, torch, tl, synth
+        assert torch.cuda.is_available(), "bench.py needs a GPU"
+        tl.load_library()
+        self.dev = torch.device("cuda:0")
+        # all work on one side stream (default priority): graphs cannot be
+        # captured on the null stream
+        self.stream = torch.cuda.Stream(device=self.dev)
+        torch.cuda.set_stream(self.stream)
+
+    def to_dev(self, bits):
+        return self.torch.from_numpy(bits.view(self.np.int16)).view(self.torch.bfloat16).to(self.dev)
+
+    def event_pairs(self, n):
+        E = self.torch.cuda.Event
+        return [(E(enable_timing=True), E(enable_timing=True)) for _ in range(n)]
+
+
+def wall_time(ctx, fn, reps):
+    ctx.torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fn()
+    ctx.torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
+def launch_bytes(M, N, K):
+    return 2 * N * K + 2 * M * K + 4 * M * N
+
+
+def decode_layer(ctx, weights, M, steps, warmup, desc, event_pass=False):
+    """Eager layer steps at batch M over tile-major weights [(name, N, K, W)]."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    acts = [ctx.to_dev(synth.normal_bf16((M, K), seed=synth.llama_decode_act_seed(i, M)))
+            for i, (_, N, K, _) in enumerate(weights)]
+    outs = [torch.empty((M, N), dtype=torch.float32, device=ctx.dev) for (_, N, _, _) in weights]
+    lb = [launch_bytes(M, N, K) for (_, N, K, _) in weights]
+
+    def step(ev=None):
+        for j, ((_, N, K, W), A, C) in enumerate(zip(weights, acts, outs)):
+            if ev is not None:
+                ev[j][0].record(ctx.stream)
+            tl.tl_gemm(A, W, C, M, N, K, desc, tl.TL_FETCH_BLOCK)
+            if ev is not None:
+                ev[j][1].record(ctx.stream)
+
+    for _ in range(warmup):
+        step()
+    wall = wall_time(ctx, step, steps)
+    res = {"M": M, "GB/s": sum(lb) * steps / wall / 1e9, "ms_per_step": wall * 1e3 / steps,
+           "step_bytes": sum(lb), "launch_bytes": lb, "step": step}
+    if event_pass:
+        # per-launch durations from HIP events recorded on the launch stream
+        # around each tl_gemm call (a separate pass over the same launches)
+        evs = [ctx.event_pairs(len(weights)) for _ in range(steps)]
+        for s in range(steps):
+            step(evs[s])
+        torch.cuda.synchronize()
+        res["per_launch_ms"] = [sum(evs[s][j][0].elapsed_time(evs[s][j][1]) for s in range(steps)) / steps
+                                for j in range(len(weights))]
+    return res
+
+
+def layout_comparison(ctx, weights_tm, weights_rm):
+    """The M = 8 layer over tile-major weights (block fetch), row-major weights
+    read natively, and row-major weights read in whole 4 KB blocks.  Each case
+    reports the bytes the kernels fetched from weights (their own tally) over
+    the layer's weight bytes."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    cases = [("tile_major_block_4KB", weights_tm, tl.layout(G=G, block_rows=BR), tl.TL_FETCH_BLOCK),
+             ("row_major_native", weights_rm, tl.layout(kind=tl.TL_LAYOUT_NK_ROW), tl.TL_FETCH_NATIVE),
+             ("row_major_block_4KB", weights_rm, tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=G), tl.TL_FETCH_BLOCK)]
+    acts = [ctx.to_dev(synth.normal_bf16((DECODE_M, K), seed=synth.llama_decode_act_seed(i, DECODE_M)))
+            for i, (_, N, K, _) in enumerate(weights_tm)]
+    outs = [torch.empty((DECODE_M, N), dtype=torch.float32, device=ctx.dev) for (_, N, _, _) in weights_tm]
+    wbytes = sum(2 * N * K for (_, N, K, _) in weights_tm)
+    res = {}
+    for name, ws, d, mode in cases:
+        def step(extra=0):
+            for (_, N, K, W), A, C in zip(ws, acts, outs):
+                tl.tl_gemm(A, W, C, DECODE_M, N, K, d, mode | extra)
+        step()
+        torch.cuda.synchronize()
+        tl.tl_fetch_counter_read()                   # clears this stream's tally
+        step(tl.TL_FETCH_COUNT)
+        torch.cuda.synchronize()
+        fetched = tl.tl_fetch_counter_read()
+        reps = 3 if mode == tl.TL_FETCH_BLOCK and name.startswith("row") else 10
+        wall = wall_time(ctx, step, reps)
+        res[name] = {"ms_per_layer": round(wall * 1e3 / reps, 3),
+                     "weight_GB/s": round(wbytes * reps / wall / 1e9, 1),
+                     "fetched_weight_bytes": fetched,
+                     "measured_amp": round(fetched / wbytes, 4) if fetched else None}
+        log(f"layout {name}: {res[name]}")
+    return res
+
+
+def prefill_layer(ctx, weights):
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    Mp = synth.LLAMA_PREFILL_M
+    acts = [ctx.to_dev(synth.normal_bf16((Mp, K), seed=synth.llama_prefill_act_seed(i)))
+            for i, (_, N, K, _) in enumerate(weights)]
+    outs = [torch.empty((Mp, N), dtype=torch.bfloat16, device=ctx.dev) for (_, N, _, _) in weights]
+    flops = [2.0 * Mp * N * K for (_, N, K, _) in weights]
+    res = {}
+    for tm, tn in ((256, 256), (256, 128), (128, 128)):
+        pd = tl.layout(G=G, block_rows=BR, tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16)
+        for _ in range(2):
+            for (_, N, K, W), A, C in zip(weights, acts, outs):
+                tl.tl_gemm(A, W, C, Mp, N, K, pd, tl.TL_FETCH_BLOCK)
+        torch.cuda.synchronize()
+        reps = 3
+        ev = ctx.event_pairs(len(weights))
+        tot = [0.0] * len(weights)
+        for _ in range(reps):
+            for j, ((_, N, K, W), A, C) in enumerate(zip(weights, acts, outs)):
+                ev[j][0].record(ctx.stream)
+                tl.tl_gemm(A, W, C, Mp, N, K, pd, tl.TL_FETCH_BLOCK)
+                ev[j][1].record(ctx.stream)
+            torch.cuda.synchronize()
+            for j in range(len(weights)):
+                tot[j] += ev[j][0].elapsed_time(ev[j][1])
+        ms = sum(tot) / reps
+        tf = sum(flops) / (ms * 1e-3) / 1e12
+        res[f"tile_{tm}x{tn}x64"] = {
+            "TFLOP/s": round(tf, 1), "frac_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+            "layer_ms": round(ms, 3),
+            "per_shape_TFLOP/s": {name: round(f / (t / reps * 1e-3) / 1e12, 1)
+                                  for (name, _, _, _), f, t in zip(weights, flops, tot)}}
+        log(f"prefill tile {tm}x{tn}: {tf:.1f} TFLOP/s")
+    return res
+
+
+def moe_layer(ctx, steps, warmup):
+    """Qwen-3-30B-A3B-shaped layer at 64 tokens: attention q, k, v, o at M = 64
+    and, for every expert the seeded top-8 routing touches, its gate+up and
+    down GEMMs at that expert's token count; tile-major weights, one tl_gemm
+    per GEMM.  Timed eagerly and as one HIP graph per layer."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    d = tl.layout(G=G, block_rows=BR)
+    Mt, H = synth.QWEN_TOKENS, synth.QWEN_HIDDEN
+    tok = synth.tokens_per_expert(synth.moe_routing())
+    hidden = ctx.to_dev(synth.normal_bf16((Mt, H), seed=synth.QWEN_SEED_HIDDEN))
+    attn_out = ctx.to_dev(synth.normal_bf16((Mt, 4096), seed=synth.QWEN_SEED_ATTN_O_IN))
+
+    def tile_major(N, K, seed):
+        W = ctx.to_dev(synth.normal_bf16((N, K), seed=seed, sigma=synth.W_SIGMA))
+        Wt = torch.empty_like(W)
+        tl.tl_repack(W, Wt, N, K, 2, G, BR)
+        return Wt
+
+    calls = []          # (A, W tile-major, C, M, N, K)
+    for i, (name, N, K) in enumerate(synth.QWEN_ATTN):
+        A = hidden if K == H else attn_out
+        calls.append((A, tile_major(N, K, synth.qwen_attn_seed(i)),
+                      torch.empty((Mt, N), dtype=torch.float32, device=ctx.dev), Mt, N, K))
+    (Ngu, Kgu), (Nd, Kd) = synth.QWEN_GATE_UP, synth.QWEN_DOWN
+    total = int(sum(len(t) for t in tok))
+    down_in = ctx.to_dev(synth.normal_bf16((total, Kd), seed=synth.QWEN_SEED_DOWN_IN))
+    row, touched = 0, 0
+    for e in range(synth.QWEN_EXPERTS):
+        Me = len(tok[e])
+        if Me == 0:
+            continue
+        touched += 1
+        A_gu = hidden[torch.from_numpy(tok[e]).to(ctx.dev)].contiguous()
+        calls.append((A_gu, tile_major(Ngu, Kgu, synth.qwen_gate_up_seed(e)),
+                      torch.empty((Me, Ngu), dtype=torch.float32, device=ctx.dev), Me, Ngu, Kgu))
+        calls.append((down_in[row:row + Me], tile_major(Nd, Kd, synth.qwen_down_seed(e)),
+                      torch.empty((Me, Nd), dtype=torch.float32, device=ctx.dev), Me, Nd, Kd))
+        row += Me
+    torch.cuda.synchronize()
+    step_bytes = sum(launch_bytes(M, N, K) for (_, _, _, M, N, K) in calls)
+    wbytes = sum(2 * N * K for (_, _, _, _, N, K) in calls)
+
+    def step():
+        for (A, W, C, M, N, K) in calls:
+            tl.tl_gemm(A, W, C, M, N, K, d, tl.TL_FETCH_BLOCK)
+
+    for _ in range(warmup):
+        step()
+    eager = wall_time(ctx, step, steps)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=ctx.stream):
+        step()
+    for _ in range(warmup):
+        graph.replay()
+    replay = wall_time(ctx, graph.replay, steps)
+    res = {"tokens": Mt, "experts_touched": touched, "gemm_calls": len(calls), "weight_bytes": wbytes,
+           "eager_GB/s": round(step_bytes * steps / eager / 1e9, 1),
+           "graph_GB/s": round(step_bytes * steps / replay / 1e9, 1),
+           "eager_ms_per_layer": round(eager * 1e3 / steps, 3),
+           "graph_ms_per_layer": round(replay * 1e3 / steps, 3)}
+    log(f"moe layer: {res}")
+    return res
+
+
+def granularity_sweep(ctx):
+    """Down projection [8192, 28672] for each memory tile (G, block_rows): the
+    exact read amplification of 32 x tn x tk compute tiles over the tile-major
+    and the row-major layout, the repack rate, and the GEMM at M = 32 (decode
+    kernel) and M = 2048 (prefill kernel, bf16 out), whose own tiles cover
+    whole memory tiles."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    N, K = 8192, 28672
+    W = ctx.to_dev(synth.normal_bf16((N, K), seed=synth.llama_weight_seed(3), sigma=synth.W_SIGMA))
+    Wt = torch.empty_like(W)
+    A32 = ctx.to_dev(synth.normal_bf16((32, K), seed=synth.llama_decode_act_seed(3, 32)))
+    A2k = ctx.to_dev(synth.normal_bf16((2048, K), seed=synth.llama_prefill_act_seed(3)))
+    C32 = torch.empty((32, N), dtype=torch.float32, device=ctx.dev)
+    C2k = torch.empty((2048, N), dtype=torch.bfloat16, device=ctx.dev)
+    rm = tl.layout(kind=tl.TL_LAYOUT_NK_ROW)
+    tiles = [(tn, tk) for tn in (64, 128, 256) for tk in (64, 128, 256)]
+    rows = []
+    for Gs in (512, 1024, 4096, 16384):
+        for br in (8, 16, 32, 64):
+            d = tl.layout(G=Gs, block_rows=br)
+            dp = tl.layout(G=Gs, block_rows=br, out_dtype=tl.TL_OUT_BF16)
+            row = {"G": Gs, "block_rows": br, "block_cols": Gs // (2 * br),
+                   "read_amp_tile_major": {f"{tn}x{tk}": tl.tl_read_amp(32, N, K, 32, tn, tk, d, Gs)["amp"]
+                                           for tn, tk in tiles},
+                   "read_amp_row_major": {f"{tn}x{tk}": tl.tl_read_amp(32, N, K, 32, tn, tk, rm, Gs)["amp"]
+                                          for tn, tk in tiles}}
+            tl.tl_repack(W, Wt, N, K, 2, Gs, br)
+            ev = ctx.event_pairs(1)[0]
+            ev[0].record(ctx.stream)
+            tl.tl_repack(W, Wt, N, K, 2, Gs, br)
+            ev[1].record(ctx.stream)
+            torch.cuda.synchronize()
+            row["repack_GB/s"] = round(4 * N * K / (ev[0].elapsed_time(ev[1]) * 1e-3) / 1e9, 1)
+            for key, A, C, M, desc, reps in (("decode_M32_GB/s", A32, C32, 32, d, 5),
+                                             ("prefill_M2048_TFLOP/s", A2k, C2k, 2048, dp, 3)):
+                try:
+                    tl.tl_gemm(A, Wt, C, M, N, K, desc, tl.TL_FETCH_BLOCK)
+                except tl.TLError as e:
+                    row[key] = str(e)
+                    continue
+                ev = ctx.event_pairs(1)[0]
+                ev[0].record(ctx.stream)
+                for _ in range(reps):
+                    tl.tl_gemm(A, Wt, C, M, N, K, desc, tl.TL_FETCH_BLOCK)
+                ev[1].record(ctx.stream)
+                torch.cuda.synchronize()
+                ms = ev[0].elapsed_time(ev[1]) / reps
+                row[key] = round((launch_bytes(M, N, K) / 1e9 if M == 32 else 2.0 * M * N * K / 1e12)
+                                 / (ms * 1e-3), 1)
+            rows.append(row)
+            log(f"sweep G={Gs} br={br}: decode {row['decode_M32_GB/s']}, prefill {row['prefill_M2048_TFLOP/s']}, "
+                f"repack {row['repack_GB/s']}")
+    return {"metric": "memory-tile granularity sweep", "data": "synthetic",
+            "config": {"workload": "down projection [8192, 28672], bf16 weights; decode M=32, prefill M=2048"},
+            "rows": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="skip M=1/32, the layout comparison and the MoE layer")
+    ap.add_argument("--sweep", action="store_true", help="run only the memory-tile granularity sweep")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the path is single-GPU; see the sharding notes in the design document)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
-    import torch
-
-    import paper_2607_04031_amd as tl
-    from paper_2607_04031_amd import synth
-
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    tl.load_library()
-    dev = torch.device("cuda:0")
-    # all work on one side stream (default priority): graphs cannot be
-    # captured on the null stream
-    stream = torch.cuda.Stream(device=dev)
-    torch.cuda.set_stream(stream)
+    ctx = Ctx()
+    if args.sweep:
+        print(json.dumps(granularity_sweep(ctx)), flush=True)
+        return
+    torch, tl, synth = ctx.torch, ctx.tl, ctx.synth
 
     # ---------------- weights: seeded, row-major, repacked on the GPU --------
     desc = tl.layout(G=G, block_rows=BR)
-    weights, weights_rm_host = [], []
+    weights, weights_rm, weights_host = [], [], []
     repack_ms, repack_bytes = 0.0, 0
     for i, (name, N, K) in enumerate(synth.LLAMA70B):
         log(f"generating {name} [{N},{K}]")
         bits = synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA)
-        W = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        W = ctx.to_dev(bits)
         Wt = torch.empty_like(W)
         tl.tl_repack(W, Wt, N, K, 2, G, BR)          # warm
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+        ev = ctx.event_pairs(1)[0]
+        ev[0].record(ctx.stream)
         tl.tl_repack(W, Wt, N, K, 2, G, BR)
-        e1.record(stream)
+        ev[1].record(ctx.stream)
         torch.cuda.synchronize()
-        repack_ms += e0.elapsed_time(e1)
+        repack_ms += ev[0].elapsed_time(ev[1])
         repack_bytes += 2 * N * K * 2
-        del W
         weights.append((name, N, K, Wt))
+        if not args.no_extras:
+            weights_rm.append((name, N, K, W))
+        del W
         if not args.no_cpu_baseline:
-            weights_rm_host.append(bits)
-        else:
-            del bits
-    acts = []
-    for i, (name, N, K, _) in enumerate(weights):
-        a = synth.normal_bf16((DECODE_M, K), seed=synth.llama_decode_act_seed(i, DECODE_M))
-        acts.append((a, torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)))
-    outs = [torch.empty((DECODE_M, N), dtype=torch.float32, device=dev) for (_, N, _, _) in weights]
-    step_bytes = sum(2 * N * K + 2 * DECODE_M * K + 4 * DECODE_M * N for (_, N, K, _) in weights)
+            weights_host.append(bits)
+        del bits
 
-    def step(events=None):
-        for j, ((name, N, K, Wt), (_, A), C) in enumerate(zip(weights, acts, outs)):
-            if events is not None:
-                events[j][0].record(stream)
-            tl.tl_gemm(A, Wt, C, DECODE_M, N, K, desc, tl.TL_FETCH_BLOCK)
-            if events is not None:
-                events[j][1].record(stream)
-
-    log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # ---------------- timed region: K eager steps ----------------
-    log(f"timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    wall_s = t1 - t0
-    ms_per_step = wall_s * 1e3 / args.steps
-    value_gbs = step_bytes * args.steps / wall_s / 1e9
+    # ---------------- timed region: K eager steps of the M = 8 layer ---------
+    log(f"warmup {args.warmup} steps, timing {args.steps} steps")
+    main_run = decode_layer(ctx, weights, DECODE_M, args.steps, args.warmup, desc, event_pass=True)
+    value_gbs = main_run["GB/s"]
 
     # the same step captured once as a HIP graph and replayed K times (the
-    # library's workspace already exists, so capture records kernels only);
-    # reported beside the eager number
+    # library's workspace already exists, so capture records kernels only)
     graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph, stream=stream):
-        step()
-    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=ctx.stream):
+        main_run["step"]()
     for _ in range(args.warmup):
         graph.replay()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        graph.replay()
-    torch.cuda.synchronize()
-    graph_gbs = step_bytes * args.steps / (time.perf_counter() - t0) / 1e9
+    graph_gbs = main_run["step_bytes"] * args.steps / wall_time(ctx, graph.replay, args.steps) / 1e9
 
-    # per-launch durations from HIP events recorded on the launch stream around
-    # each tl_gemm call (a separate pass over the same launches)
-    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-           for _ in weights] for _ in range(args.steps)]
-    for s in range(args.steps):
-        step(ev[s])
-    torch.cuda.synchronize()
-    per_shape_ms = [0.0] * len(weights)
-    for s in range(args.steps):
-        for j in range(len(weights)):
-            per_shape_ms[j] += ev[s][j][0].elapsed_time(ev[s][j][1])
-    per_shape_ms = [x / args.steps for x in per_shape_ms]
-    launch_bytes = [2 * N * K + 2 * DECODE_M * K + 4 * DECODE_M * N for (_, N, K, _) in weights]
-    achieved = sum(launch_bytes) / (sum(per_shape_ms) * 1e-3) / 1e9
+    per_ms, lb = main_run["per_launch_ms"], main_run["launch_bytes"]
+    achieved = sum(lb) / (sum(per_ms) * 1e-3) / 1e9
     per_shape = {name: {"us": round(ms * 1e3, 2), "GB/s": round(b / (ms * 1e-3) / 1e9, 1),
                         "frac_hbm_peak": round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                         "split_k": tl.tl_gemm_plan(DECODE_M, N, K, desc)["split_k"]}
-                 for (name, N, K, _), ms, b in zip(weights, per_shape_ms, launch_bytes)}
+                 for (name, N, K, _), ms, b in zip(weights, per_ms, lb)}
     log(f"decode layer M={DECODE_M}: eager {value_gbs:.1f} GB/s, graph replay {graph_gbs:.1f} GB/s, "
         f"kernels {achieved:.1f} GB/s")
+
+    # ---------------- other batch sizes, layouts, the MoE layer -------------
+    extras = None
+    if not args.no_extras:
+        extras = {}
+        for M in (1, 32):
+            r = decode_layer(ctx, weights, M, args.steps, 2, desc)
+            extras[f"decode_layer_M{M}_GB/s"] = round(r["GB/s"], 1)
+            log(f"decode layer M={M}: {r['GB/s']:.1f} GB/s")
+        extras["layouts_M8"] = layout_comparison(ctx, weights, weights_rm)
+        del weights_rm
+        torch.cuda.empty_cache()
+        extras["moe_qwen3_30b_a3b_64_tokens"] = moe_layer(ctx, args.steps, args.warmup)
+        torch.cuda.empty_cache()
 
     # ---------------- read amplification ----------------
     plan = tl.tl_gemm_plan(DECODE_M, 8192, 8192, desc, tl.TL_FETCH_BLOCK)
@@ -185,58 +417,20 @@ def main():
     rm = tl.layout(kind=tl.TL_LAYOUT_NK_ROW)
     amp_rm = tl.tl_read_amp(DECODE_M, 8192, 8192, plan["tile_m"], plan["tile_n"], plan["tile_k"], rm, G)
     kn = tl.layout(kind=tl.TL_LAYOUT_KN_ROW)
-    req_kn = tl.tl_read_amp(1, 2048, 2048, 1, 256, 128, kn, G)["max_blocks_per_tile"]
-    req_tm = tl.tl_read_amp(1, 2048, 2048, 1, 256, 128, desc, G)["max_blocks_per_tile"]
     read_amp = {
         "decode_tile": [plan["tile_m"], plan["tile_n"], plan["tile_k"]],
         "tile_major": amp_tile["amp"],
         "row_major_same_tile": amp_rm["amp"],
-        "requests_per_128x256_tile_row_major": req_kn,
-        "requests_per_128x256_tile_tile_major": req_tm,
+        "requests_per_128x256_tile_row_major": tl.tl_read_amp(1, 2048, 2048, 1, 256, 128, kn, G)["max_blocks_per_tile"],
+        "requests_per_128x256_tile_tile_major": tl.tl_read_amp(1, 2048, 2048, 1, 256, 128, desc, G)["max_blocks_per_tile"],
         "waste_frac_block_fetch": 1.0 - 1.0 / amp_tile["amp"],
     }
 
     # ---------------- prefill (M = 2048) ----------------
-    prefill = None
-    if not args.no_prefill:
-        prefill = {}
-        Mp = synth.LLAMA_PREFILL_M
-        pacts = []
-        for i, (name, N, K, _) in enumerate(weights):
-            a = synth.normal_bf16((Mp, K), seed=synth.llama_prefill_act_seed(i))
-            pacts.append(torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev))
-        pouts = [torch.empty((Mp, N), dtype=torch.bfloat16, device=dev) for (_, N, _, _) in weights]
-        flops = sum(2.0 * Mp * N * K for (_, N, K, _) in weights)
-        for tm, tn in ((256, 256), (256, 128), (128, 128)):
-            pd = tl.layout(G=G, block_rows=BR, tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16)
-            for _ in range(2):
-                for (name, N, K, Wt), A, C in zip(weights, pacts, pouts):
-                    tl.tl_gemm(A, Wt, C, Mp, N, K, pd, tl.TL_FETCH_BLOCK)
-            torch.cuda.synchronize()
-            reps = 3
-            pev = [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in weights]
-            tot = [0.0] * len(weights)
-            for _ in range(reps):
-                for j, ((name, N, K, Wt), A, C) in enumerate(zip(weights, pacts, pouts)):
-                    pev[j][0].record(stream)
-                    tl.tl_gemm(A, Wt, C, Mp, N, K, pd, tl.TL_FETCH_BLOCK)
-                    pev[j][1].record(stream)
-                torch.cuda.synchronize()
-                for j in range(len(weights)):
-                    tot[j] += pev[j][0].elapsed_time(pev[j][1])
-            ms = sum(tot) / reps
-            tf = flops / (ms * 1e-3) / 1e12
-            prefill[f"tile_{tm}x{tn}x64"] = {
-                "TFLOP/s": round(tf, 1), "frac_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
-                "layer_ms": round(ms, 3),
-                "per_shape_TFLOP/s": {name: round(2.0 * Mp * N * K / (t / reps * 1e-3) / 1e12, 1)
-                                      for (name, N, K, _), t in zip(weights, tot)}}
-            log(f"prefill tile {tm}x{tn}: {tf:.1f} TFLOP/s")
-        del pacts, pouts
+    prefill = None if args.no_prefill else prefill_layer(ctx, weights)
 
     # ---------------- HBM copy calibration (for rocprofv3 counters) ---------
-    calib_bytes = 1 << 30
-    src = torch.empty(calib_bytes, dtype=torch.uint8, device=dev)
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=ctx.dev)
     dst = torch.empty_like(src)
     for _ in range(3):
         dst.copy_(src)
@@ -249,21 +443,21 @@ def main():
         import oracle
         threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
         log(f"cpu oracle: full decode layer at M={DECODE_M}, {threads} threads")
+        acts = [synth.normal_bf16((DECODE_M, K), seed=synth.llama_decode_act_seed(i, DECODE_M))
+                for i, (_, N, K) in enumerate(synth.LLAMA70B)]
         t0 = time.perf_counter()
-        for bits, (a_bits, _) in zip(weights_rm_host, acts):
+        for bits, a_bits in zip(weights_host, acts):
             oracle.gemm_f64(a_bits, bits)
         dt = time.perf_counter() - t0
-        cpu = {"value": round(step_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
-               "sample": f"one full decode layer (4 GEMMs, M={DECODE_M}, row-major weights), fp64, "
-                         f"{dt:.2f} s"}
+        cpu = {"value": round(main_run["step_bytes"] / dt / 1e9, 3), "unit": "GB/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"one full decode layer (4 GEMMs, M={DECODE_M}, row-major weights), fp64, {dt:.2f} s"}
 
-    kernel_hash = source_hash("tl_decode.hip")
-    traffic = profiled_traffic(kernel_hash)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": profiled_traffic(source_hash("tl_decode.hip")),
                 "kernel": "decode_kernel (tile-major, M=8; a split_k > 1 call includes its reduce kernel)",
                 "per_shape": per_shape}
-
     out = {
         "metric": METRIC,
         "value": round(value_gbs, 1),
@@ -271,7 +465,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(main_run["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -279,7 +473,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": "llama-3.1-70b-shaped decode layer (qkv, o, gate_up, down), M=8, "
                                "bf16 weights tile-major G=4096 B 32x64 memory tiles, block fetch, fp32 out",
-                   "M": DECODE_M, "G": G, "block_rows": BR, "weight_bytes": sum(2 * N * K for (_, N, K, _) in weights)},
+                   "M": DECODE_M, "G": G, "block_rows": BR,
+                   "weight_bytes": sum(2 * N * K for (_, N, K, _) in weights)},
         "frac_hbm_peak": round(value_gbs / HBM_PEAK_GBS, 4),
         "graph_replay_GB/s": round(graph_gbs, 1),
         "roofline": roofline,
@@ -287,6 +482,7 @@ def main():
         "prefill": prefill,
         "read_amp": read_amp,
         "repack_GB/s": round(repack_bytes / (repack_ms * 1e-3) / 1e9, 1),
+        "extras": extras,
     }
     print(json.dumps(out), flush=True)
 

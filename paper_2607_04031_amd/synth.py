@@ -127,3 +127,13 @@ def tokens_per_expert(routing: np.ndarray, E: int = QWEN_EXPERTS) -> list[np.nda
     for e in range(E):
         out.append(np.nonzero((routing == e).any(axis=1))[0].astype(np.int64))
     return out
+
+
+def qwen_attn_seed(i: int) -> int:
+    """Seed of attention projection QWEN_ATTN[i] (q, k, v, o)."""
+    return 3000 + i
+
+
+QWEN_SEED_HIDDEN = 3      # [64, 2048] hidden states: input of q, k, v and of the experts' gate+up
+QWEN_SEED_ATTN_O_IN = 5   # [64, 4096] attention output: input of o
+QWEN_SEED_DOWN_IN = 4     # [sum of tokens per expert, 768] input of the experts' down GEMMs

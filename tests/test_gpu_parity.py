@@ -415,3 +415,47 @@ def test_graph_replay_matches_eager():
             side.synchronize()
             for (_, _, C, _, _, _, _), want in zip(tensors, eager):
                 assert torch.equal(C, want), f"replay {rep}"
+
+
+# ---------------------------------------------------------------------------
+# Qwen-3-30B-A3B-shaped MoE layer: per-expert GEMMs at the token counts the
+# seeded top-8 routing gives, and the attention projections at M = 64
+# ---------------------------------------------------------------------------
+
+def _moe_experts_sample():
+    tok = synth.tokens_per_expert(synth.moe_routing())
+    counts = np.array([len(t) for t in tok])
+    touched = np.nonzero(counts)[0]
+    # largest, smallest and a spread of token counts
+    order = touched[np.argsort(counts[touched], kind="stable")]
+    pick = sorted(set(order[[0, 1, len(order) // 3, len(order) // 2, -2, -1]].tolist()))
+    return tok, pick
+
+
+def test_moe_expert_gemms():
+    """Gate+up [1536, 2048] and down [2048, 768] of sampled experts, each at
+    its own token count (rows gathered from the seeded hidden states)."""
+    tok, pick = _moe_experts_sample()
+    hidden = synth.normal_bf16((synth.QWEN_TOKENS, synth.QWEN_HIDDEN), seed=synth.QWEN_SEED_HIDDEN)
+    total = int(sum(len(t) for t in tok))
+    down_in = synth.normal_bf16((total, synth.QWEN_DOWN[1]), seed=synth.QWEN_SEED_DOWN_IN)
+    starts = np.concatenate([[0], np.cumsum([len(t) for t in tok])])
+    for e in pick:
+        Me = len(tok[e])
+        banner(f"moe expert {e}: M={Me}")
+        A_gu = np.ascontiguousarray(hidden[tok[e]])
+        W_gu = synth.normal_bf16(synth.QWEN_GATE_UP, seed=synth.qwen_gate_up_seed(e), sigma=synth.W_SIGMA)
+        parity(host_f32(run_gemm(A_gu, W_gu, tl.layout())), oracle.gemm_f64(A_gu, W_gu), f"gate_up e={e}")
+        A_d = np.ascontiguousarray(down_in[starts[e]:starts[e] + Me])
+        W_d = synth.normal_bf16(synth.QWEN_DOWN, seed=synth.qwen_down_seed(e), sigma=synth.W_SIGMA)
+        parity(host_f32(run_gemm(A_d, W_d, tl.layout())), oracle.gemm_f64(A_d, W_d), f"down e={e}")
+
+
+@pytest.mark.parametrize("i", range(len(synth.QWEN_ATTN)))
+def test_moe_attention_projections(i):
+    name, N, K = synth.QWEN_ATTN[i]
+    banner(f"moe attention {name} M={synth.QWEN_TOKENS} N={N} K={K}")
+    seed = synth.QWEN_SEED_HIDDEN if K == synth.QWEN_HIDDEN else synth.QWEN_SEED_ATTN_O_IN
+    A = synth.normal_bf16((synth.QWEN_TOKENS, K), seed=seed)
+    W = synth.normal_bf16((N, K), seed=synth.qwen_attn_seed(i), sigma=synth.W_SIGMA)
+    parity(host_f32(run_gemm(A, W, tl.layout())), oracle.gemm_f64(A, W), f"attn {name}")
