@@ -210,63 +210,102 @@ def prefill_layer(ctx, weights):
 def moe_layer(ctx, steps, warmup):
     """Qwen-3-30B-A3B-shaped layer at 64 tokens: attention q, k, v, o at M = 64
     and, for every expert the seeded top-8 routing touches, its gate+up and
-    down GEMMs at that expert's token count; tile-major weights, one tl_gemm
-    per GEMM.  Timed eagerly and as one HIP graph per layer."""
-    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    down GEMMs at that expert's token count; tile-major weights.  Timed three
+    ways: one tl_gemm per GEMM (eager, and replayed as one HIP graph), and
+    the experts as two tl_gemm_grouped launches (gate+up over all experts,
+    then down) beside the four attention calls."""
+    tl, torch, synth, np = ctx.tl, ctx.torch, ctx.synth, ctx.np
     d = tl.layout(G=G, block_rows=BR)
-    Mt, H = synth.QWEN_TOKENS, synth.QWEN_HIDDEN
-    tok = synth.tokens_per_expert(synth.moe_routing())
+    Mt, H, E = synth.QWEN_TOKENS, synth.QWEN_HIDDEN, synth.QWEN_EXPERTS
+    routing = synth.moe_routing()
+    tok = synth.tokens_per_expert(routing)
+    offsets, ids = synth.moe_tables(routing)
+    total = int(offsets[-1])
+    max_rows = int(np.diff(offsets).max())
     hidden = ctx.to_dev(synth.normal_bf16((Mt, H), seed=synth.QWEN_SEED_HIDDEN))
     attn_out = ctx.to_dev(synth.normal_bf16((Mt, 4096), seed=synth.QWEN_SEED_ATTN_O_IN))
+    (Ngu, Kgu), (Nd, Kd) = synth.QWEN_GATE_UP, synth.QWEN_DOWN
+    down_in = ctx.to_dev(synth.normal_bf16((total, Kd), seed=synth.QWEN_SEED_DOWN_IN))
 
-    def tile_major(N, K, seed):
+    def tile_major(N, K, seed, out=None):
         W = ctx.to_dev(synth.normal_bf16((N, K), seed=seed, sigma=synth.W_SIGMA))
-        Wt = torch.empty_like(W)
+        Wt = torch.empty_like(W) if out is None else out
         tl.tl_repack(W, Wt, N, K, 2, G, BR)
         return Wt
 
-    calls = []          # (A, W tile-major, C, M, N, K)
+    attn = []           # (A, W tile-major, C, M, N, K)
     for i, (name, N, K) in enumerate(synth.QWEN_ATTN):
-        A = hidden if K == H else attn_out
-        calls.append((A, tile_major(N, K, synth.qwen_attn_seed(i)),
-                      torch.empty((Mt, N), dtype=torch.float32, device=ctx.dev), Mt, N, K))
-    (Ngu, Kgu), (Nd, Kd) = synth.QWEN_GATE_UP, synth.QWEN_DOWN
-    total = int(sum(len(t) for t in tok))
-    down_in = ctx.to_dev(synth.normal_bf16((total, Kd), seed=synth.QWEN_SEED_DOWN_IN))
-    row, touched = 0, 0
-    for e in range(synth.QWEN_EXPERTS):
+        attn.append((hidden if K == H else attn_out, tile_major(N, K, synth.qwen_attn_seed(i)),
+                     torch.empty((Mt, N), dtype=torch.float32, device=ctx.dev), Mt, N, K))
+    # expert weights stacked [E, N, K], each expert tile-major; untouched experts are never read
+    gu_stack = torch.empty((E, Ngu, Kgu), dtype=torch.bfloat16, device=ctx.dev)
+    d_stack = torch.empty((E, Nd, Kd), dtype=torch.bfloat16, device=ctx.dev)
+    per_expert, row, touched = [], 0, 0
+    for e in range(E):
+        tile_major(Ngu, Kgu, synth.qwen_gate_up_seed(e), gu_stack[e])
+        tile_major(Nd, Kd, synth.qwen_down_seed(e), d_stack[e])
         Me = len(tok[e])
         if Me == 0:
             continue
         touched += 1
         A_gu = hidden[torch.from_numpy(tok[e]).to(ctx.dev)].contiguous()
-        calls.append((A_gu, tile_major(Ngu, Kgu, synth.qwen_gate_up_seed(e)),
-                      torch.empty((Me, Ngu), dtype=torch.float32, device=ctx.dev), Me, Ngu, Kgu))
-        calls.append((down_in[row:row + Me], tile_major(Nd, Kd, synth.qwen_down_seed(e)),
-                      torch.empty((Me, Nd), dtype=torch.float32, device=ctx.dev), Me, Nd, Kd))
+        per_expert.append((A_gu, gu_stack[e], torch.empty((Me, Ngu), dtype=torch.float32, device=ctx.dev),
+                           Me, Ngu, Kgu))
+        per_expert.append((down_in[row:row + Me], d_stack[e],
+                           torch.empty((Me, Nd), dtype=torch.float32, device=ctx.dev), Me, Nd, Kd))
         row += Me
+    d_ids, d_off = (torch.from_numpy(x).to(ctx.dev) for x in (ids, offsets))
+    C_gu = torch.empty((total, Ngu), dtype=torch.float32, device=ctx.dev)
+    C_d = torch.empty((total, Nd), dtype=torch.float32, device=ctx.dev)
     torch.cuda.synchronize()
+    calls = attn + per_expert
     step_bytes = sum(launch_bytes(M, N, K) for (_, _, _, M, N, K) in calls)
     wbytes = sum(2 * N * K for (_, _, _, _, N, K) in calls)
 
-    def step():
+    def step_per_expert():
         for (A, W, C, M, N, K) in calls:
             tl.tl_gemm(A, W, C, M, N, K, d, tl.TL_FETCH_BLOCK)
 
-    for _ in range(warmup):
-        step()
-    eager = wall_time(ctx, step, steps)
+    def step_grouped():
+        for (A, W, C, M, N, K) in attn:
+            tl.tl_gemm(A, W, C, M, N, K, d, tl.TL_FETCH_BLOCK)
+        tl.tl_gemm_grouped(hidden, Mt, d_ids, d_off, E, total, max_rows, gu_stack, Ngu * Kgu * 2, C_gu,
+                           Ngu, Kgu, d, tl.TL_FETCH_BLOCK)
+        tl.tl_gemm_grouped(down_in, total, None, d_off, E, total, max_rows, d_stack, Nd * Kd * 2, C_d,
+                           Nd, Kd, d, tl.TL_FETCH_BLOCK)
+
+    res = {"tokens": Mt, "experts_touched": touched, "expert_rows": total, "weight_bytes": wbytes,
+           "step_bytes": step_bytes}
+    for name, fn in (("per_expert_eager", step_per_expert), ("grouped_eager", step_grouped)):
+        for _ in range(warmup):
+            fn()
+        wall = wall_time(ctx, fn, steps)
+        res[name] = {"GB/s": round(step_bytes * steps / wall / 1e9, 1), "ms_per_layer": round(wall * 1e3 / steps, 4)}
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=ctx.stream):
-        step()
+        step_per_expert()
     for _ in range(warmup):
         graph.replay()
-    replay = wall_time(ctx, graph.replay, steps)
-    res = {"tokens": Mt, "experts_touched": touched, "gemm_calls": len(calls), "weight_bytes": wbytes,
-           "eager_GB/s": round(step_bytes * steps / eager / 1e9, 1),
-           "graph_GB/s": round(step_bytes * steps / replay / 1e9, 1),
-           "eager_ms_per_layer": round(eager * 1e3 / steps, 3),
-           "graph_ms_per_layer": round(replay * 1e3 / steps, 3)}
+    wall = wall_time(ctx, graph.replay, steps)
+    res["per_expert_graph"] = {"GB/s": round(step_bytes * steps / wall / 1e9, 1),
+                               "ms_per_layer": round(wall * 1e3 / steps, 4)}
+    # the grouped launches alone, event-timed (the experts' share of the layer)
+    ev = ctx.event_pairs(2)
+    ev[0][0].record(ctx.stream)
+    for _ in range(steps):
+        tl.tl_gemm_grouped(hidden, Mt, d_ids, d_off, E, total, max_rows, gu_stack, Ngu * Kgu * 2, C_gu,
+                           Ngu, Kgu, d, tl.TL_FETCH_BLOCK)
+    ev[0][1].record(ctx.stream)
+    ev[1][0].record(ctx.stream)
+    for _ in range(steps):
+        tl.tl_gemm_grouped(down_in, total, None, d_off, E, total, max_rows, d_stack, Nd * Kd * 2, C_d,
+                           Nd, Kd, d, tl.TL_FETCH_BLOCK)
+    ev[1][1].record(ctx.stream)
+    torch.cuda.synchronize()
+    for j, (name, N, K) in enumerate((("gate_up", Ngu, Kgu), ("down", Nd, Kd))):
+        us = ev[j][0].elapsed_time(ev[j][1]) * 1e3 / steps
+        byts = touched * 2 * N * K + 2 * total * K + 4 * total * N   # as the per-expert calls count it
+        res[f"grouped_{name}_launch"] = {"us": round(us, 2), "GB/s": round(byts / (us * 1e-6) / 1e9, 1)}
     log(f"moe layer: {res}")
     return res
 

@@ -149,15 +149,21 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  *      even) per layout->out_dtype.  C must not overlap A or W.
  * fetch_mode: TL_FETCH_NATIVE or TL_FETCH_BLOCK, optionally | TL_FETCH_COUNT.
  *      For TL_LAYOUT_TILE both modes load whole memory tiles (the compute tile
- *      is a whole number of memory tiles).
+ *      is a whole number of memory tiles).  For TL_LAYOUT_NK_ROW, BLOCK loads
+ *      every layout->G-byte block a K step touches, whole (decode kernel only;
+ *      G a power of two, 128 <= G <= 2^30): the amplification of Section 2.5
+ *      paid as real HBM traffic, and tallied by TL_FETCH_COUNT.
  * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound); larger M runs the
- * prefill kernel (bf16 MFMA tiles 128x128x64 or 256x128x64, MFMA-bound).
+ * prefill kernel (bf16 MFMA tiles 256x256x64, 256x128x64 or 128x128x64,
+ * MFMA-bound).
  * Errors: TL_EINVAL for M, N, K < 1, NULL or misaligned pointers, a bad
  * descriptor (see tl_repack) or N % block_rows / K % block_cols != 0 for
- * TL_LAYOUT_TILE; TL_EUNSUPPORTED for elem_bytes != 2, K % 64 != 0,
- * N % 32 != 0, block_cols < 8, a TILE/BLOCK combination of layout, fetch mode
- * and tile that no kernel implements, or TL_LAYOUT_KN_ROW.  TL_ENOMEM if the
- * split-K workspace cannot be allocated; TL_EHIP if the launch fails.
+ * TL_LAYOUT_TILE, or a bad G for NK_ROW with TL_FETCH_BLOCK;
+ * TL_EUNSUPPORTED for elem_bytes != 2, K % 64 != 0, N % 32 != 0,
+ * block_cols < 8, a combination of layout, fetch mode and tile that no kernel
+ * implements (NK_ROW with BLOCK above 64 rows), or TL_LAYOUT_KN_ROW.
+ * TL_ENOMEM if the split-K workspace cannot be allocated; TL_EHIP if the
+ * launch fails.
  */
 int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
             const tl_layout_desc* layout, int32_t fetch_mode, void* stream);
@@ -166,6 +172,47 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
  * same arguments (no device work).  Same error rules as tl_gemm. */
 int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout,
                  int32_t fetch_mode, tl_plan* out);
+
+/*
+ * tl_gemm_grouped -- one launch over a stack of weights that each serve their
+ * own rows: the expert GEMMs of a mixture-of-experts layer, whose decode-time
+ * kernel (fused_moe) is the paper's main workload (Sections 2.3 and 6.2).
+ * For every group e in [0, num_groups) and every output row r in
+ * [group_offsets[e], group_offsets[e+1]):
+ *      C[r][n] = sum_k A[t][k] * W_e[n][k],   t = token_ids ? token_ids[r] : r
+ * with W_e at W + e * group_stride bytes, each in the layout 'layout'
+ * describes (TL_LAYOUT_TILE or TL_LAYOUT_NK_ROW, repacked one by one).
+ *
+ * A:             device bf16 [a_rows][K] row-major.
+ * token_ids:     device int32 [total_rows] or NULL (row r reads A row r; then
+ *                a_rows >= total_rows).  An id outside [0, a_rows) reads a
+ *                row of zeros.
+ * group_offsets: device int32 [num_groups + 1], nondecreasing, from 0 to
+ *                total_rows; read by the kernel, clamped to [0, total_rows].
+ *                Out-of-order offsets give unspecified rows of C, never an
+ *                access outside A, W or C.
+ * max_group_rows: host bound on the rows of one group; it picks the kernel's
+ *                M tile (16, 32 or 64 rows).  A group with more rows is
+ *                processed in several passes over its weight (correct, more
+ *                traffic).
+ * W:             device, group_stride >= N * K * 2 bytes apart (multiple of 16).
+ * C:             device [total_rows][N] row-major, fp32 or bf16 per
+ *                layout->out_dtype; rows of empty groups are not written.
+ * Weights stream once per group and pass (4-wave workgroups, one per (group,
+ * tile_n-row tile), K not split), so results match tl_gemm to rounding.
+ * fetch_mode: as tl_gemm (TL_FETCH_BLOCK on NK_ROW is not supported here).
+ * Errors: TL_EINVAL for num_groups < 1, total_rows < 0, a_rows < 1, rows
+ * beyond 2^31 - 1, a short or misaligned group_stride, NULL or misaligned
+ * pointers (offsets and ids 4-byte aligned), overlap of C with A or W, or a
+ * descriptor tl_gemm rejects with TL_EINVAL; TL_EUNSUPPORTED for split_k > 1,
+ * tile_m > 64, and what tl_gemm rejects with TL_EUNSUPPORTED.  total_rows == 0
+ * enqueues nothing.
+ */
+int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
+                    const int32_t* group_offsets, int32_t num_groups, int64_t total_rows,
+                    int64_t max_group_rows, const void* W, int64_t group_stride, void* C,
+                    int64_t N, int64_t K, const tl_layout_desc* layout, int32_t fetch_mode,
+                    void* stream);
 
 /*
  * tl_read_amp -- host only, exact integer count of the bytes a tiled GEMM

@@ -12,6 +12,9 @@ What each function follows (TileLens, arxiv 2607.04031):
   repack/unpack  Section 3.2 (the permutation Eq. 2 defines); Section 5.1
                  (weights are written in this order once, at load time)
   gemm_f64       Section 2.3 (C = A W^T over the K dimension), fp64
+  grouped_gemm_f64  the expert GEMMs of a mixture-of-experts layer (Sections
+                 2.3 and 6.2): per group, gather its rows of A and apply
+                 gemm_f64 with that group's weight
   round_bf16     round-to-nearest-even to 8 significant bits
   read_amp       Sections 1, 2.5 and 6.4 (requests per compute tile at
                  granularity G; weights only, Section 5.1)
@@ -121,6 +124,22 @@ def gemm_f64(A_bf16: np.ndarray, W_bf16: np.ndarray) -> np.ndarray:
     assert K == K2
     Y = np.empty((M, N), dtype=np.float64)
     _load().orc_gemm_f64(_ptr(A), _ptr(W), _ptr(Y), M, N, K)
+    return Y
+
+
+def grouped_gemm_f64(A_bf16: np.ndarray, token_ids, offsets, W_list) -> np.ndarray:
+    """Rows [offsets[e], offsets[e+1]) of the result are A[token_ids[r]] @ W_list[e]^T
+    (token_ids None: A[r]); fp64 [offsets[-1], N].  Empty groups contribute nothing."""
+    offsets = [int(x) for x in offsets]
+    assert len(offsets) == len(W_list) + 1 and offsets[0] == 0
+    N = W_list[0].shape[0]
+    Y = np.zeros((offsets[-1], N), dtype=np.float64)
+    for e, W in enumerate(W_list):
+        r0, r1 = offsets[e], offsets[e + 1]
+        if r1 <= r0:
+            continue
+        rows = np.arange(r0, r1) if token_ids is None else np.asarray(token_ids[r0:r1], dtype=np.int64)
+        Y[r0:r1] = gemm_f64(A_bf16[rows], W)
     return Y
 
 

@@ -35,7 +35,7 @@ TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE = 0, 1, 2
 TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
-EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_plan", "tl_read_amp",
+EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
             "tl_fetch_counter_read", "tl_release", "tl_strerror")
 
 
@@ -104,6 +104,9 @@ def load_library():
     lib.tl_gemm.argtypes = [p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, p]
     lib.tl_gemm_plan.restype = ctypes.c_int
     lib.tl_gemm_plan.argtypes = [i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, ctypes.POINTER(Plan)]
+    lib.tl_gemm_grouped.restype = ctypes.c_int
+    lib.tl_gemm_grouped.argtypes = [p, i64, p, p, i32, i64, i64, p, i64, p, i64, i64,
+                                    ctypes.POINTER(LayoutDesc), i32, p]
     lib.tl_read_amp.restype = ctypes.c_int
     lib.tl_read_amp.argtypes = [i64, i64, i64, i32, i32, i32, ctypes.POINTER(LayoutDesc), i64,
                                 ctypes.POINTER(Amp)]
@@ -181,6 +184,15 @@ def tl_gemm_plan(M, N, K, layout, fetch_mode=TL_FETCH_BLOCK) -> dict:
     _check(load_library().tl_gemm_plan(M, N, K, ctypes.byref(d), fetch_mode, ctypes.byref(out)),
            "tl_gemm_plan")
     return _struct_dict(out)
+
+
+def tl_gemm_grouped(A, a_rows, token_ids, group_offsets, num_groups, total_rows, max_group_rows, W,
+                    group_stride, C, N, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):
+    """token_ids may be None (row r of C reads row r of A)."""
+    d = _desc(layout)
+    _check(load_library().tl_gemm_grouped(_ptr(A), a_rows, _ptr(token_ids), _ptr(group_offsets), num_groups,
+                                          total_rows, max_group_rows, _ptr(W), group_stride, _ptr(C), N, K,
+                                          ctypes.byref(d), fetch_mode, _stream(stream)), "tl_gemm_grouped")
 
 
 def tl_read_amp(M, N, K, tile_m, tile_n, tile_k, layout, G) -> dict:

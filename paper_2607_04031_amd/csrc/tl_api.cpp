@@ -239,6 +239,26 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
     return TL_OK;
 }
 
+// A grouped launch runs the decode kernel over every group's weight with
+// 4-wave workgroups, one per (group, tile) and no K split; the group row
+// bound only chooses the 16-row M tiles per pass (larger groups take more
+// passes over their weights).
+int plan_grouped(int64_t max_group_rows, int64_t N, int64_t K, const tl_layout_desc* d, int32_t fetch_mode,
+                 Plan* P) {
+    if (!d || max_group_rows < 1) return TL_EINVAL;
+    if (d->split_k < 0 || d->tile_m < 0) return TL_EINVAL;
+    if (d->split_k > 1 || d->tile_m > kDecodeMaxM) return TL_EUNSUPPORTED;
+    tl_layout_desc d1 = *d;
+    d1.split_k = 1;
+    int rc = plan_gemm(std::min<int64_t>(max_group_rows, kDecodeMaxM), N, K, &d1, fetch_mode, P);
+    if (rc != TL_OK) return rc;
+    if (P->pub.kernel != 1 || P->block_row) return TL_EUNSUPPORTED;
+    P->waves = 4;
+    P->pub.waves = 4;
+    P->pub.workspace_bytes = 0;
+    return TL_OK;
+}
+
 }  // namespace
 }  // namespace tl
 
@@ -317,6 +337,58 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
         e = launch_prefill(q, s);
     }
     return e == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, const int32_t* group_offsets,
+                    int32_t num_groups, int64_t total_rows, int64_t max_group_rows, const void* W,
+                    int64_t group_stride, void* C, int64_t N, int64_t K, const tl_layout_desc* layout,
+                    int32_t fetch_mode, void* stream) {
+    Plan p;
+    int rc = plan_grouped(max_group_rows, N, K, layout, fetch_mode, &p);
+    if (rc != TL_OK) return rc;
+    if (num_groups < 1 || total_rows < 0 || a_rows < 1) return TL_EINVAL;
+    if (total_rows >= (int64_t(1) << 31) || a_rows >= (int64_t(1) << 31)) return TL_EINVAL;
+    if (!token_ids && a_rows < total_rows) return TL_EINVAL;
+    if (group_stride < N * K * 2 || group_stride % 16) return TL_EINVAL;
+    if (!A || !W || !C || !group_offsets || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(group_offsets) & 3u) || (reinterpret_cast<uintptr_t>(token_ids) & 3u))
+        return TL_EINVAL;
+    const int64_t tiles = N / p.pub.tile_n;
+    if (int64_t(num_groups) * tiles >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;
+    if (total_rows == 0) return TL_OK;
+    const int64_t c_bytes = total_rows * N * (p.out_bf16 ? 2 : 4);
+    const int64_t w_bytes = (int64_t(num_groups) - 1) * group_stride + N * K * 2;
+    if (overlap(C, c_bytes, A, a_rows * K * 2) || overlap(C, c_bytes, W, w_bytes)) return TL_EINVAL;
+
+    hipStream_t s = (hipStream_t)stream;
+    StreamState* st = nullptr;
+    rc = get_state(s, 0, &st);
+    if (rc != TL_OK) return rc;
+    DecodeLaunch d;
+    d.A = static_cast<const uint16_t*>(A);
+    d.W = static_cast<const uint8_t*>(W);
+    d.C = C;
+    d.ws = nullptr;
+    d.fetch = p.count ? st->fetch : nullptr;
+    d.M = std::min<int64_t>(max_group_rows, kDecodeMaxM);
+    d.N = N;
+    d.K = K;
+    d.L = p.L;
+    d.tile_n = p.pub.tile_n;
+    d.m_tiles16 = p.m_tiles16;
+    d.waves = 4;
+    d.split_k = 1;
+    d.k_unit = p.k_unit;
+    d.out_bf16 = p.out_bf16;
+    d.block_fetch = false;
+    d.fetch_G = 0;
+    d.num_groups = num_groups;
+    d.group_offsets = group_offsets;
+    d.token_ids = token_ids;
+    d.group_stride = group_stride;
+    d.a_rows = a_rows;
+    d.total_rows = total_rows;
+    return launch_decode(d, s) == hipSuccess ? TL_OK : TL_EHIP;
 }
 
 int tl_fetch_counter_read(void* stream, int64_t* bytes) {

@@ -51,6 +51,13 @@ struct DecodeParams {
     bool out_bf16;
     int log2_fetch;          // block-granular emulation on a row-major weight: log2(G)
     int64_t w_bytes;         // N * K * 2
+    // grouped (one launch over many weights, e.g. MoE experts)
+    const int* offsets;      // [groups + 1] output-row offsets of the groups
+    const int* token_ids;    // A row of each output row, or nullptr (identity)
+    int tiles_per_group;     // N / tile_n
+    int64_t group_stride;    // bytes between consecutive groups' weights
+    int a_rows;              // rows of A; token ids outside [0, a_rows) read zeros
+    int total_rows;          // rows of C; group offsets are clamped to [0, total_rows]
 };
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
@@ -98,15 +105,36 @@ __device__ inline bf16x8 load_stream(const uint8_t* p) {
 // one exchange between lanes l and l ^ 8:
 //     t = q < 8 ? x1 : x0,  s = t from lane l ^ 8,
 //     B0 = q < 8 ? x0 : s,  B1 = q < 8 ? s : x1.
-template <int MT, int NS, int U, int WAVES, bool TILE, bool BLOCKROW>
+//
+// Grouped launch (GROUPED): workgroup b serves group e = b / tiles_per_group
+// (one weight of a stack, e.g. one MoE expert) and its tile b % tiles_per_group
+// (split_k is 1).  The group's output rows [offsets[e], offsets[e+1]) are
+// clamped to [0, total_rows]; row r reads A row token_ids[r] (or r), and an
+// id outside [0, a_rows) reads zeros.  Rows are processed in chunks of
+// 16 MT, each chunk streaming the tile's weights again.
+template <int MT, int NS, int U, int WAVES, bool TILE, bool BLOCKROW, bool GROUPED>
 __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     constexpr int kWaves = WAVES;
     constexpr int kThreads = 64 * WAVES;
     constexpr int TN = 16 * NS;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int tile = blockIdx.x / p.split_k;
-    const int split = blockIdx.x - tile * p.split_k;
+    int tile, split, row0 = 0, rows = p.M;
+    const uint8_t* W = p.W;
+    if constexpr (GROUPED) {
+        const int e = blockIdx.x / p.tiles_per_group;
+        tile = blockIdx.x - e * p.tiles_per_group;
+        split = 0;
+        const int r0 = min(max(p.offsets[e], 0), p.total_rows);
+        const int r1 = min(max(p.offsets[e + 1], r0), p.total_rows);
+        if (r1 <= r0) return;                       // uniform over the workgroup
+        row0 = r0;
+        rows = r1 - r0;
+        W += int64_t(e) * p.group_stride;
+    } else {
+        tile = blockIdx.x / p.split_k;
+        split = blockIdx.x - tile * p.split_k;
+    }
 
     // K range of this split in 64-element steps
     const int u0 = int((int64_t(p.units) * split) / p.split_k);
@@ -127,8 +155,10 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
             int64_t off;
             if (TILE) off = int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << (p.log2_bc + 1));
             else off = int64_t(n) * p.K * 2;
-            wrow[j][hf] = p.W + off;
+            wrow[j][hf] = W + off;
         }
+    for (int mc = 0;;) {   // row chunks: one pass unless GROUPED
+    const int crows = rows - mc;
     // Activations are loaded like the weights (8 rows x 128 B per
     // instruction, then the lane exchange): lane (g, q) reads row
     // 16 mt + 8 hf + (q & 7) at this lane's chunk kc.  Rows past M read zeros;
@@ -140,9 +170,15 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
             const int m = mt * 16 + hf * 8 + (q & 7);
-            aok[mt][hf] = m < p.M;
-            aany[mt][hf] = mt * 16 + hf * 8 < p.M;
-            arow[mt][hf] = p.A + int64_t(aok[mt][hf] ? m : 0) * p.K + kc;
+            aok[mt][hf] = m < crows;
+            aany[mt][hf] = mt * 16 + hf * 8 < crows;
+            int arow_idx = m;
+            if constexpr (GROUPED) {
+                arow_idx = row0 + mc + m;
+                if (aok[mt][hf] && p.token_ids) arow_idx = p.token_ids[arow_idx];
+                aok[mt][hf] = aok[mt][hf] && arow_idx >= 0 && arow_idx < p.a_rows;
+            }
+            arow[mt][hf] = p.A + int64_t(aok[mt][hf] ? arow_idx : 0) * p.K + kc;
         }
 
     f32x4 acc[MT][NS];
@@ -280,11 +316,17 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int m = mt * 16 + (l >> 4) * 4 + r;
-            if (m < p.M) {
-                if (final_out) store_out(p.C, int64_t(m) * p.N + n, v[r], p.out_bf16);
-                else part[int64_t(m) * p.N + n] = v[r];
+            if (m < crows) {
+                const int64_t row = GROUPED ? int64_t(row0 + mc + m) : int64_t(m);
+                if (final_out) store_out(p.C, row * p.N + n, v[r], p.out_bf16);
+                else part[row * p.N + n] = v[r];
             }
         }
+    }
+    if constexpr (!GROUPED) break;
+    mc += 16 * MT;
+    if (mc >= rows) break;
+    __syncthreads();   // the next chunk rewrites red[]
     }
 }
 
@@ -314,35 +356,42 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, voi
     }
 }
 
-template <int MT, int NS, int WAVES, bool TILE>
+template <int MT, int NS, int WAVES, bool TILE, bool GROUPED>
 hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
     constexpr int U = MT >= 2 ? 2 : 4;   // steps in flight per wave; fewer for larger M (registers)
-    if (!TILE && p.log2_fetch > 0)   // block emulation: fewer steps in flight leave room for the block loop
-        hipLaunchKernelGGL((decode_kernel<MT, NS, 2, WAVES, TILE, !TILE>), dim3(grid), dim3(64 * WAVES), 0, stream, p);
-    else
-        hipLaunchKernelGGL((decode_kernel<MT, NS, U, WAVES, TILE, false>), dim3(grid), dim3(64 * WAVES), 0, stream, p);
+    if constexpr (!TILE && !GROUPED) {
+        if (p.log2_fetch > 0) {   // block emulation: fewer steps in flight leave room for the block loop
+            hipLaunchKernelGGL((decode_kernel<MT, NS, 2, WAVES, false, true, false>), dim3(grid), dim3(64 * WAVES), 0,
+                               stream, p);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((decode_kernel<MT, NS, U, WAVES, TILE, false, GROUPED>), dim3(grid), dim3(64 * WAVES), 0,
+                       stream, p);
     return hipGetLastError();
 }
 
 // Instantiated (MT, NS, waves) combinations -- those whose registers fit
-// the waves per SIMD they need; the planner only asks for these.
+// the waves per SIMD they need; the planner only asks for these.  Grouped
+// launches use 4 waves.
 template <int MT, int NS, bool TILE>
-hipError_t launch_w(const DecodeParams& p, int grid, int waves, hipStream_t stream) {
+hipError_t launch_w(const DecodeParams& p, int grid, int waves, bool grouped, hipStream_t stream) {
+    if (grouped) return launch_t<MT, NS, 4, TILE, true>(p, grid, stream);
     if constexpr (MT * NS <= 2) {
-        if (waves == 16) return launch_t<MT, NS, 16, TILE>(p, grid, stream);
+        if (waves == 16) return launch_t<MT, NS, 16, TILE, false>(p, grid, stream);
     }
     if constexpr (MT * NS <= 8) {
-        if (waves == 8) return launch_t<MT, NS, 8, TILE>(p, grid, stream);
+        if (waves == 8) return launch_t<MT, NS, 8, TILE, false>(p, grid, stream);
     }
-    return launch_t<MT, NS, 4, TILE>(p, grid, stream);
+    return launch_t<MT, NS, 4, TILE, false>(p, grid, stream);
 }
 
 template <int MT>
-hipError_t launch_m(const DecodeParams& p, int grid, int ns, int waves, bool tile, hipStream_t stream) {
-    if (ns == 2) return tile ? launch_w<MT, 2, true>(p, grid, waves, stream)
-                             : launch_w<MT, 2, false>(p, grid, waves, stream);
-    return tile ? launch_w<MT, 4, true>(p, grid, waves, stream)
-                : launch_w<MT, 4, false>(p, grid, waves, stream);
+hipError_t launch_m(const DecodeParams& p, int grid, int ns, int waves, bool tile, bool grouped, hipStream_t stream) {
+    if (ns == 2) return tile ? launch_w<MT, 2, true>(p, grid, waves, grouped, stream)
+                             : launch_w<MT, 2, false>(p, grid, waves, grouped, stream);
+    return tile ? launch_w<MT, 4, true>(p, grid, waves, grouped, stream)
+                : launch_w<MT, 4, false>(p, grid, waves, grouped, stream);
 }
 
 }  // namespace
@@ -369,13 +418,20 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.out_bf16 = d.out_bf16;
     p.log2_fetch = (!tile && d.block_fetch) ? ilog2(d.fetch_G) : 0;
     p.w_bytes = d.N * d.K * 2;
-    const int grid = int(d.N / d.tile_n) * d.split_k;
+    p.offsets = d.group_offsets;
+    p.token_ids = d.token_ids;
+    p.tiles_per_group = int(d.N / d.tile_n);
+    p.group_stride = d.group_stride;
+    p.a_rows = int(d.a_rows);
+    p.total_rows = int(d.total_rows);
+    const bool grouped = d.num_groups > 0;
+    const int grid = grouped ? d.num_groups * p.tiles_per_group : int(d.N / d.tile_n) * d.split_k;
     const int ns = d.tile_n / 16;
     hipError_t e;
     switch (d.m_tiles16) {
-        case 1: e = launch_m<1>(p, grid, ns, d.waves, tile, stream); break;
-        case 2: e = launch_m<2>(p, grid, ns, d.waves, tile, stream); break;
-        default: e = launch_m<4>(p, grid, ns, d.waves, tile, stream); break;
+        case 1: e = launch_m<1>(p, grid, ns, d.waves, tile, grouped, stream); break;
+        case 2: e = launch_m<2>(p, grid, ns, d.waves, tile, grouped, stream); break;
+        default: e = launch_m<4>(p, grid, ns, d.waves, tile, grouped, stream); break;
     }
     if (e != hipSuccess || d.split_k == 1) return e;
     const int64_t mn4 = d.M * d.N / 4;

@@ -56,6 +56,14 @@ struct DecodeLaunch {
     bool out_bf16;
     bool block_fetch;           // row-major weight read in whole fetch_G-byte blocks
     int64_t fetch_G;
+    // grouped launch (num_groups > 0; split_k 1, waves 4): group e has weight
+    // W + e * group_stride and output rows [group_offsets[e], group_offsets[e+1])
+    int num_groups = 0;
+    const int32_t* group_offsets = nullptr;
+    const int32_t* token_ids = nullptr;
+    int64_t group_stride = 0;
+    int64_t a_rows = 0;
+    int64_t total_rows = 0;
 };
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream);

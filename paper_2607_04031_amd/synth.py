@@ -137,3 +137,14 @@ def qwen_attn_seed(i: int) -> int:
 QWEN_SEED_HIDDEN = 3      # [64, 2048] hidden states: input of q, k, v and of the experts' gate+up
 QWEN_SEED_ATTN_O_IN = 5   # [64, 4096] attention output: input of o
 QWEN_SEED_DOWN_IN = 4     # [sum of tokens per expert, 768] input of the experts' down GEMMs
+
+
+def moe_tables(routing: np.ndarray, E: int = QWEN_EXPERTS) -> tuple[np.ndarray, np.ndarray]:
+    """Grouped-launch tables for a routing: int32 offsets [E + 1] (rows of
+    expert e are offsets[e] .. offsets[e+1] - 1) and int32 token ids, the
+    tokens of each expert in ascending order, experts one after another."""
+    tok = tokens_per_expert(routing, E)
+    offsets = np.zeros(E + 1, dtype=np.int32)
+    offsets[1:] = np.cumsum([len(t) for t in tok])
+    ids = np.concatenate(tok).astype(np.int32) if offsets[-1] else np.zeros(0, dtype=np.int32)
+    return offsets, ids

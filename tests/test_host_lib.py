@@ -191,3 +191,53 @@ def test_entry_points_reject_before_device_work():
     assert e.value.status == tl.TL_EINVAL
     # empty matrices are a no-op
     tl.tl_repack(0, 0, 0, 64, 2, 4096, 32, stream=0)
+
+
+def test_gemm_grouped_rejects_before_device_work():
+    """tl_gemm_grouped validates every argument on the host; each case below
+    fails before any HIP call (fake, aligned addresses), and total_rows == 0
+    is a no-op."""
+    N, K = 64, 128
+    good = dict(A=1 << 12, a_rows=64, token_ids=1 << 20, group_offsets=1 << 21, num_groups=4,
+                total_rows=32, max_group_rows=16, W=1 << 24, group_stride=N * K * 2, C=1 << 30,
+                N=N, K=K, layout=tl.layout(), fetch_mode=tl.TL_FETCH_BLOCK)
+
+    def call(**kw):
+        a = dict(good, **kw)
+        tl.tl_gemm_grouped(a["A"], a["a_rows"], a["token_ids"], a["group_offsets"], a["num_groups"],
+                           a["total_rows"], a["max_group_rows"], a["W"], a["group_stride"], a["C"],
+                           a["N"], a["K"], a["layout"], a["fetch_mode"], stream=0)
+
+    cases = [
+        (dict(num_groups=0), tl.TL_EINVAL),
+        (dict(total_rows=-1), tl.TL_EINVAL),
+        (dict(a_rows=0), tl.TL_EINVAL),
+        (dict(max_group_rows=0), tl.TL_EINVAL),
+        (dict(token_ids=None, a_rows=16), tl.TL_EINVAL),         # identity rows past A
+        (dict(group_stride=N * K * 2 - 16), tl.TL_EINVAL),
+        (dict(group_stride=N * K * 2 + 8), tl.TL_EINVAL),
+        (dict(group_offsets=None), tl.TL_EINVAL),
+        (dict(group_offsets=(1 << 21) + 2), tl.TL_EINVAL),
+        (dict(token_ids=(1 << 20) + 1), tl.TL_EINVAL),
+        (dict(A=(1 << 12) + 8), tl.TL_EINVAL),
+        (dict(C=(1 << 12) + 64), tl.TL_EINVAL),                   # C overlaps A
+        (dict(C=(1 << 24) + 4096), tl.TL_EINVAL),                 # C overlaps W
+        (dict(N=48), tl.TL_EINVAL),                               # N % block_rows
+        (dict(layout=tl.layout(split_k=2)), tl.TL_EUNSUPPORTED),
+        (dict(layout=tl.layout(tile_m=128)), tl.TL_EUNSUPPORTED),
+        (dict(layout=tl.layout(kind=tl.TL_LAYOUT_NK_ROW)), None),  # valid: checked by its own case below
+        (dict(layout=tl.layout(kind=tl.TL_LAYOUT_NK_ROW), fetch_mode=tl.TL_FETCH_BLOCK), None),
+        (dict(layout=tl.layout(kind=tl.TL_LAYOUT_KN_ROW)), tl.TL_EUNSUPPORTED),
+        (dict(num_groups=1 << 30, N=4096, group_stride=4096 * K * 2), tl.TL_EUNSUPPORTED),  # grid >= 2^31
+    ]
+    for kw, status in cases:
+        if status is None:
+            continue
+        with pytest.raises(tl.TLError) as e:
+            call(**kw)
+        assert e.value.status == status, kw
+    # row-major weights read in whole blocks are a decode-only (ungrouped) mode
+    with pytest.raises(tl.TLError) as e:
+        call(layout=tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=4096), fetch_mode=tl.TL_FETCH_BLOCK)
+    assert e.value.status == tl.TL_EUNSUPPORTED
+    call(total_rows=0)                                            # enqueues nothing

@@ -218,6 +218,67 @@ def test_gemm_points_equal_full():
     assert np.array_equal(oracle.gemm_f64_points(A, W, ms, ns), full[ms, ns])
 
 
+def _group_of_row(offsets, r):
+    """Group of output row r by a linear scan (the grouped oracle loops over groups instead)."""
+    for e in range(len(offsets) - 1):
+        if offsets[e] <= r < offsets[e + 1]:
+            return e
+    raise AssertionError(r)
+
+
+@pytest.mark.parametrize("with_ids", [True, False])
+def test_grouped_gemm_brute_force_rows(with_ids):
+    """Row-wise brute force with exact integers: row r takes the weight of the
+    group whose offset range holds r and the A row its token id names.  Empty
+    groups (first, middle, last) and a token used by several groups included."""
+    K, N = 24, 5
+    offsets = [0, 0, 3, 3, 7, 8, 8]
+    A = synth.small_int_bf16((6 if with_ids else 8, K), seed=21)
+    Ws = [synth.small_int_bf16((N, K), seed=30 + e) for e in range(len(offsets) - 1)]
+    ids = np.array([5, 0, 2, 2, 1, 4, 0, 3]) if with_ids else None
+    got = oracle.grouped_gemm_f64(A, ids, offsets, Ws)
+    Ai = synth.bf16_bits_to_f32(A).astype(np.int64)
+    assert got.shape == (offsets[-1], N)
+    for r in range(offsets[-1]):
+        e = _group_of_row(offsets, r)
+        t = ids[r] if with_ids else r
+        Wi = synth.bf16_bits_to_f32(Ws[e]).astype(np.int64)
+        for n in range(N):
+            assert got[r, n] == float(sum(int(Ai[t, k]) * int(Wi[n, k]) for k in range(K)))
+
+
+def test_grouped_gemm_equals_stacked_weights_einsum():
+    """The same rows through a per-row weight stack and numpy einsum in float64."""
+    K, N = 64, 12
+    routing = synth.moe_routing(M=10, E=6, topk=2, seed=5)
+    offsets, ids = synth.moe_tables(routing, E=6)
+    A = synth.normal_bf16((10, K), seed=6)
+    Ws = [synth.normal_bf16((N, K), seed=40 + e, sigma=0.02) for e in range(6)]
+    got = oracle.grouped_gemm_f64(A, ids, offsets, Ws)
+    Af = synth.bf16_bits_to_f32(A).astype(np.float64)
+    Wf = np.stack([synth.bf16_bits_to_f32(W).astype(np.float64) for W in Ws])
+    groups = np.searchsorted(offsets, np.arange(offsets[-1]), side="right") - 1
+    want = np.einsum("rnk,rk->rn", Wf[groups], Af[ids])
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-14)
+
+
+def test_moe_routing_tables():
+    """Top-8 of 128 distinct experts per token: every token appears in exactly
+    8 groups, once per group, and group rows list tokens in ascending order."""
+    routing = synth.moe_routing()
+    assert routing.shape == (synth.QWEN_TOKENS, synth.QWEN_TOPK)
+    assert all(len(set(r)) == synth.QWEN_TOPK for r in routing.tolist())
+    offsets, ids = synth.moe_tables(routing)
+    assert offsets[0] == 0 and offsets[-1] == synth.QWEN_TOKENS * synth.QWEN_TOPK
+    assert np.all(np.diff(offsets) >= 0)
+    assert np.array_equal(np.bincount(ids, minlength=synth.QWEN_TOKENS),
+                          np.full(synth.QWEN_TOKENS, synth.QWEN_TOPK))
+    for e in range(synth.QWEN_EXPERTS):
+        g = ids[offsets[e]:offsets[e + 1]]
+        assert np.all(np.diff(g) > 0)
+        assert all(e in routing[t] for t in g.tolist())
+
+
 def test_round_bf16_against_float32_bit_rounding():
     """The oracle's bf16 rounding of doubles equals numpy float32 -> bf16 RNE
     on values that are exactly float32, and breaks ties to even."""
