@@ -121,6 +121,7 @@ struct Plan {
     int64_t k_unit = 64;
     bool block_row = false;      // block-granular emulation on a row-major weight
     int64_t fetch_G = 0;
+    int64_t n_main = 0;          // prefill: columns covered by the main tiles (rest: 128 x 128)
 };
 
 constexpr int kDecodeMaxM = 64;
@@ -227,12 +228,30 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         if (d->split_k > 1) return TL_EUNSUPPORTED;
         // the kernel addresses A and W with 32-bit byte offsets
         if (M * K * 2 >= (int64_t(1) << 32) || N * K * 2 >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;
+        // Quantisation: 256 x 256 tiles that leave the last round of
+        // workgroups part-empty (QKV at M = 2048: 320 tiles on 256 CUs) cover
+        // the widest column range whose tile count is a multiple of the CU
+        // count, and a second launch of 128 x 128 tiles covers the remaining
+        // columns when they fit in one round (two 128 x 128 workgroups per CU).
+        p.n_main = N;
+        const int64_t mt = (M + tm - 1) / tm;
+        const int64_t tiles = mt * ((N + tn - 1) / tn);
+        if (!d->tile_m && !d->tile_n && tm == 256 && tn == 256 && N % 256 == 0 && tiles > kCUs &&
+            tiles % kCUs != 0 && (!tile || 128 % p.L.br == 0)) {
+            for (int64_t n1 = N - 256; n1 >= 256; n1 -= 256) {
+                if ((mt * (n1 / 256)) % kCUs) continue;
+                const int64_t rest = ((M + 127) / 128) * ((N - n1) / 128);
+                if (rest <= 2 * kCUs) p.n_main = n1;
+                break;
+            }
+        }
         p.pub.tile_m = tm;
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
         p.pub.split_k = 1;
-        p.pub.waves = 4;
-        p.pub.workgroups = ((M + tm - 1) / tm) * ((N + tn - 1) / tn);
+        p.pub.waves = tm == 256 && tn == 256 ? 8 : 4;
+        p.pub.workgroups = mt * (p.n_main / tn + (p.n_main % tn ? 1 : 0)) +
+                           ((M + 127) / 128) * ((N - p.n_main) / 128);
         p.pub.workspace_bytes = 0;
     }
     *P = p;
@@ -334,6 +353,7 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
         q.tile_m = p.pub.tile_m;
         q.tile_n = p.pub.tile_n;
         q.out_bf16 = p.out_bf16;
+        q.n_main = p.n_main;
         e = launch_prefill(q, s);
     }
     return e == hipSuccess ? TL_OK : TL_EHIP;

@@ -78,6 +78,9 @@ struct PrefillLaunch {
     int tile_m;                 // 128 or 256
     int tile_n;                 // 128 or 256 (256 only with tile_m 256)
     bool out_bf16;
+    // columns [0, n_main) use tile_m x tile_n tiles; columns [n_main, N), if
+    // any, a second launch of 128 x 128 tiles (n_main is a multiple of tile_n)
+    int64_t n_main;
 };
 
 hipError_t launch_prefill(const PrefillLaunch& p, hipStream_t stream);

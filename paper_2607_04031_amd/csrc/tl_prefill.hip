@@ -34,6 +34,7 @@ struct PrefillParams {
     void* C;
     unsigned long long* fetch;
     int M, N, K;
+    int64_t ldc;             // row stride of C in elements (N of the whole GEMM)
     int m_tiles;
     int64_t strip_bytes;
     int log2_br, log2_bc, log2_G;
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
                     const int row = row_base + i * 32 + 8 * (v >> 2) + (v & 3);
                     const int col = col_base + j * 32;
                     if (full || (row < p.M && col < p.N))
-                        C[int64_t(row) * p.N + col] = f32_to_bf16_rne(acc[i][j][v]);
+                        C[int64_t(row) * p.ldc + col] = f32_to_bf16_rne(acc[i][j][v]);
                 }
     } else {
         float* C = static_cast<float*>(p.C);
@@ -225,7 +226,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
                 for (int v = 0; v < 16; ++v) {
                     const int row = row_base + i * 32 + 8 * (v >> 2) + (v & 3);
                     const int col = col_base + j * 32;
-                    if (full || (row < p.M && col < p.N)) C[int64_t(row) * p.N + col] = acc[i][j][v];
+                    if (full || (row < p.M && col < p.N)) C[int64_t(row) * p.ldc + col] = acc[i][j][v];
                 }
     }
 }
@@ -237,18 +238,23 @@ hipError_t launch_t(const PrefillParams& p, int grid, bool tile, hipStream_t s) 
     return hipGetLastError();
 }
 
-}  // namespace
-
-hipError_t launch_prefill(const PrefillLaunch& q, hipStream_t stream) {
+// One launch over columns [n_begin, n_begin + n_cols) of the GEMM with
+// tile_m x tile_n tiles.  The weight rows of that range start n_begin * K * 2
+// bytes into W in both layouts (tile-major strips of block_rows rows are
+// contiguous, and n_begin is a multiple of block_rows).
+hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols, int tile_m, int tile_n,
+                        hipStream_t stream) {
     PrefillParams p;
+    const int64_t c_elem = q.out_bf16 ? 2 : 4;
     p.A = q.A;
-    p.W = q.W;
-    p.C = q.C;
+    p.W = q.W + n_begin * q.K * 2;
+    p.C = static_cast<uint8_t*>(q.C) + n_begin * c_elem;
     p.fetch = q.fetch;
     p.M = int(q.M);
-    p.N = int(q.N);
+    p.N = int(n_cols);
     p.K = int(q.K);
-    p.m_tiles = int((q.M + q.tile_m - 1) / q.tile_m);
+    p.ldc = q.N;
+    p.m_tiles = int((q.M + tile_m - 1) / tile_m);
     const bool tile = q.L.kind == TL_LAYOUT_TILE;
     p.strip_bytes = tile ? q.L.br * q.K * 2 : 0;
     p.log2_br = tile ? q.L.log2_br : 0;
@@ -257,12 +263,20 @@ hipError_t launch_prefill(const PrefillLaunch& q, hipStream_t stream) {
     p.br_mask = tile ? int(q.L.br - 1) : 0;
     p.bc_mask = tile ? int(q.L.bc - 1) : 0;
     p.out_bf16 = q.out_bf16;
-    const int64_t n_tiles = (q.N + q.tile_n - 1) / q.tile_n;
+    const int64_t n_tiles = (n_cols + tile_n - 1) / tile_n;
     const int grid = int(p.m_tiles * n_tiles);
     // 256x256: 8 waves (2 per SIMD) of 128x64; smaller tiles: 4 waves in 2 x 2
-    if (q.tile_m == 256 && q.tile_n == 256) return launch_t<256, 256, 2, 4>(p, grid, tile, stream);
-    if (q.tile_m == 256) return launch_t<256, 128, 2, 2>(p, grid, tile, stream);
+    if (tile_m == 256 && tile_n == 256) return launch_t<256, 256, 2, 4>(p, grid, tile, stream);
+    if (tile_m == 256) return launch_t<256, 128, 2, 2>(p, grid, tile, stream);
     return launch_t<128, 128, 2, 2>(p, grid, tile, stream);
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const PrefillLaunch& q, hipStream_t stream) {
+    hipError_t e = launch_range(q, 0, q.n_main, q.tile_m, q.tile_n, stream);
+    if (e != hipSuccess || q.n_main == q.N) return e;
+    return launch_range(q, q.n_main, q.N - q.n_main, 128, 128, stream);
 }
 
 }  // namespace tl

@@ -289,6 +289,36 @@ def test_prefill_tile_major_parity(M, N, K, tm, tn):
     parity_bf16_out(host_bits(Cb), y_ref, "prefill bf16")
 
 
+@pytest.mark.parametrize("bf16_out", [False, True])
+def test_prefill_column_split_plan(bf16_out):
+    """M = 1024, N = 33024: 516 tiles of 256 x 256 would leave 252 CUs idle in a
+    third round, so the plan covers columns [0, 32768) with 256 x 256 tiles
+    (two full rounds) and the last 256 columns with a second launch of
+    128 x 128 tiles."""
+    M, N, K = 1024, 33024, 256
+    plan = tl.tl_gemm_plan(M, N, K, tl.layout())
+    assert plan["workgroups"] == 512 + 16
+    banner(f"prefill column split bf16_out={bf16_out}")
+    A = synth.normal_bf16((M, K), seed=91)
+    W = synth.normal_bf16((N, K), seed=92, sigma=synth.W_SIGMA)
+    d = tl.layout(out_dtype=tl.TL_OUT_BF16 if bf16_out else tl.TL_OUT_F32)
+    C = run_gemm(A, W, d)
+    y_ref = oracle.gemm_f64(A, W)
+    if bf16_out:
+        parity_bf16_out(host_bits(C), y_ref, "split bf16")
+    else:
+        parity(host_f32(C), y_ref, "split f32")
+
+
+def test_prefill_column_split_exact():
+    M, N, K = 1024, 33024, 256
+    A = synth.small_int_bf16((M, K), seed=93)
+    W = synth.small_int_bf16((N, K), seed=94)
+    banner("prefill column split exact")
+    C = run_gemm(A, W, tl.layout())
+    assert np.array_equal(host_f32(C).astype(np.float64), oracle.gemm_f64(A, W))
+
+
 def test_prefill_exact_inputs():
     M, N, K = 256, 256, 1024
     banner("prefill one-hot / small-int")
@@ -373,12 +403,20 @@ def test_llama_prefill_full_size_sampled(i, name, N, K):
     M = synth.LLAMA_PREFILL_M
     A_bits = synth.normal_bf16((M, K), seed=synth.llama_prefill_act_seed(i))
     A = dev_bf16(A_bits)
-    for tm, tn in ((128, 128), (256, 128), (256, 256)):
+    # (0, 0): the library's plan, the one bench.py times (QKV: 256 x 256 tiles
+    # on columns [0, 8192), 128 x 128 tiles on the rest)
+    for tm, tn in ((128, 128), (256, 128), (256, 256), (0, 0)):
         C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
         tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16),
                    tl.TL_FETCH_BLOCK)
         _sync()
         _sampled_check(A_bits, W_bits, C, 512, seed=tm + tn + i, bf16_out=True)
+    if N == 10240:
+        # both sides of the column split, every row tile
+        ms = np.repeat(np.arange(0, M, 97), 4)
+        ns = np.tile(np.array([8190, 8191, 8192, 8193]), len(ms) // 4)
+        got = C[torch.from_numpy(ms).cuda(), torch.from_numpy(ns).cuda()]
+        parity_bf16_out(host_bits(got), oracle.gemm_f64_points(A_bits, W_bits, ms, ns), "split boundary")
 
 
 # ---------------------------------------------------------------------------

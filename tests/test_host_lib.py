@@ -134,6 +134,23 @@ def test_gemm_plan_decode_and_prefill_shapes():
     assert p["tile_m"] == 128
 
 
+def test_prefill_plan_column_split():
+    """256 x 256 tiles whose count leaves the last round part-empty are kept on
+    the widest column range with a whole number of rounds; the rest of the
+    columns take 128 x 128 tiles when those fit in one round."""
+    bf = tl.layout(out_dtype=tl.TL_OUT_BF16)
+    assert tl.tl_gemm_plan(2048, 10240, 8192, bf)["workgroups"] == 256 + 256      # QKV
+    assert tl.tl_gemm_plan(2048, 8192, 8192, bf)["workgroups"] == 256              # O: no split
+    assert tl.tl_gemm_plan(2048, 57344, 8192, bf)["workgroups"] == 1792            # gate+up: 7 rounds
+    assert tl.tl_gemm_plan(4096, 10240, 8192, bf)["workgroups"] == 512 + 512
+    # pinned tiles are never split
+    pinned = tl.layout(tile_m=256, tile_n=256, out_dtype=tl.TL_OUT_BF16)
+    assert tl.tl_gemm_plan(2048, 10240, 8192, pinned)["workgroups"] == 320
+    # a memory tile taller than the 128-row remainder tiles keeps one launch
+    tall = tl.layout(G=65536, block_rows=256, out_dtype=tl.TL_OUT_BF16)
+    assert tl.tl_gemm_plan(2048, 10240, 8192, tall)["workgroups"] == 320
+
+
 def test_gemm_plan_error_codes():
     d = tl.layout()
     cases = [
