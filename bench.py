@@ -17,6 +17,7 @@ read in whole 4 KB blocks (a large-granularity memory emulated), with the
 fetch amplification the kernel counts; prefill TFLOP/s at M = 2048 (the
 library's plan, and tiles 256x256x64, 256x128x64, 128x128x64 pinned; bf16 out); a Qwen-3-30B-A3B-shaped MoE
 layer (64 tokens, top-8 of 128 experts, plus the attention projections);
+the TileLens-HW view load of an 8192 x 8192 box (2-D and 4-D views);
 read amplification of the decode tile and of the paper's 128 x 256 tile;
 repack GB/s; the decode kernel's roofline; the CPU oracle on a bounded sample.
 
@@ -312,6 +313,32 @@ def moe_layer(ctx, steps, warmup):
     return res
 
 
+def view_load(ctx, weights):
+    """tl_view_load of an 8192 x 8192 bf16 box of the down weight (K x N
+    order: 8192 contiguous elements x 8192 columns), as a 2-D view and as an
+    equivalent 4-D view (the contiguous dimension split in two, the columns in
+    strips of 256); bytes read + written per second."""
+    tl, torch = ctx.tl, ctx.torch
+    _, N, K, Wt = weights[3]
+    box_bytes = 8192 * 8192 * 2
+    out = torch.empty(box_bytes, dtype=torch.uint8, device=ctx.dev)
+    views = {"2d": tl.view([1, K], [4096, 0], [8192, 8192]),
+             "4d": tl.view([1, 4096, K, 256 * K], [0, 1, 0, 0], [4096, 2, 256, 32])}
+    res = {}
+    for name, v in views.items():
+        tl.tl_view_load(Wt, v, K, N, 2, G, BR, out)
+        ev = ctx.event_pairs(1)[0]
+        ev[0].record(ctx.stream)
+        for _ in range(5):
+            tl.tl_view_load(Wt, v, K, N, 2, G, BR, out)
+        ev[1].record(ctx.stream)
+        torch.cuda.synchronize()
+        us = ev[0].elapsed_time(ev[1]) * 1e3 / 5
+        res[name] = {"us": round(us, 1), "GB/s": round(2 * box_bytes / (us * 1e-6) / 1e9, 1)}
+    log(f"view load: {res}")
+    return res
+
+
 def granularity_sweep(ctx):
     """Down projection [8192, 28672] for each memory tile (G, block_rows): the
     exact read amplification of 32 x tn x tk compute tiles over the tile-major
@@ -451,6 +478,7 @@ def main():
         torch.cuda.empty_cache()
         extras["moe_qwen3_30b_a3b_64_tokens"] = moe_layer(ctx, args.steps, args.warmup)
         torch.cuda.empty_cache()
+        extras["view_load"] = view_load(ctx, weights)
 
     # ---------------- read amplification ----------------
     plan = tl.tl_gemm_plan(DECODE_M, 8192, 8192, desc, tl.TL_FETCH_BLOCK)

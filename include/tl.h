@@ -231,6 +231,55 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
 int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
                 int32_t tile_k, const tl_layout_desc* layout, int64_t G, tl_amp* out);
 
+/* A multi-dimensional view of a weight, as a TMA descriptor would give it
+ * (Section 4.3): the K x N weight (K contiguous: W[N][K] row-major, the
+ * paper's column-major K x N) seen as a tensor of rank 'rank' whose
+ * dimension d advances strides[d] elements (strides[0] = 1, the contiguous
+ * dimension; a stride >= K is a whole number of columns, K apart), and a box
+ * of box[0] x ... x box[rank-1] elements starting at coords. */
+#define TL_VIEW_MAX_RANK 5
+typedef struct tl_view {
+    int32_t rank;                         /* 1 .. TL_VIEW_MAX_RANK */
+    int32_t box[TL_VIEW_MAX_RANK];        /* elements loaded per dimension (the TMA tile) */
+    int64_t strides[TL_VIEW_MAX_RANK];    /* element strides; strides[0] = 1 */
+    int64_t coords[TL_VIEW_MAX_RANK];     /* first element of the box per dimension */
+} tl_view;
+
+/*
+ * tl_view_offsets -- host only: the byte offsets, from the weight's base, of
+ * every element of the view's box in a tile-major weight (memory tile
+ * G / (elem_bytes * block_rows) x block_rows, as tl_repack writes it), in
+ * the order a TMA load visits them (dimension 0 fastest).  They are generated
+ * the way TileLens-HW extends the TMA engine (Section 4.3): the tile base from
+ * the split-and-sum of coordinate x stride products around the leading stride
+ * K (Eq. 4), nested counters with the strides of Eq. 5, and for a box
+ * narrower than the memory tile (Case 2) the bit permutation of the
+ * intra-tile offset.  *count (if not NULL) receives the element count; with
+ * offsets == NULL nothing else is written.
+ * Errors: TL_EINVAL for a bad layout (see tl_repack), K % block_cols or
+ * N % block_rows != 0, rank outside 1..5, strides[0] != 1, a non-positive
+ * stride or box, a negative coordinate, a stride >= K that is not a multiple
+ * of K, a box reaching outside the K x N matrix, or capacity < count;
+ * TL_EUNSUPPORTED when the view breaks the invariants the hardware relies on:
+ * box[0] not a power of two, a box not starting on a memory-tile boundary, a
+ * row-index stride that is not a whole number of memory tiles, or a column
+ * stride that splits a memory tile other than the one-column stride K.
+ */
+int tl_view_offsets(const tl_view* view, int64_t K, int64_t N, int32_t elem_bytes, int64_t G,
+                    int32_t block_rows, int64_t* offsets, int64_t capacity, int64_t* count);
+
+/*
+ * tl_view_load -- device: the TMA-like load of the view's box from a
+ * tile-major weight.  src_tm: device, the N x K weight as tl_repack wrote it.
+ * dst: device, receives count * elem_bytes bytes, the box's elements densely
+ * in view order (dimension 0 fastest).  Source addresses are computed on the
+ * GPU by the same generator as tl_view_offsets.  Both pointers 16-byte
+ * aligned, not overlapping.  Errors: those of tl_view_offsets, TL_EINVAL for
+ * NULL, misaligned or overlapping pointers, TL_EHIP if the launch fails.
+ */
+int tl_view_load(const void* src_tm, const tl_view* view, int64_t K, int64_t N, int32_t elem_bytes,
+                 int64_t G, int32_t block_rows, void* dst, void* stream);
+
 /* tl_fetch_counter_read -- synchronises 'stream', stores the weight bytes
  * tallied by tl_gemm calls made on it with TL_FETCH_COUNT since the last read
  * into *bytes, and resets the tally to zero.  Errors: TL_EINVAL for NULL

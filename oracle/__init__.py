@@ -15,6 +15,9 @@ What each function follows (TileLens, arxiv 2607.04031):
   grouped_gemm_f64  the expert GEMMs of a mixture-of-experts layer (Sections
                  2.3 and 6.2): per group, gather its rows of A and apply
                  gemm_f64 with that group's weight
+  view_offsets   Section 4.3: tile-major byte offsets of the elements of a
+                 box of a multi-dimensional view (linear index -> (i, j) ->
+                 Eq. 2), in the order a TMA load visits them
   round_bf16     round-to-nearest-even to 8 significant bits
   read_amp       Sections 1, 2.5 and 6.4 (requests per compute tile at
                  granularity G; weights only, Section 5.1)
@@ -72,6 +75,8 @@ def _load():
     lib.orc_round_bf16.argtypes = [ctypes.c_double]
     lib.orc_round_bf16_array.restype = None
     lib.orc_round_bf16_array.argtypes = [p, p, i64]
+    lib.orc_view_offsets.restype = i64
+    lib.orc_view_offsets.argtypes = [ctypes.c_int, p, p, p, i64, i64, i64, i64, p]
     lib.orc_read_amp.restype = ctypes.c_int
     lib.orc_read_amp.argtypes = [i64] * 6 + [ctypes.c_int] + [i64] * 4 + [
         ctypes.c_int, ctypes.POINTER(Amp)]
@@ -113,6 +118,25 @@ def unpack(src_tm: np.ndarray, G: int, block_rows: int) -> np.ndarray:
     out = np.empty_like(src_tm)
     _load().orc_unpack(_ptr(_as_bytes(src_tm)), _ptr(out), rows, cols, s, G, block_rows)
     return out
+
+
+def view_offsets(strides, coords, box, K: int, s: int, G: int, block_rows: int) -> np.ndarray:
+    """int64 byte offsets, dimension 0 fastest, of every element of the box."""
+    rank = len(box)
+    assert len(strides) == len(coords) == rank <= 8
+    st = np.ascontiguousarray(strides, dtype=np.int64)
+    co = np.ascontiguousarray(coords, dtype=np.int64)
+    bx = np.ascontiguousarray(box, dtype=np.int64)
+    out = np.empty(int(np.prod(bx)), dtype=np.int64)
+    _load().orc_view_offsets(rank, _ptr(st), _ptr(co), _ptr(bx), K, s, G, block_rows, _ptr(out))
+    return out
+
+
+def view_gather(src_tm: np.ndarray, strides, coords, box, K: int, s: int, G: int, block_rows: int) -> np.ndarray:
+    """Bytes of the box's elements from a tile-major buffer, in view order (uint8 [elements * s])."""
+    offs = view_offsets(strides, coords, box, K, s, G, block_rows)
+    raw = _as_bytes(src_tm).reshape(-1)
+    return raw[(offs[:, None] + np.arange(s)[None, :]).reshape(-1)]
 
 
 def gemm_f64(A_bf16: np.ndarray, W_bf16: np.ndarray) -> np.ndarray:

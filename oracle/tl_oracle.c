@@ -72,6 +72,36 @@ void orc_unpack(const uint8_t* src, uint8_t* dst, int64_t rows, int64_t cols,
                    src + orc_tm_offset(r, c, cols, s, G, block_rows), (size_t)s);
 }
 
+/* A multi-dimensional view of a K x N column-major matrix (Section 4.3,
+ * "Challenges of supporting tile-major in TMA"): dimension d has extent
+ * dims[d] and element stride strides[d]; the box of box[0] x ... elements
+ * starts at coords.  Elements are visited with dimension 0 fastest (the
+ * order in which a TMA load writes its destination).  For each one the
+ * view's linear element index lin = sum_d (coords[d] + x_d) * strides[d] is
+ * the column-major index j * K + i of the matrix element, so i = lin mod K and
+ * j = lin / K, and its tile-major byte offset is Eq. 2.  out[] receives one
+ * offset per box element.  Returns the number of elements. */
+int64_t orc_view_offsets(int rank, const int64_t* strides, const int64_t* coords,
+                         const int64_t* box, int64_t K, int64_t s, int64_t G,
+                         int64_t block_rows, int64_t* out) {
+    int64_t x[8] = {0};
+    int64_t n = 1;
+    for (int d = 0; d < rank; ++d) n *= box[d];
+    for (int64_t e = 0; e < n; ++e) {
+        int64_t lin = 0;
+        for (int d = 0; d < rank; ++d) lin += (coords[d] + x[d]) * strides[d];
+        int64_t i = lin % K, j = lin / K;
+        out[e] = orc_tm_offset(j, i, K, s, G, block_rows);
+        /* next element: dimension 0 fastest */
+        for (int d = 0; d < rank; ++d) {
+            x[d] += 1;
+            if (x[d] < box[d]) break;
+            x[d] = 0;
+        }
+    }
+    return n;
+}
+
 /* ---------------------------------------------------------------------- */
 /* GEMM                                                                    */
 /* ---------------------------------------------------------------------- */

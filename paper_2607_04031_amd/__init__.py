@@ -36,7 +36,25 @@ TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
 EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
-            "tl_fetch_counter_read", "tl_release", "tl_strerror")
+            "tl_view_offsets", "tl_view_load", "tl_fetch_counter_read", "tl_release", "tl_strerror")
+TL_VIEW_MAX_RANK = 5
+
+
+class View(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_int32),
+                ("box", ctypes.c_int32 * 5),
+                ("strides", ctypes.c_int64 * 5),
+                ("coords", ctypes.c_int64 * 5)]
+
+
+def view(strides, coords, box) -> View:
+    """tl_view of rank len(box); dimension 0 is the contiguous one."""
+    v = View()
+    v.rank = len(box)
+    assert len(strides) == len(coords) == v.rank <= 5
+    for d in range(v.rank):
+        v.box[d], v.strides[d], v.coords[d] = int(box[d]), int(strides[d]), int(coords[d])
+    return v
 
 
 class LayoutDesc(ctypes.Structure):
@@ -107,6 +125,10 @@ def load_library():
     lib.tl_gemm_grouped.restype = ctypes.c_int
     lib.tl_gemm_grouped.argtypes = [p, i64, p, p, i32, i64, i64, p, i64, p, i64, i64,
                                     ctypes.POINTER(LayoutDesc), i32, p]
+    lib.tl_view_offsets.restype = ctypes.c_int
+    lib.tl_view_offsets.argtypes = [ctypes.POINTER(View), i64, i64, i32, i64, i32, p, i64, ctypes.POINTER(i64)]
+    lib.tl_view_load.restype = ctypes.c_int
+    lib.tl_view_load.argtypes = [p, ctypes.POINTER(View), i64, i64, i32, i64, i32, p, p]
     lib.tl_read_amp.restype = ctypes.c_int
     lib.tl_read_amp.argtypes = [i64, i64, i64, i32, i32, i32, ctypes.POINTER(LayoutDesc), i64,
                                 ctypes.POINTER(Amp)]
@@ -193,6 +215,24 @@ def tl_gemm_grouped(A, a_rows, token_ids, group_offsets, num_groups, total_rows,
     _check(load_library().tl_gemm_grouped(_ptr(A), a_rows, _ptr(token_ids), _ptr(group_offsets), num_groups,
                                           total_rows, max_group_rows, _ptr(W), group_stride, _ptr(C), N, K,
                                           ctypes.byref(d), fetch_mode, _stream(stream)), "tl_gemm_grouped")
+
+
+def tl_view_offsets(v: View, K, N, elem_bytes, G, block_rows):
+    """numpy int64 byte offsets of the box's elements (view order)."""
+    import numpy as np
+    lib = load_library()
+    n = ctypes.c_int64(0)
+    _check(lib.tl_view_offsets(ctypes.byref(v), K, N, elem_bytes, G, block_rows, None, 0, ctypes.byref(n)),
+           "tl_view_offsets")
+    out = np.empty(n.value, dtype=np.int64)
+    _check(lib.tl_view_offsets(ctypes.byref(v), K, N, elem_bytes, G, block_rows, out.ctypes.data, n.value,
+                               ctypes.byref(n)), "tl_view_offsets")
+    return out
+
+
+def tl_view_load(src_tm, v: View, K, N, elem_bytes, G, block_rows, dst, stream=None):
+    _check(load_library().tl_view_load(_ptr(src_tm), ctypes.byref(v), K, N, elem_bytes, G, block_rows, _ptr(dst),
+                                       _stream(stream)), "tl_view_load")
 
 
 def tl_read_amp(M, N, K, tile_m, tile_n, tile_k, layout, G) -> dict:

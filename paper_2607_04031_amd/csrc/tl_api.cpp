@@ -411,6 +411,31 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, con
     return launch_decode(d, s) == hipSuccess ? TL_OK : TL_EHIP;
 }
 
+int tl_view_offsets(const tl_view* view, int64_t K, int64_t N, int32_t elem_bytes, int64_t G, int32_t block_rows,
+                    int64_t* offsets, int64_t capacity, int64_t* count) {
+    ViewProgram P;
+    int rc = make_view_program(view, K, N, elem_bytes, G, block_rows, &P);
+    if (rc != TL_OK) return rc;
+    if (count) *count = P.elements;
+    if (!offsets) return TL_OK;
+    if (capacity < P.elements) return TL_EINVAL;
+    for (int64_t e = 0; e < P.elements; ++e) offsets[e] = view_offset(P, e);
+    return TL_OK;
+}
+
+int tl_view_load(const void* src_tm, const tl_view* view, int64_t K, int64_t N, int32_t elem_bytes, int64_t G,
+                 int32_t block_rows, void* dst, void* stream) {
+    ViewProgram P;
+    int rc = make_view_program(view, K, N, elem_bytes, G, block_rows, &P);
+    if (rc != TL_OK) return rc;
+    if (!src_tm || !dst || !aligned16(src_tm) || !aligned16(dst)) return TL_EINVAL;
+    const int64_t src_bytes = N * K * elem_bytes, dst_bytes = P.elements * elem_bytes;
+    if (overlap(src_tm, src_bytes, dst, dst_bytes)) return TL_EINVAL;
+    hipError_t e = launch_view_load(static_cast<const uint8_t*>(src_tm), src_bytes, P, static_cast<uint8_t*>(dst),
+                                    (hipStream_t)stream);
+    return e == hipSuccess ? TL_OK : TL_EHIP;
+}
+
 int tl_fetch_counter_read(void* stream, int64_t* bytes) {
     if (!bytes) return TL_EINVAL;
     hipStream_t s = (hipStream_t)stream;
