@@ -17,7 +17,8 @@ read in whole 4 KB blocks (a large-granularity memory emulated), with the
 fetch amplification the kernel counts; prefill TFLOP/s at M = 2048 (the
 library's plan, and tiles 256x256x64, 256x128x64, 128x128x64 pinned; bf16 out); a Qwen-3-30B-A3B-shaped MoE
 layer (64 tokens, top-8 of 128 experts, plus the attention projections);
-the TileLens-HW view load of an 8192 x 8192 box (2-D and 4-D views);
+the TileLens-HW view load of an 8192 x 8192 box (2-D and 4-D views); the
+gate+up GEMM on an emulated fixed-latency memory against Eq. 6;
 read amplification of the decode tile and of the paper's 128 x 256 tile;
 repack GB/s; the decode kernel's roofline; the CPU oracle on a bounded sample.
 
@@ -313,6 +314,48 @@ def moe_layer(ctx, steps, warmup):
     return res
 
 
+def lgms_sweep(ctx, weights):
+    """Eq. 6 on an emulated fixed-latency memory: the gate+up decode GEMM at
+    M = 8 through tl_gemm_lgms for read latencies of 2-20 us and 1, 2, 4 or 8
+    K steps in flight per wave; beside each measurement, Little's law for the
+    bytes the resident workgroups keep in flight, and the Eq. 6 degree that
+    saturates the no-latency rate B."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    _, N, K, Wt = weights[2]
+    M = DECODE_M
+    A = ctx.to_dev(synth.normal_bf16((M, K), seed=synth.llama_decode_act_seed(2, M)))
+    C = torch.empty((M, N), dtype=torch.float32, device=ctx.dev)
+    d = tl.layout(G=G, block_rows=BR)
+    byts = launch_bytes(M, N, K)
+    n_tiles, split = N // 32, 1                  # 1792 tiles: no K split (the library's rule)
+    step_bytes = 32 * 64 * 2                    # one wave's K step of its 32-row tile
+    k_iters = K // 64 // 4                      # K iterations of a workgroup (4 waves)
+
+    def timed(lat, steps, reps=3):
+        tl.tl_gemm_lgms(A, Wt, C, M, N, K, d, lat, steps)
+        ev = ctx.event_pairs(1)[0]
+        ev[0].record(ctx.stream)
+        for _ in range(reps):
+            tl.tl_gemm_lgms(A, Wt, C, M, N, K, d, lat, steps)
+        ev[1].record(ctx.stream)
+        torch.cuda.synchronize()
+        return byts / (ev[0].elapsed_time(ev[1]) / reps * 1e-3) / 1e9
+
+    B = timed(0, 4)
+    rows = []
+    for lat_us in (2, 5, 10, 20):
+        for steps in (1, 2, 4, 8):
+            resident = min(n_tiles * split, 256 * tl.tl_lgms_occupancy(steps))
+            p_iter = resident * 4 * step_bytes          # bytes one K iteration of all resident workgroups demands
+            little = min(B, resident * 4 * steps * step_bytes / (lat_us * 1e-6) / 1e9)
+            rows.append({"latency_us": lat_us, "steps_in_flight": steps, "GB/s": round(timed(lat_us * 1000, steps), 1),
+                         "littles_law_GB/s": round(little, 1), "resident_workgroups": resident,
+                         "eq6_degree": tl.tl_prefetch_degree(B * 1e9, lat_us * 1e-6, p_iter, k_iters)})
+    res = {"no_latency_GB/s": round(B, 1), "shape": "gate_up [57344, 8192], M=8", "rows": rows}
+    log(f"lgms emulation: {res}")
+    return res
+
+
 def view_load(ctx, weights):
     """tl_view_load of an 8192 x 8192 bf16 box of the down weight (K x N
     order: 8192 contiguous elements x 8192 columns), as a 2-D view and as an
@@ -479,6 +522,7 @@ def main():
         extras["moe_qwen3_30b_a3b_64_tokens"] = moe_layer(ctx, args.steps, args.warmup)
         torch.cuda.empty_cache()
         extras["view_load"] = view_load(ctx, weights)
+        extras["lgms_emulation"] = lgms_sweep(ctx, weights)
 
     # ---------------- read amplification ----------------
     plan = tl.tl_gemm_plan(DECODE_M, 8192, 8192, desc, tl.TL_FETCH_BLOCK)

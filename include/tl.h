@@ -231,6 +231,47 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
 int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
                 int32_t tile_k, const tl_layout_desc* layout, int64_t G, tl_amp* out);
 
+/*
+ * tl_prefetch_degree -- host only, Eq. 6 (Section 5.3): the prefetch degree
+ * that keeps a memory of the given bandwidth busy over the given read
+ * latency when every K iteration of the resident workgroups demands
+ * bytes_per_iteration bytes:
+ *     d = min(floor(collision_factor * bandwidth * latency / bytes_per_iteration), k_iterations)
+ * (requests of equal size make the request form and this byte form equal;
+ * the paper uses collision_factor 2 for NAND plane collisions, 1 is the plain
+ * equation).  Units: any consistent pair, e.g. bytes/s and s.
+ * Errors: TL_EINVAL for NULL degree, bandwidth <= 0, latency < 0,
+ * bytes_per_iteration <= 0, k_iterations < 0 or collision_factor <= 0.
+ */
+int tl_prefetch_degree(double bandwidth, double latency, double bytes_per_iteration, int64_t k_iterations,
+                       double collision_factor, int64_t* degree);
+
+/*
+ * tl_gemm_lgms -- the decode GEMM of tl_gemm (M <= 16, tile-major weight,
+ * 32-row compute tiles, 4-wave workgroups interleaved along K, K split across
+ * workgroups until there are about 1024 of them unless layout->split_k says
+ * otherwise) on an emulated large-granularity memory whose every read
+ * completes no earlier than latency_ns after it is issued (Section 5.3's
+ * microsecond-scale reads, imposed on HBM by waiting on the GPU's constant
+ * clock).  Each wave keeps steps_in_flight (1, 2, 4 or 8) K steps of 64 of its
+ * weight tile's loads outstanding: the prefetch degree d = steps_in_flight - 1
+ * of Eq. 6 at workgroup granularity.  Same results as tl_gemm up to fp32
+ * summation order.
+ * Errors: TL_EINVAL for steps_in_flight not in {1, 2, 4, 8}, latency_ns
+ * outside [0, 1e9], and what tl_gemm rejects with TL_EINVAL;
+ * TL_EUNSUPPORTED for M > 16, a layout other than TL_LAYOUT_TILE,
+ * block_rows > 32, or what tl_gemm rejects with it; TL_EHIP, TL_ENOMEM as
+ * tl_gemm.
+ */
+int tl_gemm_lgms(const void* A, const void* W_tm, void* C, int64_t M, int64_t N, int64_t K,
+                 const tl_layout_desc* layout, int64_t latency_ns, int32_t steps_in_flight, void* stream);
+
+/* tl_lgms_occupancy -- resident tl_gemm_lgms workgroups per CU for a given
+ * steps_in_flight (registers grow with it), to size Eq. 6's per-iteration
+ * demand.  Errors: TL_EINVAL for a NULL pointer or a steps_in_flight not in
+ * {1, 2, 4, 8}; TL_EHIP if the occupancy query fails. */
+int tl_lgms_occupancy(int32_t steps_in_flight, int32_t* workgroups_per_cu);
+
 /* A multi-dimensional view of a weight, as a TMA descriptor would give it
  * (Section 4.3): the K x N weight (K contiguous: W[N][K] row-major, the
  * paper's column-major K x N) seen as a tensor of rank 'rank' whose

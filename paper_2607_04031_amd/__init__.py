@@ -36,7 +36,8 @@ TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
 EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
-            "tl_view_offsets", "tl_view_load", "tl_fetch_counter_read", "tl_release", "tl_strerror")
+            "tl_view_offsets", "tl_view_load", "tl_prefetch_degree", "tl_gemm_lgms", "tl_lgms_occupancy",
+            "tl_fetch_counter_read", "tl_release", "tl_strerror")
 TL_VIEW_MAX_RANK = 5
 
 
@@ -125,6 +126,13 @@ def load_library():
     lib.tl_gemm_grouped.restype = ctypes.c_int
     lib.tl_gemm_grouped.argtypes = [p, i64, p, p, i32, i64, i64, p, i64, p, i64, i64,
                                     ctypes.POINTER(LayoutDesc), i32, p]
+    lib.tl_prefetch_degree.restype = ctypes.c_int
+    lib.tl_prefetch_degree.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, i64, ctypes.c_double,
+                                       ctypes.POINTER(i64)]
+    lib.tl_gemm_lgms.restype = ctypes.c_int
+    lib.tl_gemm_lgms.argtypes = [p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i64, i32, p]
+    lib.tl_lgms_occupancy.restype = ctypes.c_int
+    lib.tl_lgms_occupancy.argtypes = [i32, ctypes.POINTER(i32)]
     lib.tl_view_offsets.restype = ctypes.c_int
     lib.tl_view_offsets.argtypes = [ctypes.POINTER(View), i64, i64, i32, i64, i32, p, i64, ctypes.POINTER(i64)]
     lib.tl_view_load.restype = ctypes.c_int
@@ -215,6 +223,26 @@ def tl_gemm_grouped(A, a_rows, token_ids, group_offsets, num_groups, total_rows,
     _check(load_library().tl_gemm_grouped(_ptr(A), a_rows, _ptr(token_ids), _ptr(group_offsets), num_groups,
                                           total_rows, max_group_rows, _ptr(W), group_stride, _ptr(C), N, K,
                                           ctypes.byref(d), fetch_mode, _stream(stream)), "tl_gemm_grouped")
+
+
+def tl_prefetch_degree(bandwidth, latency, bytes_per_iteration, k_iterations, collision_factor=1.0) -> int:
+    d = ctypes.c_int64(0)
+    _check(load_library().tl_prefetch_degree(float(bandwidth), float(latency), float(bytes_per_iteration),
+                                             int(k_iterations), float(collision_factor), ctypes.byref(d)),
+           "tl_prefetch_degree")
+    return d.value
+
+
+def tl_gemm_lgms(A, W, C, M, N, K, layout, latency_ns, steps_in_flight, stream=None):
+    d = _desc(layout)
+    _check(load_library().tl_gemm_lgms(_ptr(A), _ptr(W), _ptr(C), M, N, K, ctypes.byref(d), int(latency_ns),
+                                       int(steps_in_flight), _stream(stream)), "tl_gemm_lgms")
+
+
+def tl_lgms_occupancy(steps_in_flight) -> int:
+    n = ctypes.c_int32(0)
+    _check(load_library().tl_lgms_occupancy(int(steps_in_flight), ctypes.byref(n)), "tl_lgms_occupancy")
+    return n.value
 
 
 def tl_view_offsets(v: View, K, N, elem_bytes, G, block_rows):

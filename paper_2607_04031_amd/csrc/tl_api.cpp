@@ -1,6 +1,7 @@
 // libtl C ABI: argument validation, kernel planning, per-(device, stream)
 // library state, dispatch.  Nothing is enqueued unless every check passes.
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -409,6 +410,79 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, con
     d.a_rows = a_rows;
     d.total_rows = total_rows;
     return launch_decode(d, s) == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+int tl_prefetch_degree(double bandwidth, double latency, double bytes_per_iteration, int64_t k_iterations,
+                       double collision_factor, int64_t* degree) {
+    if (!degree || !(bandwidth > 0) || !(latency >= 0) || !(bytes_per_iteration > 0) || k_iterations < 0 ||
+        !(collision_factor > 0))
+        return TL_EINVAL;
+    const double first = std::floor(collision_factor * bandwidth * latency / bytes_per_iteration);   // Eq. 6
+    *degree = first < double(k_iterations) ? int64_t(first) : k_iterations;
+    return TL_OK;
+}
+
+int tl_lgms_occupancy(int32_t steps_in_flight, int32_t* workgroups_per_cu) {
+    if (!workgroups_per_cu) return TL_EINVAL;
+    if (steps_in_flight != 1 && steps_in_flight != 2 && steps_in_flight != 4 && steps_in_flight != 8) return TL_EINVAL;
+    const int n = lgms_ctas_per_cu(steps_in_flight);
+    if (n < 0) return TL_EHIP;
+    *workgroups_per_cu = n;
+    return TL_OK;
+}
+
+int tl_gemm_lgms(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout,
+                 int64_t latency_ns, int32_t steps_in_flight, void* stream) {
+    if (!layout) return TL_EINVAL;
+    if (steps_in_flight != 1 && steps_in_flight != 2 && steps_in_flight != 4 && steps_in_flight != 8) return TL_EINVAL;
+    if (latency_ns < 0 || latency_ns > 1000000000) return TL_EINVAL;
+    if (layout->kind != TL_LAYOUT_TILE) return TL_EUNSUPPORTED;
+    tl_layout_desc d1 = *layout;
+    d1.tile_n = 32;
+    d1.tile_m = 0;
+    d1.split_k = layout->split_k;
+    Plan p;
+    int rc = plan_gemm(M, N, K, &d1, TL_FETCH_BLOCK, &p);
+    if (rc != TL_OK) return rc;
+    if (M > 16 || p.pub.kernel != 1) return TL_EUNSUPPORTED;
+    if (!A || !W || !C || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
+    const int64_t c_bytes = M * N * (p.out_bf16 ? 2 : 4);
+    if (overlap(C, c_bytes, A, M * K * 2) || overlap(C, c_bytes, W, N * K * 2)) return TL_EINVAL;
+    // 4-wave workgroups: split K until there are about 1024 of them
+    const int64_t n_tiles = N / 32, units = K / p.k_unit;
+    int64_t S = layout->split_k;
+    if (S == 0) {
+        S = (kTargetWorkgroups + n_tiles - 1) / n_tiles;
+        S = std::max<int64_t>(1, std::min<int64_t>({S, units / std::max<int64_t>(1, 1024 / p.k_unit), kMaxSplitK}));
+    }
+    if (S < 1 || S > units || S > kMaxSplitK) return TL_EUNSUPPORTED;
+    int dev = 0, khz = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return TL_EHIP;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0) return TL_EHIP;
+    const int64_t ticks = (latency_ns * int64_t(khz) + 999999) / 1000000;
+    hipStream_t s = (hipStream_t)stream;
+    StreamState* st = nullptr;
+    rc = get_state(s, size_t(S > 1 ? S * M * N * 4 : 0), &st);
+    if (rc != TL_OK) return rc;
+    DecodeLaunch dl;
+    dl.A = static_cast<const uint16_t*>(A);
+    dl.W = static_cast<const uint8_t*>(W);
+    dl.C = C;
+    dl.ws = st->ws;
+    dl.fetch = nullptr;
+    dl.M = M;
+    dl.N = N;
+    dl.K = K;
+    dl.L = p.L;
+    dl.tile_n = 32;
+    dl.m_tiles16 = 1;
+    dl.waves = 4;
+    dl.split_k = int(S);
+    dl.k_unit = p.k_unit;
+    dl.out_bf16 = p.out_bf16;
+    dl.block_fetch = false;
+    dl.fetch_G = 0;
+    return launch_lgms(dl, ticks, steps_in_flight, s) == hipSuccess ? TL_OK : TL_EHIP;
 }
 
 int tl_view_offsets(const tl_view* view, int64_t K, int64_t N, int32_t elem_bytes, int64_t G, int32_t block_rows,

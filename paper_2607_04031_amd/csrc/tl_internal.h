@@ -68,6 +68,14 @@ struct DecodeLaunch {
 };
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream);
+// the fixed-order split-K reduce that follows a decode launch with split_k > 1
+// (passes 'e' through when it is an error or split_k is 1)
+hipError_t launch_splitk_reduce(const DecodeLaunch& d, hipError_t e, hipStream_t stream);
+// large-granularity-memory emulation (decode, M <= 16, tile_n 32, 4 waves):
+// every read completes no earlier than latency_ticks wall-clock ticks after
+// issue; each wave keeps steps_in_flight (1, 2, 4 or 8) K steps in flight
+hipError_t launch_lgms(const DecodeLaunch& d, int64_t latency_ticks, int steps_in_flight, hipStream_t stream);
+int lgms_ctas_per_cu(int steps_in_flight);   // resident workgroups per CU, -1 on a HIP error
 
 struct PrefillLaunch {
     const uint16_t* A;
