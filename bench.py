@@ -17,7 +17,8 @@ read in whole 4 KB blocks (a large-granularity memory emulated), with the
 fetch amplification the kernel counts; prefill TFLOP/s at M = 2048 (the
 library's plan, and tiles 256x256x64, 256x128x64, 128x128x64 pinned; bf16 out); a Qwen-3-30B-A3B-shaped MoE
 layer (64 tokens, top-8 of 128 experts, plus the attention projections);
-the TileLens-HW view load of an 8192 x 8192 box (2-D and 4-D views); the
+the layer with FP8 weights (64 x 64 memory tiles); the TileLens-HW view load
+of an 8192 x 8192 box (2-D and 4-D views); the
 gate+up GEMM on an emulated fixed-latency memory against Eq. 6;
 read amplification of the decode tile and of the paper's 128 x 256 tile;
 repack GB/s; the decode kernel's roofline; the CPU oracle on a bounded sample.
@@ -314,6 +315,46 @@ def moe_layer(ctx, steps, warmup):
     return res
 
 
+def fp8_layer(ctx, steps, warmup):
+    """The Llama-70B-shaped decode layer at M = 8 with FP8 (E4M3) weights in
+    64 x 64 memory tiles (4 KB), per-channel scales, bf16 activations
+    (tl_gemm_w8): half the weight bytes of the bf16 layer."""
+    tl, torch, synth, np = ctx.tl, ctx.torch, ctx.synth, ctx.np
+    d8 = tl.layout(elem_bytes=1, G=4096, block_rows=64)
+    calls, lb = [], []
+    for i, (name, N, K) in enumerate(synth.LLAMA70B):
+        q, sc = synth.fp8_weights((N, K), seed=synth.llama_weight_seed(i))
+        W = torch.from_numpy(q).to(ctx.dev)
+        Wt = torch.empty_like(W)
+        tl.tl_repack(W, Wt, N, K, 1, 4096, 64)
+        del W
+        A = ctx.to_dev(synth.normal_bf16((DECODE_M, K), seed=synth.llama_decode_act_seed(i, DECODE_M)))
+        C = torch.empty((DECODE_M, N), dtype=torch.float32, device=ctx.dev)
+        calls.append((name, A, Wt, torch.from_numpy(sc).to(ctx.dev), C, N, K))
+        lb.append(N * K + 2 * DECODE_M * K + 4 * DECODE_M * N)
+
+    def step(ev=None):
+        for j, (_, A, Wt, sc, C, N, K) in enumerate(calls):
+            if ev is not None:
+                ev[j][0].record(ctx.stream)
+            tl.tl_gemm_w8(A, Wt, sc, C, DECODE_M, N, K, d8, tl.TL_FETCH_BLOCK)
+            if ev is not None:
+                ev[j][1].record(ctx.stream)
+
+    for _ in range(warmup):
+        step()
+    wall = wall_time(ctx, step, steps)
+    evs = [ctx.event_pairs(len(calls)) for _ in range(10)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    per = {c[0]: round(sum(e[j][0].elapsed_time(e[j][1]) for e in evs) / len(evs) * 1e3, 2) for j, c in enumerate(calls)}
+    res = {"GB/s": round(sum(lb) * steps / wall / 1e9, 1), "ms_per_layer": round(wall * 1e3 / steps, 4),
+           "weight_bytes": sum(N * K for (_, _, _, _, _, N, K) in calls), "per_shape_us": per}
+    log(f"fp8 decode layer: {res}")
+    return res
+
+
 def lgms_sweep(ctx, weights):
     """Eq. 6 on an emulated fixed-latency memory: the gate+up decode GEMM at
     M = 8 through tl_gemm_lgms for read latencies of 2-20 us and 1, 2, 4 or 8
@@ -520,6 +561,8 @@ def main():
         del weights_rm
         torch.cuda.empty_cache()
         extras["moe_qwen3_30b_a3b_64_tokens"] = moe_layer(ctx, args.steps, args.warmup)
+        torch.cuda.empty_cache()
+        extras["fp8_decode_layer_M8"] = fp8_layer(ctx, args.steps, args.warmup)
         torch.cuda.empty_cache()
         extras["view_load"] = view_load(ctx, weights)
         extras["lgms_emulation"] = lgms_sweep(ctx, weights)

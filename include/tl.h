@@ -71,7 +71,7 @@ enum {
  * one library binary serves every memory-tile shape (Sections 1 and 4.3). */
 typedef struct tl_layout_desc {
     int32_t kind;        /* tl_layout_kind */
-    int32_t elem_bytes;  /* element size s in bytes; tl_gemm needs 2 (bf16) */
+    int32_t elem_bytes;  /* element size s in bytes; tl_gemm: 2 (bf16) or 1 (FP8 E4M3) */
     int64_t G;           /* TL_LAYOUT_TILE: memory-tile size in bytes (power of
                             two).  *_ROW with TL_FETCH_BLOCK: the emulated fetch
                             block.  Otherwise ignored. */
@@ -155,18 +155,37 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  *      paid as real HBM traffic, and tallied by TL_FETCH_COUNT.
  * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound); larger M runs the
  * prefill kernel (bf16 MFMA tiles 256x256x64, 256x128x64 or 128x128x64,
- * MFMA-bound).
+ * MFMA-bound).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
+ * byte per element, e.g. 64 x 64 memory tiles of 4 KB, Section 3.1): decode
+ * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
+ * per-channel scales).
  * Errors: TL_EINVAL for M, N, K < 1, NULL or misaligned pointers, a bad
  * descriptor (see tl_repack) or N % block_rows / K % block_cols != 0 for
  * TL_LAYOUT_TILE, or a bad G for NK_ROW with TL_FETCH_BLOCK;
- * TL_EUNSUPPORTED for elem_bytes != 2, K % 64 != 0, N % 32 != 0,
- * block_cols < 8, a combination of layout, fetch mode and tile that no kernel
- * implements (NK_ROW with BLOCK above 64 rows), or TL_LAYOUT_KN_ROW.
+ * TL_EUNSUPPORTED for elem_bytes other than 1 or 2, K % 64 != 0,
+ * N % 32 != 0, block_cols * elem_bytes < 16, a combination of layout, fetch
+ * mode and tile that no kernel implements (NK_ROW with BLOCK above 64 rows or
+ * with FP8, FP8 above 64 rows), or TL_LAYOUT_KN_ROW.
  * TL_ENOMEM if the split-K workspace cannot be allocated; TL_EHIP if the
  * launch fails.
  */
 int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
             const tl_layout_desc* layout, int32_t fetch_mode, void* stream);
+
+/*
+ * tl_gemm_w8 -- weight-only 8-bit decode: C[m][n] = scales[n] *
+ * sum_k A[m][k] * W[n][k], with W an FP8 weight (OCP E4M3: sign, 4 exponent
+ * bits with bias 7, 3 mantissa bits, no infinities, S.1111.111 = NaN) in the
+ * layout 'layout' describes (layout->elem_bytes must be 1; tile-major with
+ * e.g. 64 x 64 memory tiles of 4 KB, or TL_LAYOUT_NK_ROW), A bf16.  scales:
+ * device fp32 [N] or NULL (all 1).  Each weight byte is converted exactly to
+ * bf16 and the products accumulate in fp32 as in tl_gemm.  M <= 64.
+ * Errors: TL_EINVAL for layout->elem_bytes != 1, misaligned scales, scales
+ * overlapping C, and what tl_gemm rejects with TL_EINVAL; TL_EUNSUPPORTED as
+ * tl_gemm.
+ */
+int tl_gemm_w8(const void* A, const void* W_fp8, const float* scales, void* C, int64_t M, int64_t N,
+               int64_t K, const tl_layout_desc* layout, int32_t fetch_mode, void* stream);
 
 /* tl_gemm_plan -- host only: fill *out with what tl_gemm would launch for the
  * same arguments (no device work).  Same error rules as tl_gemm. */

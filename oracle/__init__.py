@@ -18,6 +18,9 @@ What each function follows (TileLens, arxiv 2607.04031):
   view_offsets   Section 4.3: tile-major byte offsets of the elements of a
                  box of a multi-dimensional view (linear index -> (i, j) ->
                  Eq. 2), in the order a TMA load visits them
+  fp8_e4m3 / gemm_w8_f64  the FP8 weights the paper's 64 x 64 memory tile
+                 holds (Section 3.1): OCP E4M3 decoded by its definition, and
+                 the GEMM over them with per-output-channel scales, fp64
   round_bf16     round-to-nearest-even to 8 significant bits
   read_amp       Sections 1, 2.5 and 6.4 (requests per compute tile at
                  granularity G; weights only, Section 5.1)
@@ -75,6 +78,10 @@ def _load():
     lib.orc_round_bf16.argtypes = [ctypes.c_double]
     lib.orc_round_bf16_array.restype = None
     lib.orc_round_bf16_array.argtypes = [p, p, i64]
+    lib.orc_fp8_e4m3.restype = ctypes.c_double
+    lib.orc_fp8_e4m3.argtypes = [ctypes.c_uint8]
+    lib.orc_gemm_w8_f64.restype = None
+    lib.orc_gemm_w8_f64.argtypes = [p, p, p, p, i64, i64, i64]
     lib.orc_view_offsets.restype = i64
     lib.orc_view_offsets.argtypes = [ctypes.c_int, p, p, p, i64, i64, i64, i64, p]
     lib.orc_read_amp.restype = ctypes.c_int
@@ -164,6 +171,23 @@ def grouped_gemm_f64(A_bf16: np.ndarray, token_ids, offsets, W_list) -> np.ndarr
             continue
         rows = np.arange(r0, r1) if token_ids is None else np.asarray(token_ids[r0:r1], dtype=np.int64)
         Y[r0:r1] = gemm_f64(A_bf16[rows], W)
+    return Y
+
+
+def fp8_e4m3(v: int) -> float:
+    return _load().orc_fp8_e4m3(int(v))
+
+
+def gemm_w8_f64(A_bf16: np.ndarray, W_fp8: np.ndarray, scales=None) -> np.ndarray:
+    """A: uint16 bf16 bits [M,K]; W_fp8: uint8 E4M3 bytes [N,K] row-major; scales: [N] or None -> fp64 [M,N]."""
+    A = np.ascontiguousarray(A_bf16, dtype=np.uint16)
+    W = np.ascontiguousarray(W_fp8, dtype=np.uint8)
+    M, K = A.shape
+    N, K2 = W.shape
+    assert K == K2
+    sc = None if scales is None else np.ascontiguousarray(scales, dtype=np.float64)
+    Y = np.empty((M, N), dtype=np.float64)
+    _load().orc_gemm_w8_f64(_ptr(A), _ptr(W), None if sc is None else _ptr(sc), _ptr(Y), M, N, K)
     return Y
 
 

@@ -137,6 +137,34 @@ void orc_gemm_f64(const uint16_t* A, const uint16_t* W, double* Y,
 
 /* Same definition on a list of output coordinates only (for spot checks of
  * full-size results): y[i] = sum_k A[m_i][k] * W[n_i][k]. */
+/* OCP FP8 E4M3 byte -> value: sign bit, 4 exponent bits (bias 7), 3
+ * mantissa bits; exponent 0 is subnormal (m / 8 * 2^-6); exponent 15 with
+ * mantissa 7 is NaN; there are no infinities. */
+double orc_fp8_e4m3(uint8_t v) {
+    int sign = v / 128, e = (v / 8) % 16, m = v % 8;
+    double mag;
+    if (e == 15 && m == 7) return NAN;
+    if (e == 0) mag = ldexp((double)m / 8.0, -6);
+    else mag = ldexp(1.0 + (double)m / 8.0, e - 7);
+    return sign ? -mag : mag;
+}
+
+/* Weight-only 8-bit GEMM: Y[m][n] = scale[n] * sum_k A[m][k] * W8[n][k],
+ * A bf16 row-major [M][K], W8 FP8 E4M3 row-major [N][K], scale NULL = 1;
+ * fp64, k ascending. */
+void orc_gemm_w8_f64(const uint16_t* A, const uint8_t* W8, const double* scale, double* Y,
+                     int64_t M, int64_t N, int64_t K) {
+    #pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t m = 0; m < M; ++m) {
+            double acc = 0.0;
+            for (int64_t k = 0; k < K; ++k)
+                acc += orc_bf16_to_f64(A[m * K + k]) * orc_fp8_e4m3(W8[n * K + k]);
+            Y[m * N + n] = scale ? acc * scale[n] : acc;
+        }
+    }
+}
+
 void orc_gemm_f64_points(const uint16_t* A, const uint16_t* W,
                          const int64_t* ms, const int64_t* ns, double* y,
                          int64_t count, int64_t K) {

@@ -35,7 +35,7 @@ TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE = 0, 1, 2
 TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
-EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
+EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
             "tl_view_offsets", "tl_view_load", "tl_prefetch_degree", "tl_gemm_lgms", "tl_lgms_occupancy",
             "tl_fetch_counter_read", "tl_release", "tl_strerror")
 TL_VIEW_MAX_RANK = 5
@@ -121,6 +121,8 @@ def load_library():
     lib.tl_unpack.argtypes = [p, p, i64, i64, i32, i64, i32, p]
     lib.tl_gemm.restype = ctypes.c_int
     lib.tl_gemm.argtypes = [p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, p]
+    lib.tl_gemm_w8.restype = ctypes.c_int
+    lib.tl_gemm_w8.argtypes = [p, p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, p]
     lib.tl_gemm_plan.restype = ctypes.c_int
     lib.tl_gemm_plan.argtypes = [i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, ctypes.POINTER(Plan)]
     lib.tl_gemm_grouped.restype = ctypes.c_int
@@ -206,6 +208,13 @@ def tl_gemm(A, W, C, M, N, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):
     d = _desc(layout)
     _check(load_library().tl_gemm(_ptr(A), _ptr(W), _ptr(C), M, N, K, ctypes.byref(d), fetch_mode,
                                   _stream(stream)), "tl_gemm")
+
+
+def tl_gemm_w8(A, W_fp8, scales, C, M, N, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):
+    """scales may be None (all 1)."""
+    d = _desc(layout)
+    _check(load_library().tl_gemm_w8(_ptr(A), _ptr(W_fp8), _ptr(scales), _ptr(C), M, N, K, ctypes.byref(d),
+                                     fetch_mode, _stream(stream)), "tl_gemm_w8")
 
 
 def tl_gemm_plan(M, N, K, layout, fetch_mode=TL_FETCH_BLOCK) -> dict:

@@ -123,6 +123,7 @@ struct Plan {
     bool block_row = false;      // block-granular emulation on a row-major weight
     int64_t fetch_G = 0;
     int64_t n_main = 0;          // prefill: columns covered by the main tiles (rest: 128 x 128)
+    bool fp8 = false;            // 1-byte (OCP E4M3) weight, decode kernel
 };
 
 constexpr int kDecodeMaxM = 64;
@@ -139,22 +140,24 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
     if (d->tile_m < 0 || d->tile_n < 0 || d->tile_k < 0 || d->split_k < 0) return TL_EINVAL;
     if (d->kind != TL_LAYOUT_NK_ROW && d->kind != TL_LAYOUT_KN_ROW && d->kind != TL_LAYOUT_TILE)
         return TL_EINVAL;
-    if (d->elem_bytes != 2) return d->elem_bytes < 1 ? TL_EINVAL : TL_EUNSUPPORTED;
+    if (d->elem_bytes != 2 && d->elem_bytes != 1) return d->elem_bytes < 1 ? TL_EINVAL : TL_EUNSUPPORTED;
+    const int s = d->elem_bytes;
     if (M > (int64_t(1) << 31) || N > (int64_t(1) << 31) || K > (int64_t(1) << 31)) return TL_EINVAL;
 
     Plan p;
     std::memset(&p.pub, 0, sizeof p.pub);
     p.out_bf16 = d->out_dtype == TL_OUT_BF16;
     p.count = (fetch_mode & TL_FETCH_COUNT) != 0;
+    p.fp8 = s == 1;
     const bool block = (fetch_mode & TL_FETCH_BLOCK) != 0;
 
     if (d->kind == TL_LAYOUT_TILE) {
-        if (make_tile_layout(2, d->G, d->block_rows, &p.L) != TL_OK) return TL_EINVAL;
+        if (make_tile_layout(s, d->G, d->block_rows, &p.L) != TL_OK) return TL_EINVAL;
         if (N % p.L.br || K % p.L.bc) return TL_EINVAL;
-        if (p.L.bc < 8) return TL_EUNSUPPORTED;
+        if (p.L.bc * s < 16) return TL_EUNSUPPORTED;   // a 16-byte lane load stays in one memory-tile row
     } else if (d->kind == TL_LAYOUT_NK_ROW) {
         p.L.kind = TL_LAYOUT_NK_ROW;
-        if (block) {
+        if (block && !p.fp8) {
             // whole G-byte blocks of the row-major weight; G >= 128 keeps each
             // 128-byte row segment of a K step inside one block
             if (!is_pow2(d->G) || d->G < 128 || d->G > (int64_t(1) << 30)) return TL_EINVAL;
@@ -170,6 +173,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
     p.k_unit = tile ? std::max<int64_t>(64, p.L.bc) : 64;
 
     if (p.block_row && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;   // decode kernel only
+    if (p.fp8 && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;        // FP8: decode kernel only
     if (M <= kDecodeMaxM && d->tile_m <= 64) {
         p.pub.kernel = 1;
         p.m_tiles16 = int((M + 15) / 16);
@@ -272,7 +276,7 @@ int plan_grouped(int64_t max_group_rows, int64_t N, int64_t K, const tl_layout_d
     d1.split_k = 1;
     int rc = plan_gemm(std::min<int64_t>(max_group_rows, kDecodeMaxM), N, K, &d1, fetch_mode, P);
     if (rc != TL_OK) return rc;
-    if (P->pub.kernel != 1 || P->block_row) return TL_EUNSUPPORTED;
+    if (P->pub.kernel != 1 || P->block_row || P->fp8) return TL_EUNSUPPORTED;
     P->waves = 4;
     P->pub.waves = 4;
     P->pub.workspace_bytes = 0;
@@ -306,14 +310,17 @@ int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout, 
     return TL_OK;
 }
 
-int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
-            const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
+static int gemm_impl(const void* A, const void* W, const float* scales, void* C, int64_t M, int64_t N, int64_t K,
+                     const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
     Plan p;
     int rc = plan_gemm(M, N, K, layout, fetch_mode, &p);
     if (rc != TL_OK) return rc;
     if (!A || !W || !C || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
+    if (scales && (reinterpret_cast<uintptr_t>(scales) & 3u)) return TL_EINVAL;
     const int64_t c_bytes = M * N * (p.out_bf16 ? 2 : 4);
-    if (overlap(C, c_bytes, A, M * K * 2) || overlap(C, c_bytes, W, N * K * 2)) return TL_EINVAL;
+    const int64_t w_bytes = N * K * layout->elem_bytes;
+    if (overlap(C, c_bytes, A, M * K * 2) || overlap(C, c_bytes, W, w_bytes)) return TL_EINVAL;
+    if (scales && overlap(C, c_bytes, scales, N * 4)) return TL_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
     StreamState* st = nullptr;
@@ -340,6 +347,8 @@ int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t
         d.out_bf16 = p.out_bf16;
         d.block_fetch = p.block_row;
         d.fetch_G = p.fetch_G;
+        d.fp8 = p.fp8;
+        d.scales = scales;
         e = launch_decode(d, s);
     } else {
         PrefillLaunch q;
@@ -412,6 +421,18 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, con
     return launch_decode(d, s) == hipSuccess ? TL_OK : TL_EHIP;
 }
 
+int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
+            const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
+    return gemm_impl(A, W, nullptr, C, M, N, K, layout, fetch_mode, stream);
+}
+
+int tl_gemm_w8(const void* A, const void* W_fp8, const float* scales, void* C, int64_t M, int64_t N, int64_t K,
+               const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
+    if (!layout) return TL_EINVAL;
+    if (layout->elem_bytes != 1) return TL_EINVAL;
+    return gemm_impl(A, W_fp8, scales, C, M, N, K, layout, fetch_mode, stream);
+}
+
 int tl_prefetch_degree(double bandwidth, double latency, double bytes_per_iteration, int64_t k_iterations,
                        double collision_factor, int64_t* degree) {
     if (!degree || !(bandwidth > 0) || !(latency >= 0) || !(bytes_per_iteration > 0) || k_iterations < 0 ||
@@ -436,7 +457,7 @@ int tl_gemm_lgms(const void* A, const void* W, void* C, int64_t M, int64_t N, in
     if (!layout) return TL_EINVAL;
     if (steps_in_flight != 1 && steps_in_flight != 2 && steps_in_flight != 4 && steps_in_flight != 8) return TL_EINVAL;
     if (latency_ns < 0 || latency_ns > 1000000000) return TL_EINVAL;
-    if (layout->kind != TL_LAYOUT_TILE) return TL_EUNSUPPORTED;
+    if (layout->kind != TL_LAYOUT_TILE || layout->elem_bytes != 2) return TL_EUNSUPPORTED;
     tl_layout_desc d1 = *layout;
     d1.tile_n = 32;
     d1.tile_m = 0;

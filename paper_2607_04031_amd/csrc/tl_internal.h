@@ -65,6 +65,9 @@ struct DecodeLaunch {
     int64_t group_stride = 0;
     int64_t a_rows = 0;
     int64_t total_rows = 0;
+    // FP8 (E4M3) weight, bf16 activations; optional per-output-channel scales [N]
+    bool fp8 = false;
+    const float* scales = nullptr;
 };
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream);

@@ -148,3 +148,26 @@ def moe_tables(routing: np.ndarray, E: int = QWEN_EXPERTS) -> tuple[np.ndarray, 
     offsets[1:] = np.cumsum([len(t) for t in tok])
     ids = np.concatenate(tok).astype(np.int32) if offsets[-1] else np.zeros(0, dtype=np.int32)
     return offsets, ids
+
+
+def quantize_e4m3(w: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """Per-output-channel FP8 (OCP E4M3) weights for a float32 [N, K] array:
+    scales[n] = max_k |w[n, k]| / 448 (448 = the largest E4M3 value) and the
+    bytes of w / scales rounded to nearest even by torch's float8_e4m3fn
+    conversion.  Returns (uint8 [N, K], float32 [N])."""
+    import torch
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    amax = np.abs(w).max(axis=1)
+    scales = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
+    q = torch.from_numpy(w / scales[:, None]).to(torch.float8_e4m3fn)
+    return q.view(torch.uint8).numpy().copy(), scales
+
+
+def fp8_weights(shape, seed: int, sigma: float = W_SIGMA) -> tuple[np.ndarray, np.ndarray]:
+    """FP8 weights of the normal_bf16 draw with the same seed (float32 draws,
+    before bf16 rounding), per-channel scaled."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal(size=shape, dtype=np.float32)
+    if sigma != 1.0:
+        x *= np.float32(sigma)
+    return quantize_e4m3(x)

@@ -134,6 +134,29 @@ def test_gemm_plan_decode_and_prefill_shapes():
     assert p["tile_m"] == 128
 
 
+def test_fp8_plans():
+    """FP8 (elem_bytes 1) weights: decode kernel only; 64 x 64 memory tiles
+    (G = 4096, block_rows = 64) give 64-row compute tiles; 16-byte lane loads
+    need block_cols >= 16; no prefill, grouped or emulated-latency path."""
+    fp8 = tl.layout(elem_bytes=1, G=4096, block_rows=64)
+    p = tl.tl_gemm_plan(8, 8192, 8192, fp8)
+    assert p["kernel"] == 1 and p["tile_n"] == 64 and p["tile_k"] == 64
+    assert tl.tl_read_amp(8, 8192, 8192, p["tile_m"], p["tile_n"], p["tile_k"], fp8, 4096)["amp"] == 1.0
+    for args, status in (((128, 8192, 8192, fp8), tl.TL_EUNSUPPORTED),
+                         ((8, 8192, 8192, tl.layout(elem_bytes=1, G=512, block_rows=64)), tl.TL_EUNSUPPORTED),
+                         ((8, 8192, 8192, tl.layout(elem_bytes=3)), tl.TL_EUNSUPPORTED),
+                         ((8, 8192, 8192, tl.layout(elem_bytes=0)), tl.TL_EINVAL)):
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_plan(*args)
+        assert e.value.status == status, args
+    with pytest.raises(tl.TLError) as e:       # the W8 entry point needs an FP8 descriptor
+        tl.tl_gemm_w8(4096, 8192, None, 1 << 20, 8, 512, 512, tl.layout(), tl.TL_FETCH_BLOCK, stream=0)
+    assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm_lgms(4096, 8192, 1 << 20, 8, 512, 512, fp8, 1000, 2, stream=0)
+    assert e.value.status == tl.TL_EUNSUPPORTED
+
+
 def test_prefill_plan_column_split():
     """256 x 256 tiles whose count leaves the last round part-empty are kept on
     the widest column range with a whole number of rounds; the rest of the
@@ -158,7 +181,7 @@ def test_gemm_plan_error_codes():
         ((8, 64, 64, tl.layout(G=1000)), tl.TL_EINVAL),
         ((8, 48, 64, d), tl.TL_EINVAL),                      # N % br
         ((8, 64, 96, d), tl.TL_EINVAL),                      # K % bc
-        ((8, 64, 64, tl.layout(elem_bytes=1)), tl.TL_EUNSUPPORTED),
+        ((8, 64, 64, tl.layout(elem_bytes=4)), tl.TL_EUNSUPPORTED),    # only bf16 and FP8 weights
         ((8, 64, 64, tl.layout(kind=tl.TL_LAYOUT_KN_ROW)), tl.TL_EUNSUPPORTED),
         ((8, 64, 64, tl.layout(G=512, block_rows=64)), tl.TL_EUNSUPPORTED),   # bc = 4
         ((8, 64, 64, tl.layout(out_dtype=7)), tl.TL_EINVAL),

@@ -279,6 +279,34 @@ def test_moe_routing_tables():
         assert all(e in routing[t] for t in g.tolist())
 
 
+def test_fp8_e4m3_decode_against_torch_and_special_values():
+    """The oracle's E4M3 decode (written from the format) equals torch's
+    float8_e4m3fn for all 256 bytes; spot values of the format."""
+    import torch
+    vals = np.array([oracle.fp8_e4m3(v) for v in range(256)])
+    ref = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    assert np.array_equal(np.isnan(vals), np.isnan(ref))
+    assert np.array_equal(vals[~np.isnan(vals)], ref[~np.isnan(ref)])
+    assert oracle.fp8_e4m3(0x7E) == 448.0 and oracle.fp8_e4m3(0xFE) == -448.0      # largest
+    assert oracle.fp8_e4m3(0x08) == 2.0 ** -6 and oracle.fp8_e4m3(0x01) == 2.0 ** -9  # min normal, min subnormal
+    assert oracle.fp8_e4m3(0x38) == 1.0 and oracle.fp8_e4m3(0xC0) == -2.0
+    assert math.isnan(oracle.fp8_e4m3(0x7F)) and math.isnan(oracle.fp8_e4m3(0xFF))
+    assert oracle.fp8_e4m3(0x80) == 0.0 and math.copysign(1.0, oracle.fp8_e4m3(0x80)) == -1.0
+
+
+def test_gemm_w8_small_integers_equal_bf16_gemm():
+    """Integers in [-8, 8] are exact in E4M3 and bf16: the W8 GEMM of their
+    E4M3 bytes equals the bf16 GEMM of the same values, and scales multiply."""
+    import torch
+    A = synth.small_int_bf16((6, 200), seed=31)
+    Wi = np.random.default_rng(32).integers(-8, 9, size=(13, 200)).astype(np.float32)
+    W8 = torch.from_numpy(Wi).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    Wb = synth.f32_to_bf16_bits(Wi)
+    assert np.array_equal(oracle.gemm_w8_f64(A, W8), oracle.gemm_f64(A, Wb))
+    sc = np.linspace(0.5, 2.0, 13)
+    assert np.allclose(oracle.gemm_w8_f64(A, W8, sc), oracle.gemm_f64(A, Wb) * sc[None, :], rtol=1e-15, atol=0)
+
+
 def test_round_bf16_against_float32_bit_rounding():
     """The oracle's bf16 rounding of doubles equals numpy float32 -> bf16 RNE
     on values that are exactly float32, and breaks ties to even."""
