@@ -27,74 +27,10 @@
 #include <algorithm>
 #include <cstring>
 
-#include "tl_internal.h"
+#include "tl_decode_common.h"
 
 namespace tl {
 namespace {
-
-typedef short bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-
-struct DecodeParams {
-    const uint16_t* A;
-    const uint8_t* W;
-    void* C;
-    float* ws;
-    unsigned long long* fetch;
-    int M, N, K;
-    int split_k;
-    int steps_per_unit;      // 64-element steps per split unit
-    int units;               // K / k_unit
-    int64_t strip_bytes;     // br * K * 2 (TILE) -- bytes per strip of br rows
-    int log2_br, log2_bc, log2_G;
-    int bc_mask;
-    bool out_bf16;
-    int log2_fetch;          // block-granular emulation on a row-major weight: log2(G)
-    int64_t w_bytes;         // N * K * 2
-    // grouped (one launch over many weights, e.g. MoE experts)
-    const int* offsets;      // [groups + 1] output-row offsets of the groups
-    const int* token_ids;    // A row of each output row, or nullptr (identity)
-    int tiles_per_group;     // N / tile_n
-    int64_t group_stride;    // bytes between consecutive groups' weights
-    int a_rows;              // rows of A; token ids outside [0, a_rows) read zeros
-    int total_rows;          // rows of C; group offsets are clamped to [0, total_rows]
-    const float* scales;     // FP8 weights: per-output-channel scale [N], or nullptr (1)
-};
-
-__device__ inline uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))  // NaN stays NaN
-        return uint16_t((u >> 16) | 0x0040u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return uint16_t(u >> 16);
-}
-
-__device__ inline void store_out(void* C, int64_t idx, float v, bool out_bf16) {
-    if (out_bf16) static_cast<uint16_t*>(C)[idx] = f32_to_bf16_rne(v);
-    else static_cast<float*>(C)[idx] = v;
-}
-
-// Byte offset of the 8-element chunk starting at (row base, k) of the weight.
-template <bool TILE>
-__device__ inline int64_t w_koff(const DecodeParams& p, int k) {
-    if (TILE) return (int64_t(k >> p.log2_bc) << p.log2_G) + int64_t((k & p.bc_mask) << 1);
-    return int64_t(k) << 1;
-}
-
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-
-// Value of 'v' held by lane l ^ 8 (DPP row_ror:8 inside each 16-lane row).
-__device__ inline bf16x8 swap8(bf16x8 v) {
-    i32x4 x = __builtin_bit_cast(i32x4, v), y;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) y[i] = __builtin_amdgcn_update_dpp(0, x[i], 0x128, 0xf, 0xf, false);
-    return __builtin_bit_cast(bf16x8, y);
-}
-
-__device__ inline bf16x8 load_stream(const uint8_t* p) {
-    return __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(p));
-}
 
 // Weight loads.  Lane l = 16 g + q needs, per 16-row n-subtile and 64-wide K
 // step, the MFMA B operands  B0 = W[row q][k-chunk g], B1 = W[row q][chunk 4+g]
@@ -332,249 +268,6 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     }
 }
 
-// FP8 (OCP E4M3) weights, bf16 activations (weight-only 8-bit decode).  A
-// 64-element K step of one weight row is 64 bytes; lane l = 16 g + q loads the
-// 16 bytes k0 + 16 g .. + 15 of row q of each 16-row subtile, so with the
-// (64, 64) FP8 memory tile one instruction reads 16 consecutive memory-tile
-// rows = 1 KB contiguous, with no lane exchange.  The two 8-byte halves are
-// converted exactly to bf16 (every E4M3 value is a bf16 value) and feed two
-// MFMA 16x16x32: the first sums k0 + 16 g + 0..7 over the four lane groups,
-// the second k0 + 16 g + 8..15, with the activations loaded in the same
-// grouping.  Per-output-channel scales multiply the fp32 sums.
-__device__ inline bf16x8 fp8x8_to_bf16(uint32_t lo, uint32_t hi) {
-    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-    u32x4v r;
-    r[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 1.0f, false));
-    r[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 1.0f, true));
-    r[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 1.0f, false));
-    r[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 1.0f, true));
-    return __builtin_bit_cast(bf16x8, r);
-}
-
-template <int MT, int NS, int U, int WAVES, bool TILE>
-__global__ __launch_bounds__(64 * WAVES) void decode_fp8_kernel(DecodeParams p) {
-    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-    constexpr int kWaves = WAVES;
-    constexpr int kThreads = 64 * WAVES;
-    constexpr int TN = 16 * NS;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int tile = blockIdx.x / p.split_k;
-    const int split = blockIdx.x - tile * p.split_k;
-    const int u0 = int((int64_t(p.units) * split) / p.split_k);
-    const int u1 = int((int64_t(p.units) * (split + 1)) / p.split_k);
-    const int st0 = u0 * p.steps_per_unit, st1 = u1 * p.steps_per_unit;
-    const int n_base = tile * TN;
-    const int g = lane >> 4, q = lane & 15;
-    const int kg = g * 16;                     // this lane's 16 K values of a step
-    const uint8_t* wrow[NS];
-#pragma unroll
-    for (int j = 0; j < NS; ++j) {
-        const int n = n_base + j * 16 + q;
-        wrow[j] = p.W + (TILE ? int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << p.log2_bc)
-                              : int64_t(n) * p.K);
-    }
-    const uint16_t* arow[MT];
-    bool aok[MT], aany[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + q;
-        aok[mt] = m < p.M;
-        aany[mt] = mt * 16 < p.M;
-        arow[mt] = p.A + int64_t(aok[mt] ? m : 0) * p.K + kg;
-    }
-    f32x4 acc[MT][NS];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int j = 0; j < NS; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const bf16x8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
-    const int nsteps = st1 - st0 - wave > 0 ? (st1 - st0 - wave + kWaves - 1) / kWaves : 0;
-    int st = st0 + wave;
-    int i = 0;
-    auto koff = [&](int k) -> int64_t {
-        if (TILE) return (int64_t(k >> p.log2_bc) << p.log2_G) + int64_t(k & p.bc_mask);
-        return int64_t(k);
-    };
-    auto load = [&](int k, u32x4v (&x)[NS], bf16x8 (&a)[MT][2]) {
-        const int64_t ko = koff(k + kg);
-#pragma unroll
-        for (int j = 0; j < NS; ++j) x[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(wrow[j] + ko));
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            if (aany[mt]) {
-                a[mt][0] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + k) : zero8;
-                a[mt][1] = aok[mt] ? *reinterpret_cast<const bf16x8*>(arow[mt] + k + 8) : zero8;
-            } else {
-                a[mt][0] = zero8;
-                a[mt][1] = zero8;
-            }
-        }
-    };
-    auto compute = [&](const u32x4v (&x)[NS], const bf16x8 (&a)[MT][2]) {
-#pragma unroll
-        for (int j = 0; j < NS; ++j) {
-            const bf16x8 w0 = fp8x8_to_bf16(x[j][0], x[j][1]);
-            const bf16x8 w1 = fp8x8_to_bf16(x[j][2], x[j][3]);
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mt][0], w0, acc[mt][j], 0, 0, 0);
-                acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mt][1], w1, acc[mt][j], 0, 0, 0);
-            }
-        }
-    };
-    for (; i + U <= nsteps; i += U) {
-        u32x4v x[U][NS];
-        bf16x8 a[U][MT][2];
-#pragma unroll
-        for (int u = 0; u < U; ++u) load((st + u * kWaves) * 64, x[u], a[u]);
-#pragma unroll
-        for (int u = 0; u < U; ++u) compute(x[u], a[u]);
-        st += U * kWaves;
-    }
-    for (; i < nsteps; ++i) {
-        u32x4v x[NS];
-        bf16x8 a[MT][2];
-        load(st * 64, x, a);
-        compute(x, a);
-        st += kWaves;
-    }
-    if (p.fetch && lane == 0 && nsteps > 0) atomicAdd(p.fetch, (unsigned long long)nsteps * NS * 1024ull);
-
-    static_assert(WAVES * MT * NS <= 64, "reduction buffer exceeds 64 KB");
-    __shared__ f32x4 red[kWaves][MT][NS][64];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int j = 0; j < NS; ++j) red[wave][mt][j][lane] = acc[mt][j];
-    __syncthreads();
-    constexpr int kEntries = MT * NS * 64;
-    const bool final_out = p.split_k == 1;
-    float* part = p.ws + int64_t(split) * p.M * p.N;
-    for (int e = threadIdx.x; e < kEntries; e += kThreads) {
-        const int mt = e / (NS * 64);
-        const int j = (e / 64) % NS;
-        const int l = e % 64;
-        f32x4 v = red[0][mt][j][l];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) v += red[w][mt][j][l];
-        const int n = n_base + j * 16 + (l & 15);
-        const float sc = p.scales ? p.scales[n] : 1.0f;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int m = mt * 16 + (l >> 4) * 4 + r;
-            if (m < p.M) {
-                if (final_out) store_out(p.C, int64_t(m) * p.N + n, v[r] * sc, p.out_bf16);
-                else part[int64_t(m) * p.N + n] = v[r] * sc;
-            }
-        }
-    }
-}
-
-// Large-granularity-memory emulation for the prefetch-depth model (Eq. 6,
-// Section 5.3): the decode GEMM (M <= 16, 32-row tiles, 4 waves interleaved
-// along K, tile-major weight) on a memory whose every read completes no
-// earlier than 'latency' wall-clock ticks after it is issued.  Each wave keeps
-// D K steps of loads in flight in a ring of registers -- the prefetch degree
-// d = D - 1 of Eq. 6 -- and consumes step i only once the clock has passed
-// its issue time plus the latency, then reissues the slot for step i + D.
-// Every wait ends: the clock is monotonic and the target fixed.
-template <int D>
-__global__ __launch_bounds__(256) void lgms_kernel(DecodeParams p, long long latency) {
-    constexpr int kWaves = 4, NS = 2, TN = 32;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int tile = blockIdx.x / p.split_k;
-    const int split = blockIdx.x - tile * p.split_k;
-    const int u0 = int((int64_t(p.units) * split) / p.split_k);
-    const int u1 = int((int64_t(p.units) * (split + 1)) / p.split_k);
-    const int st0 = u0 * p.steps_per_unit, st1 = u1 * p.steps_per_unit;
-    const int n_base = tile * TN;
-    const int g = lane >> 4, q = lane & 15;
-    const bool lo = q < 8;
-    const int kc = (((q >> 3) << 2) + g) << 3;
-    const uint8_t* wrow[NS][2];
-#pragma unroll
-    for (int j = 0; j < NS; ++j)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-            const int n = n_base + j * 16 + hf * 8 + (q & 7);
-            wrow[j][hf] = p.W + int64_t(n >> p.log2_br) * p.strip_bytes +
-                          (int64_t(n & ((1 << p.log2_br) - 1)) << (p.log2_bc + 1));
-        }
-    const int m = (q & 7);
-    const bool aok0 = m < p.M, aok1 = m + 8 < p.M, aany1 = 8 < p.M;
-    const uint16_t* arow0 = p.A + int64_t(aok0 ? m : 0) * p.K + kc;
-    const uint16_t* arow1 = p.A + int64_t(aok1 ? m + 8 : 0) * p.K + kc;
-    const bf16x8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
-    f32x4 acc[NS];
-#pragma unroll
-    for (int j = 0; j < NS; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int nsteps = st1 - st0 - wave > 0 ? (st1 - st0 - wave + kWaves - 1) / kWaves : 0;
-    bf16x8 x[D][NS][2], xa[D][2];
-    long long t_issue[D];
-    auto issue = [&](int slot_i, int i) {   // loads of this wave's i-th step
-        const int k = (st0 + wave + i * kWaves) * 64;
-        const int64_t ko = (int64_t((k + kc) >> p.log2_bc) << p.log2_G) + int64_t(((k + kc) & p.bc_mask) << 1);
-#pragma unroll
-        for (int j = 0; j < NS; ++j)
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf) x[slot_i][j][hf] = load_stream(wrow[j][hf] + ko);
-        xa[slot_i][0] = aok0 ? *reinterpret_cast<const bf16x8*>(arow0 + k) : zero8;
-        xa[slot_i][1] = (aany1 && aok1) ? *reinterpret_cast<const bf16x8*>(arow1 + k) : zero8;
-        t_issue[slot_i] = wall_clock64();
-    };
-#pragma unroll
-    for (int u = 0; u < D; ++u)
-        if (u < nsteps) issue(u, u);
-    for (int base = 0; base < nsteps; base += D) {
-#pragma unroll
-        for (int u = 0; u < D; ++u) {
-            const int i = base + u;
-            if (i < nsteps) {
-                while (wall_clock64() < t_issue[u] + latency) __builtin_amdgcn_s_sleep(1);
-                bf16x8 a0, a1;
-                {
-                    const bf16x8 t = lo ? xa[u][1] : xa[u][0];
-                    const bf16x8 sw = swap8(t);
-                    a0 = lo ? xa[u][0] : sw;
-                    a1 = lo ? sw : xa[u][1];
-                }
-#pragma unroll
-                for (int j = 0; j < NS; ++j) {
-                    const bf16x8 t = lo ? x[u][j][1] : x[u][j][0];
-                    const bf16x8 sw = swap8(t);
-                    const bf16x8 b0 = lo ? x[u][j][0] : sw, b1 = lo ? sw : x[u][j][1];
-                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc[j], 0, 0, 0);
-                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc[j], 0, 0, 0);
-                }
-                if (i + D < nsteps) issue(u, i + D);
-            }
-        }
-    }
-    __shared__ f32x4 red[kWaves][NS][64];
-#pragma unroll
-    for (int j = 0; j < NS; ++j) red[wave][j][lane] = acc[j];
-    __syncthreads();
-    const bool final_out = p.split_k == 1;
-    float* part = p.ws + int64_t(split) * p.M * p.N;
-    for (int e = threadIdx.x; e < NS * 64; e += 256) {
-        const int j = e / 64, l = e % 64;
-        f32x4 v = red[0][j][l];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) v += red[w][j][l];
-        const int n = n_base + j * 16 + (l & 15);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int mm = (l >> 4) * 4 + r;
-            if (mm < p.M) {
-                if (final_out) store_out(p.C, int64_t(mm) * p.N + n, v[r], p.out_bf16);
-                else part[int64_t(mm) * p.N + n] = v[r];
-            }
-        }
-    }
-}
-
 // C[i] = sum over s = 0..S-1 (ascending) of ws[s][i]; i covers M*N/4 float4s.
 // All S partial loads are issued before the in-order sum (latency-bound
 // kernel); S <= kMaxSplitReduce.
@@ -639,43 +332,7 @@ hipError_t launch_m(const DecodeParams& p, int grid, int ns, int waves, bool til
                 : launch_w<MT, 4, false>(p, grid, waves, grouped, stream);
 }
 
-template <int MT, int NS, int WAVES, bool TILE>
-hipError_t launch_fp8_t(const DecodeParams& p, int grid, hipStream_t stream) {
-    constexpr int U = MT >= 2 ? 2 : 4;
-    hipLaunchKernelGGL((decode_fp8_kernel<MT, NS, U, WAVES, TILE>), dim3(grid), dim3(64 * WAVES), 0, stream, p);
-    return hipGetLastError();
-}
-
-template <int MT, int NS, bool TILE>
-hipError_t launch_fp8_w(const DecodeParams& p, int grid, int waves, hipStream_t stream) {
-    if constexpr (MT * NS <= 2) {
-        if (waves == 16) return launch_fp8_t<MT, NS, 16, TILE>(p, grid, stream);
-    }
-    if constexpr (MT * NS <= 8) {
-        if (waves == 8) return launch_fp8_t<MT, NS, 8, TILE>(p, grid, stream);
-    }
-    return launch_fp8_t<MT, NS, 4, TILE>(p, grid, stream);
-}
-
-template <int MT>
-hipError_t launch_fp8_m(const DecodeParams& p, int grid, int ns, int waves, bool tile, hipStream_t stream) {
-    if (ns == 2) return tile ? launch_fp8_w<MT, 2, true>(p, grid, waves, stream)
-                             : launch_fp8_w<MT, 2, false>(p, grid, waves, stream);
-    return tile ? launch_fp8_w<MT, 4, true>(p, grid, waves, stream) : launch_fp8_w<MT, 4, false>(p, grid, waves, stream);
-}
-
-template <int D>
-const void* lgms_fn() { return reinterpret_cast<const void*>(&lgms_kernel<D>); }
-
 }  // namespace
-
-int lgms_ctas_per_cu(int steps_in_flight) {
-    int n = 0;
-    const void* f = steps_in_flight == 1 ? lgms_fn<1>() : steps_in_flight == 2 ? lgms_fn<2>()
-                  : steps_in_flight == 4 ? lgms_fn<4>() : lgms_fn<8>();
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, 256, 0) != hipSuccess) return -1;
-    return n;
-}
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     DecodeParams p;
@@ -711,14 +368,7 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     const int grid = grouped ? d.num_groups * p.tiles_per_group : int(d.N / d.tile_n) * d.split_k;
     const int ns = d.tile_n / 16;
     hipError_t e;
-    if (d.fp8) {
-        switch (d.m_tiles16) {
-            case 1: e = launch_fp8_m<1>(p, grid, ns, d.waves, tile, stream); break;
-            case 2: e = launch_fp8_m<2>(p, grid, ns, d.waves, tile, stream); break;
-            default: e = launch_fp8_m<4>(p, grid, ns, d.waves, tile, stream); break;
-        }
-        return launch_splitk_reduce(d, e, stream);
-    }
+    if (d.fp8) return launch_splitk_reduce(d, launch_fp8_decode(p, grid, d.m_tiles16, ns, d.waves, tile, stream), stream);
     switch (d.m_tiles16) {
         case 1: e = launch_m<1>(p, grid, ns, d.waves, tile, grouped, stream); break;
         case 2: e = launch_m<2>(p, grid, ns, d.waves, tile, grouped, stream); break;
@@ -736,36 +386,6 @@ hipError_t launch_splitk_reduce(const DecodeLaunch& d, hipError_t e, hipStream_t
     else
         hipLaunchKernelGGL((splitk_reduce_kernel<false>), dim3(rgrid), dim3(256), 0, stream, d.ws, d.C, mn4, d.split_k);
     return hipGetLastError();
-}
-
-hipError_t launch_lgms(const DecodeLaunch& d, int64_t latency_ticks, int steps_in_flight, hipStream_t stream) {
-    DecodeParams p;
-    std::memset(&p, 0, sizeof p);
-    p.A = d.A;
-    p.W = d.W;
-    p.C = d.C;
-    p.ws = d.ws;
-    p.M = int(d.M);
-    p.N = int(d.N);
-    p.K = int(d.K);
-    p.split_k = d.split_k;
-    p.steps_per_unit = int(d.k_unit / 64);
-    p.units = int(d.K / d.k_unit);
-    p.strip_bytes = d.L.br * d.K * 2;
-    p.log2_br = d.L.log2_br;
-    p.log2_bc = d.L.log2_bc;
-    p.log2_G = d.L.log2_G;
-    p.bc_mask = int(d.L.bc - 1);
-    p.out_bf16 = d.out_bf16;
-    const int grid = int(d.N / 32) * d.split_k;
-    const long long lat = (long long)latency_ticks;
-    switch (steps_in_flight) {
-        case 1: hipLaunchKernelGGL(lgms_kernel<1>, dim3(grid), dim3(256), 0, stream, p, lat); break;
-        case 2: hipLaunchKernelGGL(lgms_kernel<2>, dim3(grid), dim3(256), 0, stream, p, lat); break;
-        case 4: hipLaunchKernelGGL(lgms_kernel<4>, dim3(grid), dim3(256), 0, stream, p, lat); break;
-        default: hipLaunchKernelGGL(lgms_kernel<8>, dim3(grid), dim3(256), 0, stream, p, lat); break;
-    }
-    return launch_splitk_reduce(d, hipGetLastError(), stream);
 }
 
 }  // namespace tl
