@@ -15,5 +15,8 @@ def load(name: str) -> dict:
             try:
                 out[key] = int(val)
             except ValueError:
-                out[key] = val
+                try:
+                    out[key] = float(val)
+                except ValueError:
+                    out[key] = val
     return out

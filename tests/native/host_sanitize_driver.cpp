@@ -1,0 +1,70 @@
+// Host-only driver for the sanitizer test (tests/test_host_sanitizers.py):
+// calls the library's pure-host entry points -- planning, the exact
+// read-amplification count, the view address generator, Eq. 6 and argument
+// validation -- in a build with AddressSanitizer and UndefinedBehaviorSanitizer.
+// The kernel launchers live in the .hip sources, which this build leaves out;
+// the stubs below stand in for them and abort if anything reaches them.
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+#include "tl_internal.h"
+
+namespace tl {
+hipError_t launch_repack(const void*, void*, int64_t, int64_t, const Layout&, bool, hipStream_t) { std::abort(); }
+hipError_t launch_decode(const DecodeLaunch&, hipStream_t) { std::abort(); }
+hipError_t launch_splitk_reduce(const DecodeLaunch&, hipError_t, hipStream_t) { std::abort(); }
+hipError_t launch_lgms(const DecodeLaunch&, int64_t, int, hipStream_t) { std::abort(); }
+int lgms_ctas_per_cu(int) { std::abort(); }
+hipError_t launch_prefill(const PrefillLaunch&, hipStream_t) { std::abort(); }
+hipError_t launch_view_load(const uint8_t*, int64_t, const ViewProgram&, uint8_t*, hipStream_t) { std::abort(); }
+}  // namespace tl
+
+int main() {
+    int bad = 0;
+    tl_layout_desc d = {};
+    d.elem_bytes = 2;
+    d.G = 4096;
+    d.block_rows = 32;
+    tl_amp a;
+    // read amplification: every layout, ragged tiles and shapes, G != memory-tile size
+    for (int kind : {TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE})
+        for (int64_t M : {1, 7, 64})
+            for (int64_t N : {32, 96, 1024})
+                for (int64_t K : {64, 192, 4096})
+                    for (int tn : {16, 64, 96})
+                        for (int tk : {32, 64, 160})
+                            for (int64_t G : {512, 4096, 16384}) {
+                                d.kind = kind;
+                                const bool tile_ok = kind != TL_LAYOUT_TILE || (N % 32 == 0 && K % 64 == 0);
+                                const int rc = tl_read_amp(M, N, K, 16, tn, tk, &d, G, &a);
+                                if ((rc == TL_OK) != tile_ok) ++bad;
+                            }
+    // views: 2-D to 4-D, Case 1, Case 2 and wider-than-tile boxes
+    d.kind = TL_LAYOUT_TILE;
+    std::vector<int64_t> offs(1 << 16);
+    int64_t n = 0;
+    for (int u : {16, 32, 64, 128}) {
+        tl_view v = {};
+        v.rank = 3;
+        v.box[0] = u; v.box[1] = 64; v.box[2] = 2;
+        v.strides[0] = 1; v.strides[1] = 1024; v.strides[2] = 128;
+        v.coords[1] = 32;
+        if (tl_view_offsets(&v, 1024, 256, 2, 4096, 32, offs.data(), int64_t(offs.size()), &n) != TL_OK) ++bad;
+        v.coords[0] = 8;                               // not on a memory-tile boundary
+        if (tl_view_offsets(&v, 1024, 256, 2, 4096, 32, offs.data(), int64_t(offs.size()), &n) != TL_EUNSUPPORTED) ++bad;
+    }
+    // planning and validation
+    tl_plan p;
+    for (int64_t M : {1, 8, 16, 17, 32, 64, 65, 1000, 2048, 4096})
+        for (int64_t N : {512, 8192, 10240, 57344})
+            if (tl_gemm_plan(M, N, 8192, &d, TL_FETCH_BLOCK, &p) != TL_OK) ++bad;
+    tl_layout_desc bad_desc = d;
+    bad_desc.G = 1000;
+    if (tl_gemm_plan(8, 512, 512, &bad_desc, TL_FETCH_BLOCK, &p) != TL_EINVAL) ++bad;
+    if (tl_gemm(nullptr, nullptr, nullptr, 8, 512, 512, &d, TL_FETCH_BLOCK, nullptr) != TL_EINVAL) ++bad;
+    int64_t deg = -1;
+    if (tl_prefetch_degree(8e12, 5e-6, 16777216.0, 128, 1.0, &deg) != TL_OK || deg != 2) ++bad;
+    std::printf("host sanitize driver: %d unexpected results, last view %lld elements\n", bad, (long long)n);
+    return bad ? 1 : 0;
+}
