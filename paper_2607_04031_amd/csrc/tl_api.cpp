@@ -189,20 +189,29 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         if (d->tile_k && (d->tile_k != p.k_unit)) return TL_EUNSUPPORTED;
         const int64_t n_tiles = N / tn;
         const int64_t units = K / p.k_unit;
-        // Balance: every CU should stream the same number of bytes.  With at
-        // least 4 tiles per CU, one 4-wave workgroup per tile; with one or two
-        // tiles per CU (N = 256 or 512 tiles), one workgroup per tile whose 8
-        // or 16 waves split K among themselves (reduced in LDS, no second
-        // kernel); otherwise split K across workgroups (fp32 partials + a
-        // fixed-order reduce kernel).
+        // Balance: every CU should stream the same number of bytes.
+        //  - at least two tiles per CU: one workgroup per tile, K not split;
+        //  - tiles that divide the CUs or fill them a whole number of times
+        //    (N = 8192: 256 tiles of 32 rows, 128 of 64): one workgroup per
+        //    CU, whose 8 or 16 waves split K among themselves (reduced in
+        //    LDS), or four per CU when each K split still streams >= 4096 K
+        //    (the reduce launch then costs a few per cent at most);
+        //  - otherwise split K until there are about 1024 workgroups.
+        // K splits write fp32 partials that a fixed-order reduce kernel sums;
+        // every split covers >= 1024 K.  (Chosen from measurements of the
+        // Llama-70B decode shapes at M = 1, 8 and 32.)
         int64_t S = d->split_k;
         if (S == 0) {
-            if (n_tiles >= kTargetWorkgroups || n_tiles % kCUs == 0) {
+            const int64_t min_units = std::max<int64_t>(1, 1024 / p.k_unit);
+            const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(units / min_units, kMaxSplitK));
+            if (n_tiles >= 2 * kCUs) {
                 S = 1;
+            } else if (kCUs % n_tiles == 0 || n_tiles % kCUs == 0) {
+                S = std::max<int64_t>(1, kCUs / n_tiles);
+                if (K / (4 * S) >= 4096) S *= 4;
+                S = std::min(S, max_s);
             } else {
-                const int64_t min_units = std::max<int64_t>(1, 1024 / p.k_unit);  // >= 1024 K per split
-                S = (kTargetWorkgroups + n_tiles - 1) / n_tiles;
-                S = std::max<int64_t>(1, std::min<int64_t>(S, units / min_units));
+                S = std::min((kTargetWorkgroups + n_tiles - 1) / n_tiles, max_s);
             }
         }
         if (S < 1 || S > units || S > kMaxSplitK) return TL_EUNSUPPORTED;

@@ -155,6 +155,32 @@ def test_decode_split_k_parity_and_reproducible(split_k):
     assert np.array_equal(C1, C2)    # fixed-order reduction: bitwise reproducible
 
 
+def test_decode_split_k_interleaved_calls():
+    """Split calls of different shapes and split counts, back to back on one
+    stream: each workgroup arrival counter must be back at zero after every
+    call, so every call equals the same call made alone."""
+    banner("decode split-K interleaved calls")
+    cases = [(8, 512, 4096, 3), (1, 1024, 2048, 7), (8, 512, 4096, 2), (32, 256, 8192, 16), (8, 512, 4096, 3)]
+    alone = {}
+    for (M, N, K, S) in cases:
+        A = synth.normal_bf16((M, K), seed=M + N)
+        W = synth.normal_bf16((N, K), seed=K, sigma=synth.W_SIGMA)
+        alone.setdefault((M, N, K, S), host_f32(run_gemm(A, W, tl.layout(split_k=S))))
+    import torch
+    outs = []
+    for (M, N, K, S) in cases * 2:              # no synchronisation between the calls
+        A = dev_bf16(synth.normal_bf16((M, K), seed=M + N))
+        W = dev_bf16(synth.normal_bf16((N, K), seed=K, sigma=synth.W_SIGMA))
+        Wt = torch.empty_like(W)
+        tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
+        C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(split_k=S), tl.TL_FETCH_BLOCK)
+        outs.append(((M, N, K, S), C, A, Wt))
+    _sync()
+    for key, C, _, _ in outs:
+        assert np.array_equal(host_f32(C), alone[key]), key
+
+
 @pytest.mark.parametrize("M", [1, 8, 32, 64])
 def test_decode_one_hot_exact(M):
     """A[m] = e_{k_m}: every output is one weight element, exact in any order."""

@@ -114,7 +114,7 @@ def test_gemm_plan_decode_and_prefill_shapes():
     d = tl.layout()
     # Llama-70B-shaped decode at M = 8: whole memory tiles per compute tile
     for N, K, S, waves in [(10240, 8192, 4, 4), (8192, 8192, 1, 16), (57344, 8192, 1, 4),
-                           (8192, 28672, 1, 16)]:
+                           (8192, 28672, 4, 4)]:
         p = tl.tl_gemm_plan(8, N, K, d)
         assert p["kernel"] == 1 and p["tile_n"] == 32 and p["tile_k"] == 64
         assert p["split_k"] == S and p["waves"] == waves
@@ -124,6 +124,10 @@ def test_gemm_plan_decode_and_prefill_shapes():
     # 512 tiles -> 8 waves; registers cap waves as M and tile_n grow
     assert tl.tl_gemm_plan(8, 16384, 1024, d)["waves"] == 8
     assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 64      # M > 16: 64-row tiles
+    # 128 tiles of 64 rows: K split in two, one 8-wave workgroup per CU
+    p = tl.tl_gemm_plan(32, 8192, 8192, d)
+    assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (64, 2, 8, 256)
+    assert tl.tl_gemm_plan(32, 57344, 8192, d)["split_k"] == 1      # >= 2 tiles per CU: no split
     assert tl.tl_gemm_plan(32, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64))["waves"] == 4
