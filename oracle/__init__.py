@@ -8,9 +8,12 @@ The arithmetic lives in ``tl_oracle.c`` (plain C, fp64, '/' and '%' only);
 this module is argument marshalling over ctypes plus numpy buffers.
 
 What each function follows (TileLens, arxiv 2607.04031):
-  tm_offset      Eq. 1 and Eq. 2, Section 3.2
-  repack/unpack  Section 3.2 (the permutation Eq. 2 defines); Section 5.1
-                 (weights are written in this order once, at load time)
+  tm_offset      Eq. 1 and Eq. 2, Section 3.2; Section 3.3 (a dimension that
+                 is not a multiple of the memory tile is padded to whole tiles)
+  packed_bytes   Section 3.3: bytes of the padded tile-major copy
+  repack/unpack  Section 3.2 (the permutation Eq. 2 defines, padding zero);
+                 Section 5.1 (weights are written in this order once, at
+                 load time)
   gemm_f64       Section 2.3 (C = A W^T over the K dimension), fp64
   grouped_gemm_f64  the expert GEMMs of a mixture-of-experts layer (Sections
                  2.3 and 6.2): per group, gather its rows of A and apply
@@ -64,6 +67,8 @@ def _load():
     i64, p = ctypes.c_int64, ctypes.c_void_p
     lib.orc_tm_offset.restype = i64
     lib.orc_tm_offset.argtypes = [i64] * 6
+    lib.orc_packed_bytes.restype = i64
+    lib.orc_packed_bytes.argtypes = [i64] * 5
     lib.orc_elem_offset.restype = i64
     lib.orc_elem_offset.argtypes = [ctypes.c_int] + [i64] * 7
     lib.orc_repack.restype = None
@@ -110,19 +115,36 @@ def _as_bytes(x: np.ndarray) -> np.ndarray:
     return np.ascontiguousarray(x).view(np.uint8).reshape(-1)
 
 
+def packed_bytes(rows: int, cols: int, s: int, G: int, block_rows: int) -> int:
+    """Bytes of the tile-major copy: whole memory tiles (Section 3.3)."""
+    return _load().orc_packed_bytes(rows, cols, s, G, block_rows)
+
+
+def padded_shape(rows: int, cols: int, s: int, G: int, block_rows: int):
+    """(rows, cols) rounded up to whole memory tiles of block_rows x G / (s * block_rows)."""
+    a = G // (s * block_rows)
+    return (-(-rows // block_rows) * block_rows, -(-cols // a) * a)
+
+
 def repack(src: np.ndarray, G: int, block_rows: int) -> np.ndarray:
-    """Row-major [rows, cols] -> tile-major bytes, same dtype and shape."""
+    """Row-major [rows, cols] -> tile-major copy, same dtype, shape rounded up
+    to whole memory tiles (= the input's shape when the tile divides it);
+    padding elements are zero."""
     rows, cols = src.shape
     s = src.dtype.itemsize
-    out = np.empty_like(src)
+    out = np.empty(padded_shape(rows, cols, s, G, block_rows), dtype=src.dtype)
+    assert out.nbytes == packed_bytes(rows, cols, s, G, block_rows)
     _load().orc_repack(_ptr(_as_bytes(src)), _ptr(out), rows, cols, s, G, block_rows)
     return out
 
 
-def unpack(src_tm: np.ndarray, G: int, block_rows: int) -> np.ndarray:
-    rows, cols = src_tm.shape
+def unpack(src_tm: np.ndarray, G: int, block_rows: int, rows: int = None, cols: int = None) -> np.ndarray:
+    """Tile-major copy -> row-major [rows, cols] (default: src_tm's shape)."""
+    rows = src_tm.shape[0] if rows is None else rows
+    cols = src_tm.shape[1] if cols is None else cols
     s = src_tm.dtype.itemsize
-    out = np.empty_like(src_tm)
+    assert src_tm.nbytes >= packed_bytes(rows, cols, s, G, block_rows)
+    out = np.empty((rows, cols), dtype=src_tm.dtype)
     _load().orc_unpack(_ptr(_as_bytes(src_tm)), _ptr(out), rows, cols, s, G, block_rows)
     return out
 

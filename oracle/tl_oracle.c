@@ -34,14 +34,26 @@ enum { ORC_NK_ROW = 0, ORC_KN_ROW = 1, ORC_TILE = 2 };
 /* Eq. 1 (tile indices) and Eq. 2 (tile-major byte offset), Section 3.2.
  *   T_i = i / a, i' = i mod a, T_j = j / b, j' = j mod b
  *   offset = (T_j * K/a + T_i) * (a*b*s) + (j' * a + i') * s
- * with i = c, j = r, K = cols, a = block_cols, b = block_rows. */
+ * with i = c, j = r, K = cols, a = block_cols, b = block_rows.
+ * Section 3.3: when a dimension is not a multiple of the memory tile's side
+ * the weight is padded to whole memory tiles, so a strip of b rows holds
+ * ceil(K / a) memory tiles (K / a when a divides K, the paper's case). */
 int64_t orc_tm_offset(int64_t r, int64_t c, int64_t cols, int64_t s,
                       int64_t G, int64_t block_rows) {
     int64_t b = block_rows;
     int64_t a = G / (s * b);
+    int64_t tiles_per_strip = (cols + a - 1) / a;
     int64_t Ti = c / a, ip = c % a;
     int64_t Tj = r / b, jp = r % b;
-    return (Tj * (cols / a) + Ti) * (a * b * s) + (jp * a + ip) * s;
+    return (Tj * tiles_per_strip + Ti) * (a * b * s) + (jp * a + ip) * s;
+}
+
+/* Bytes of the tile-major copy of a rows x cols matrix: whole memory tiles,
+ * ceil(rows / b) strips of ceil(cols / a) tiles of G bytes (Section 3.3). */
+int64_t orc_packed_bytes(int64_t rows, int64_t cols, int64_t s, int64_t G, int64_t block_rows) {
+    int64_t b = block_rows;
+    int64_t a = G / (s * b);
+    return ((rows + b - 1) / b) * ((cols + a - 1) / a) * G;
 }
 
 /* Byte offset of logical weight element (n, k) of a logical W[N][K], for
@@ -54,16 +66,18 @@ int64_t orc_elem_offset(int kind, int64_t n, int64_t k, int64_t N, int64_t K,
 }
 
 /* Row-major -> tile-major: every element moves from its row-major byte
- * offset to its Eq. 2 offset.  Plain definition, one element at a time. */
+ * offset to its Eq. 2 offset; the padding of partial memory tiles is zero
+ * (dst holds orc_packed_bytes).  Plain definition, one element at a time. */
 void orc_repack(const uint8_t* src, uint8_t* dst, int64_t rows, int64_t cols,
                 int64_t s, int64_t G, int64_t block_rows) {
+    memset(dst, 0, (size_t)orc_packed_bytes(rows, cols, s, G, block_rows));
     for (int64_t r = 0; r < rows; ++r)
         for (int64_t c = 0; c < cols; ++c)
             memcpy(dst + orc_tm_offset(r, c, cols, s, G, block_rows),
                    src + (r * cols + c) * s, (size_t)s);
 }
 
-/* Tile-major -> row-major, the inverse permutation. */
+/* Tile-major -> row-major, the inverse permutation (padding is not read). */
 void orc_unpack(const uint8_t* src, uint8_t* dst, int64_t rows, int64_t cols,
                 int64_t s, int64_t G, int64_t block_rows) {
     for (int64_t r = 0; r < rows; ++r)
@@ -240,7 +254,8 @@ int orc_read_amp(int64_t M, int64_t N, int64_t K, int64_t tm, int64_t tn, int64_
                  int kind, int64_t s, int64_t layout_G, int64_t block_rows,
                  int64_t G, int brute_m, orc_amp* out) {
     if (M < 1 || N < 1 || K < 1 || tm < 1 || tn < 1 || tk < 1 || s < 1 || G < 1) return -1;
-    int64_t total_bytes = N * K * s;
+    /* bytes the stored weight spans: the padded copy for tile-major */
+    int64_t total_bytes = kind == ORC_TILE ? orc_packed_bytes(N, K, s, layout_G, block_rows) : N * K * s;
     int64_t nblocks = (total_bytes + G - 1) / G;
     int64_t* stamp = (int64_t*)malloc((size_t)nblocks * sizeof(int64_t));
     uint8_t* seen = (uint8_t*)calloc((size_t)nblocks, 1);

@@ -56,6 +56,58 @@ def test_repack_roundtrip_and_bijection(rows, cols, s, G, br):
     assert np.all(offs % s == 0)
 
 
+# Section 3.3: a dimension that is not a multiple of the memory tile's side
+# is padded to whole memory tiles.
+PADDED_CASES = [
+    # rows, cols, elem_bytes, G, block_rows
+    (40, 100, 2, 4096, 32),      # both dimensions ragged, (64, 32) BF16 tile
+    (33, 64, 2, 4096, 32),       # one row past a strip
+    (32, 72, 2, 4096, 32),       # cols ragged only
+    (7, 24, 2, 4096, 32),        # smaller than one memory tile
+    (100, 200, 1, 4096, 64),     # FP8 64 x 64
+    (50, 136, 2, 512, 8),        # bc = 32
+    (65, 264, 2, 16384, 16),     # bc = 512
+    (3, 5, 4, 1024, 4),          # 4-byte elements, bc = 64
+]
+
+
+@pytest.mark.parametrize("rows,cols,s,G,br", PADDED_CASES)
+def test_padded_repack_equals_numpy_pad_then_block_reshape(rows, cols, s, G, br):
+    """Zero-pad to whole memory tiles with numpy, then the block reshape: the
+    padded tile-major copy, pads included, without the oracle's offsets."""
+    bc = G // (s * br)
+    dt = {1: np.uint8, 2: np.uint16, 4: np.uint32}[s]
+    src = synth.random_bytes(rows * cols * s, seed=rows * cols + G).view(dt).reshape(rows, cols)
+    R, C = -(-rows // br) * br, -(-cols // bc) * bc
+    padded = np.pad(src, ((0, R - rows), (0, C - cols)))
+    want = padded.reshape(R // br, br, C // bc, bc).transpose(0, 2, 1, 3).reshape(-1)
+    got = oracle.repack(src, G, br)
+    assert got.shape == (R, C)
+    assert np.array_equal(got.reshape(-1), want)
+    assert oracle.packed_bytes(rows, cols, s, G, br) == R * C * s == (R // br) * (C // bc) * G
+
+
+@pytest.mark.parametrize("rows,cols,s,G,br", PADDED_CASES)
+def test_padded_roundtrip_and_offsets_inside_copy(rows, cols, s, G, br):
+    dt = {1: np.uint8, 2: np.uint16, 4: np.uint32}[s]
+    src = synth.random_bytes(rows * cols * s, seed=11).view(dt).reshape(rows, cols)
+    tm = oracle.repack(src, G, br)
+    assert np.array_equal(oracle.unpack(tm, G, br, rows, cols), src)
+    offs = np.array([oracle.tm_offset(r, c, cols, s, G, br) for r in range(rows) for c in range(cols)])
+    assert len(set(offs.tolist())) == offs.size
+    assert offs.min() >= 0 and offs.max() + s <= oracle.packed_bytes(rows, cols, s, G, br)
+    # every memory tile of the copy holds at least one element of the matrix
+    assert len(set((offs // G).tolist())) == oracle.packed_bytes(rows, cols, s, G, br) // G
+
+
+def test_padding_is_invisible_when_the_tile_divides():
+    """Divisible shapes: the padded definition is the paper's Eq. 2 exactly."""
+    for (rows, cols, s, G, br) in REPACK_CASES:
+        assert oracle.packed_bytes(rows, cols, s, G, br) == rows * cols * s
+        assert oracle.repack(np.zeros((rows, cols), {1: np.uint8, 2: np.uint16, 4: np.uint32}[s]), G, br).shape \
+            == (rows, cols)
+
+
 def test_eq3_four_d_strides_view():
     """Eq. 3: the tile-major buffer viewed with shape (a, b, K/a, N/b) and
     element strides (1, a, ab, Kb) returns element (i, j) of the K x N matrix
@@ -448,6 +500,33 @@ def test_ragged_tiles_against_python_sets():
                 useful += (min(n0 + tn, N) - n0) * (min(k0 + tk, K) - k0) * s
         r = oracle.read_amp(1, N, K, 1, tn, tk, kind, G)
         assert r["requests"] == req and r["useful_bytes"] == useful == N * K * s
+
+
+@pytest.mark.parametrize("N,K,br,G", [(40, 100, 32, 4096), (100, 72, 32, 4096), (33, 200, 16, 4096),
+                                      (70, 24, 8, 1024)])
+def test_padded_tile_major_amp_is_the_padding_ratio(N, K, br, G):
+    """Compute tile = memory tile on a padded weight: every (n-tile, k-step)
+    fetches exactly one block, so fetched / useful is the ratio of the padded
+    to the true matrix size -- a closed form independent of the enumeration."""
+    s = 2
+    bc = G // (s * br)
+    r = oracle.read_amp(3, N, K, 2, br, bc, TILE, G, s=s, layout_G=G, block_rows=br)
+    tiles = -(-N // br) * -(-K // bc)
+    assert r["min_blocks_per_tile"] == r["max_blocks_per_tile"] == 1
+    assert r["requests"] == 2 * tiles                      # ceil(3 / 2) m-tiles
+    assert r["unique_blocks"] == tiles
+    assert r["useful_bytes"] == 2 * N * K * s
+    assert r["amp"] == pytest.approx(tiles * G / (N * K * s))
+
+
+def test_padded_amp_hand_counted():
+    """N = 40, K = 100, (64, 32) BF16 memory tiles -> 2 x 2 tiles of 4 KB.
+    Compute tile 16 x 128: n-tiles [0,16) [16,32) [32,40) each span one strip
+    and the single K step [0,100) spans both tile columns: 3 tiles x 2 blocks."""
+    r = oracle.read_amp(1, 40, 100, 1, 16, 128, TILE, 4096, s=2, layout_G=4096, block_rows=32)
+    assert r["requests"] == 6 and r["fetched_bytes"] == 6 * 4096
+    assert r["useful_bytes"] == 40 * 100 * 2
+    assert r["unique_blocks"] == 4
 
 
 def test_granularity_sweep_expectations_on_slice():
