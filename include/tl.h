@@ -114,26 +114,45 @@ typedef struct tl_plan {
 } tl_plan;
 
 /*
+ * tl_tile_bytes -- host only: *bytes = size of the tile-major copy of a
+ * rows x cols matrix, ceil(rows / br) * ceil(cols / bc) memory tiles of G
+ * bytes (br = block_rows, bc = G / (elem_bytes * br)).  Equals
+ * rows * cols * elem_bytes when br divides rows and bc divides cols, the
+ * paper's assumption (Section 3.3); otherwise the copy is padded to whole
+ * memory tiles, the remedy the same section names.  0 for an empty matrix.
+ * Errors: TL_EINVAL for a NULL bytes, negative sizes, rows * cols > 2^40 or
+ * a bad (elem_bytes, G, block_rows) (see tl_repack).
+ */
+int tl_tile_bytes(int64_t rows, int64_t cols, int32_t elem_bytes, int64_t G, int32_t block_rows,
+                  int64_t* bytes);
+
+/*
  * tl_repack -- row-major -> tile-major (Eq. 2, Section 3.2).
  *
  * src: device, rows x cols elements of elem_bytes each, row-major (cols
  *      contiguous).  For a GEMM weight rows = N and cols = K.
- * dst: device, the same number of bytes, written in tile-major order: element
- *      (r, c) goes to byte
- *        ((r / br) * (cols / bc) + c / bc) * G + ((r % br) * bc + c % bc) * s
+ * dst: device, tl_tile_bytes(rows, cols, ...) bytes, written in tile-major
+ *      order: element (r, c) goes to byte
+ *        ((r / br) * ceil(cols / bc) + c / bc) * G + ((r % br) * bc + c % bc) * s
  *      with br = block_rows, bc = G / (s * br), s = elem_bytes.  Memory tiles
- *      follow one another along cols inside each strip of br rows.
+ *      follow one another along cols inside each strip of br rows.  When br
+ *      does not divide rows or bc does not divide cols, the last strip and the
+ *      last memory tile of every strip are padded (Section 3.3): their bytes
+ *      outside the matrix are written as zeros.
  * The copy moves bytes only (dtype-agnostic); weights are repacked once, when
  * they are loaded (Section 5.1).
  * Errors: TL_EINVAL unless elem_bytes in {1,2,4,8}; G and block_rows powers of
- * two with elem_bytes * block_rows <= G; rows % br == 0; cols % bc == 0;
- * src, dst non-NULL, 16-byte aligned, and not overlapping.  Empty matrices
- * (rows == 0 or cols == 0) are a no-op.
+ * two with elem_bytes * block_rows <= G <= 2^30; rows * cols <= 2^40; src,
+ * dst non-NULL, 16-byte aligned, and not overlapping; TL_EUNSUPPORTED for a
+ * copy of 2^32 memory tiles or more.  Empty matrices (rows == 0 or cols == 0)
+ * are a no-op.
  */
 int tl_repack(const void* src, void* dst, int64_t rows, int64_t cols, int32_t elem_bytes,
               int64_t G, int32_t block_rows, void* stream);
 
-/* tl_unpack -- the inverse permutation of tl_repack, same contract. */
+/* tl_unpack -- the inverse permutation of tl_repack, same contract: src_tm
+ * holds tl_tile_bytes bytes (its padding is not read), dst rows x cols
+ * elements row-major. */
 int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t elem_bytes,
               int64_t G, int32_t block_rows, void* stream);
 
@@ -144,7 +163,9 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * A:   device bf16, row-major [M][K] (lda = K).  Activations are read from HBM
  *      as usual; only the weight lives in the large-granularity layout
  *      (Section 5.1).
- * W:   device bf16 weight in the layout layout->kind describes.
+ * W:   device bf16 weight in the layout layout->kind describes; tile-major:
+ *      the tl_tile_bytes bytes tl_repack wrote, padded when N or K is not a
+ *      multiple of the memory tile's sides (Section 3.3) -- any N and K.
  * C:   device, row-major [M][N] (ldc = N), fp32 or bf16 (round to nearest
  *      even) per layout->out_dtype.  C must not overlap A or W.
  * fetch_mode: TL_FETCH_NATIVE or TL_FETCH_BLOCK, optionally | TL_FETCH_COUNT.
@@ -160,12 +181,12 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
  * per-channel scales).
  * Errors: TL_EINVAL for M, N, K < 1, NULL or misaligned pointers, a bad
- * descriptor (see tl_repack) or N % block_rows / K % block_cols != 0 for
- * TL_LAYOUT_TILE, or a bad G for NK_ROW with TL_FETCH_BLOCK;
- * TL_EUNSUPPORTED for elem_bytes other than 1 or 2, K % 64 != 0,
- * N % 32 != 0, block_cols * elem_bytes < 16, a combination of layout, fetch
- * mode and tile that no kernel implements (NK_ROW with BLOCK above 64 rows or
- * with FP8, FP8 above 64 rows), or TL_LAYOUT_KN_ROW.
+ * descriptor (see tl_repack), or a bad G for NK_ROW with TL_FETCH_BLOCK;
+ * TL_EUNSUPPORTED for elem_bytes other than 1 or 2, K not a multiple of
+ * 16 / elem_bytes (one 16-byte load: keeps rows of A 16-byte aligned),
+ * block_cols * elem_bytes < 16, a combination of layout, fetch mode and tile
+ * that no kernel implements (NK_ROW with BLOCK above 64 rows, with FP8, or
+ * with K % 64 or N % 32 != 0; FP8 above 64 rows), or TL_LAYOUT_KN_ROW.
  * TL_ENOMEM if the split-K workspace cannot be allocated; TL_EHIP if the
  * launch fails.
  */
@@ -214,7 +235,8 @@ int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout,
  *                M tile (16, 32 or 64 rows).  A group with more rows is
  *                processed in several passes over its weight (correct, more
  *                traffic).
- * W:             device, group_stride >= N * K * 2 bytes apart (multiple of 16).
+ * W:             device, group_stride bytes apart (a multiple of 16, at least
+ *                one weight: tl_tile_bytes for tile-major, N * K * 2 else).
  * C:             device [total_rows][N] row-major, fp32 or bf16 per
  *                layout->out_dtype; rows of empty groups are not written.
  * Weights stream once per group and pass (4-wave workgroups, one per (group,
@@ -242,10 +264,12 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
  * element of its weight sub-tile (clipped at the matrix edge); nothing is
  * reused across tiles, steps or m-tiles; only the weight is counted
  * (Section 5.1).  layout->kind, elem_bytes and, for TILE, layout->G and
- * block_rows define byte offsets; G here is the memory system's granularity
- * and may differ from layout->G.  Other descriptor fields are ignored.
- * Errors: TL_EINVAL for non-positive sizes or tiles, G < 1, a bad TILE
- * descriptor, or NULL pointers.
+ * block_rows define byte offsets (a padded tile-major copy when the memory
+ * tile does not divide N or K, as tl_repack writes it; useful bytes count the
+ * N x K matrix only); G here is the memory system's granularity and may
+ * differ from layout->G.  Other descriptor fields are ignored.
+ * Errors: TL_EINVAL for non-positive sizes or tiles, G < 1, N * K > 2^40, a
+ * bad TILE descriptor, or NULL pointers.
  */
 int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
                 int32_t tile_k, const tl_layout_desc* layout, int64_t G, tl_amp* out);
@@ -279,8 +303,9 @@ int tl_prefetch_degree(double bandwidth, double latency, double bytes_per_iterat
  * Errors: TL_EINVAL for steps_in_flight not in {1, 2, 4, 8}, latency_ns
  * outside [0, 1e9], and what tl_gemm rejects with TL_EINVAL;
  * TL_EUNSUPPORTED for M > 16, a layout other than TL_LAYOUT_TILE,
- * block_rows > 32, or what tl_gemm rejects with it; TL_EHIP, TL_ENOMEM as
- * tl_gemm.
+ * block_rows > 32, a padded weight (N % 32, K % 64, N % block_rows or
+ * K % block_cols != 0), or what tl_gemm rejects with it; TL_EHIP, TL_ENOMEM
+ * as tl_gemm.
  */
 int tl_gemm_lgms(const void* A, const void* W_tm, void* C, int64_t M, int64_t N, int64_t K,
                  const tl_layout_desc* layout, int64_t latency_ns, int32_t steps_in_flight, void* stream);

@@ -5,6 +5,7 @@ arguments (torch tensors -> device pointers, the current torch stream -> a
 hipStream_t) and turns status codes into exceptions.  The entry points carry
 the C names and argument order of ``include/tl.h``:
 
+    tl_tile_bytes(rows, cols, elem_bytes, G, block_rows) -> int
     tl_repack(src, dst, rows, cols, elem_bytes, G, block_rows, stream=None)
     tl_unpack(src_tm, dst, rows, cols, elem_bytes, G, block_rows, stream=None)
     tl_gemm(A, W, C, M, N, K, layout, fetch_mode, stream=None)
@@ -35,7 +36,7 @@ TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE = 0, 1, 2
 TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
-EXPORTED = ("tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
+EXPORTED = ("tl_tile_bytes", "tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
             "tl_view_offsets", "tl_view_load", "tl_prefetch_degree", "tl_gemm_lgms", "tl_lgms_occupancy",
             "tl_fetch_counter_read", "tl_release", "tl_strerror")
 TL_VIEW_MAX_RANK = 5
@@ -115,6 +116,8 @@ def load_library():
     import torch  # noqa: F401  (binds libtl to torch's libamdhip64)
     lib = ctypes.CDLL(LIB_PATH)
     i32, i64, p = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+    lib.tl_tile_bytes.restype = ctypes.c_int
+    lib.tl_tile_bytes.argtypes = [i64, i64, i32, i64, i32, ctypes.POINTER(i64)]
     lib.tl_repack.restype = ctypes.c_int
     lib.tl_repack.argtypes = [p, p, i64, i64, i32, i64, i32, p]
     lib.tl_unpack.restype = ctypes.c_int
@@ -193,6 +196,12 @@ def _check(rc: int, where: str):
 # ---------------------------------------------------------------------------
 # C ABI, same names and argument order
 # ---------------------------------------------------------------------------
+
+def tl_tile_bytes(rows, cols, elem_bytes, G, block_rows) -> int:
+    out = ctypes.c_int64()
+    _check(load_library().tl_tile_bytes(rows, cols, elem_bytes, G, block_rows, ctypes.byref(out)), "tl_tile_bytes")
+    return out.value
+
 
 def tl_repack(src, dst, rows, cols, elem_bytes, G, block_rows, stream=None):
     _check(load_library().tl_repack(_ptr(src), _ptr(dst), rows, cols, elem_bytes, G, block_rows,
@@ -306,19 +315,30 @@ def layout(kind=TL_LAYOUT_TILE, G=4096, block_rows=32, out_dtype=TL_OUT_F32, ele
                       split_k=split_k))
 
 
+def padded_shape(rows, cols, elem_bytes, G=4096, block_rows=32):
+    """(rows, cols) rounded up to whole memory tiles: the shape of a tensor
+    that holds the tile-major copy (tl_tile_bytes bytes)."""
+    bc = G // (elem_bytes * block_rows)
+    return (-(-rows // block_rows) * block_rows, -(-cols // bc) * bc)
+
+
 def repack(w, G=4096, block_rows=32, out=None, stream=None):
-    """Tile-major copy of a 2-D device tensor (same dtype and shape)."""
+    """Tile-major copy of a 2-D device tensor, same dtype, shape rounded up
+    to whole memory tiles (the input's shape when the tile divides it)."""
     import torch
-    out = torch.empty_like(w) if out is None else out
     rows, cols = w.shape
+    if out is None:
+        out = torch.empty(padded_shape(rows, cols, w.element_size(), G, block_rows), dtype=w.dtype, device=w.device)
     tl_repack(w, out, rows, cols, w.element_size(), G, block_rows, stream)
     return out
 
 
-def unpack(w_tm, G=4096, block_rows=32, out=None, stream=None):
+def unpack(w_tm, G=4096, block_rows=32, rows=None, cols=None, out=None, stream=None):
+    """Row-major [rows, cols] (default: w_tm's shape) from a tile-major copy."""
     import torch
-    out = torch.empty_like(w_tm) if out is None else out
-    rows, cols = w_tm.shape
+    rows = w_tm.shape[0] if rows is None else rows
+    cols = w_tm.shape[1] if cols is None else cols
+    out = torch.empty((rows, cols), dtype=w_tm.dtype, device=w_tm.device) if out is None else out
     tl_unpack(w_tm, out, rows, cols, w_tm.element_size(), G, block_rows, stream)
     return out
 

@@ -85,26 +85,28 @@ bool overlap(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
     return x < y + uintptr_t(b_bytes) && y < x + uintptr_t(a_bytes);
 }
 
+constexpr int64_t kMaxElems = int64_t(1) << 40;   // rows * cols bound (keeps byte counts in int64)
+
 int check_repack_args(const void* src, const void* dst, int64_t rows, int64_t cols, int32_t s,
-                      int64_t G, int32_t br, Layout* L) {
+                      int64_t G, int32_t br, bool inverse, Layout* L) {
     if (rows < 0 || cols < 0) return TL_EINVAL;
     if (make_tile_layout(s, G, br, L) != TL_OK) return TL_EINVAL;
-    if (rows % L->br || cols % L->bc) return TL_EINVAL;
     if (rows == 0 || cols == 0) return TL_OK;
     if (!src || !dst || !aligned16(src) || !aligned16(dst)) return TL_EINVAL;
-    if (rows > (int64_t(1) << 40) / std::max<int64_t>(cols, 1)) return TL_EINVAL;
-    const int64_t bytes = rows * cols * s;
-    if (overlap(src, bytes, dst, bytes)) return TL_EINVAL;
+    if (rows > kMaxElems / std::max<int64_t>(cols, 1) || cols > kMaxElems) return TL_EINVAL;
+    // the row-major matrix and the padded tile-major copy (src and dst, or the reverse)
+    const int64_t rm_bytes = rows * cols * s, tm_bytes = packed_bytes(*L, rows, cols);
+    if (overlap(src, inverse ? tm_bytes : rm_bytes, dst, inverse ? rm_bytes : tm_bytes)) return TL_EINVAL;
     return TL_OK;
 }
 
 int do_repack(const void* src, void* dst, int64_t rows, int64_t cols, int32_t s, int64_t G,
               int32_t br, void* stream, bool inverse) {
     Layout L;
-    int rc = check_repack_args(src, dst, rows, cols, s, G, br, &L);
+    int rc = check_repack_args(src, dst, rows, cols, s, G, br, inverse, &L);
     if (rc != TL_OK) return rc;
     if (rows == 0 || cols == 0) return TL_OK;
-    if ((rows * cols * s) / L.G >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;  // 32-bit block index
+    if (packed_bytes(L, rows, cols) / L.G >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;  // 32-bit block index
     hipError_t e = launch_repack(src, dst, rows, cols, L, inverse, (hipStream_t)stream);
     return e == hipSuccess ? TL_OK : TL_EHIP;
 }
@@ -153,7 +155,6 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
 
     if (d->kind == TL_LAYOUT_TILE) {
         if (make_tile_layout(s, d->G, d->block_rows, &p.L) != TL_OK) return TL_EINVAL;
-        if (N % p.L.br || K % p.L.bc) return TL_EINVAL;
         if (p.L.bc * s < 16) return TL_EUNSUPPORTED;   // a 16-byte lane load stays in one memory-tile row
     } else if (d->kind == TL_LAYOUT_NK_ROW) {
         p.L.kind = TL_LAYOUT_NK_ROW;
@@ -167,7 +168,12 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
     } else {
         return TL_EUNSUPPORTED;
     }
-    if (K % 64 || N % 32) return TL_EUNSUPPORTED;
+    // Any N; K a multiple of one 16-byte lane load, so activation (and
+    // row-major weight) rows stay 16-byte aligned and a load is either wholly
+    // inside K or wholly past it.  Ragged N or K (padded tile-major weights,
+    // Section 3.3) is not implemented for the row-major block emulation.
+    if (K % (16 / s)) return TL_EUNSUPPORTED;
+    if (p.block_row && (K % 64 || N % 32)) return TL_EUNSUPPORTED;
 
     const bool tile = d->kind == TL_LAYOUT_TILE;
     p.k_unit = tile ? std::max<int64_t>(64, p.L.bc) : 64;
@@ -185,10 +191,9 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         int tn = d->tile_n ? d->tile_n : tn_default;
         if (tn != 32 && tn != 64) return TL_EUNSUPPORTED;
         if (tile && tn % p.L.br) return TL_EUNSUPPORTED;
-        if (N % tn) return TL_EUNSUPPORTED;
         if (d->tile_k && (d->tile_k != p.k_unit)) return TL_EUNSUPPORTED;
-        const int64_t n_tiles = N / tn;
-        const int64_t units = K / p.k_unit;
+        const int64_t n_tiles = (N + tn - 1) / tn;
+        const int64_t units = (K + p.k_unit - 1) / p.k_unit;
         // Balance: every CU should stream the same number of bytes.
         //  - at least two tiles per CU: one workgroup per tile, K not split;
         //  - tiles that divide the CUs or fill them a whole number of times
@@ -230,7 +235,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.pub.split_k = int(S);
         p.pub.waves = waves;
         p.pub.workgroups = wgs;
-        p.pub.workspace_bytes = S > 1 ? S * M * N * 4 : 0;
+        p.pub.workspace_bytes = S > 1 ? S * ((M * N + 3) / 4 * 4) * 4 : 0;
     } else {
         p.pub.kernel = 2;
         int tm = d->tile_m ? d->tile_m : (M >= 1024 ? 256 : 128);
@@ -241,7 +246,8 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         if (d->tile_k && d->tile_k != p.k_unit) return TL_EUNSUPPORTED;
         if (d->split_k > 1) return TL_EUNSUPPORTED;
         // the kernel addresses A and W with 32-bit byte offsets
-        if (M * K * 2 >= (int64_t(1) << 32) || N * K * 2 >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;
+        const int64_t wb = tile ? packed_bytes(p.L, N, K) : N * K * 2;
+        if (M * K * 2 >= (int64_t(1) << 32) || wb >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;
         // Quantisation: 256 x 256 tiles that leave the last round of
         // workgroups part-empty (QKV at M = 2048: 320 tiles on 256 CUs) cover
         // the widest column range whose tile count is a multiple of the CU
@@ -309,6 +315,15 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
     return do_repack(src_tm, dst, rows, cols, elem_bytes, G, block_rows, stream, true);
 }
 
+int tl_tile_bytes(int64_t rows, int64_t cols, int32_t elem_bytes, int64_t G, int32_t block_rows, int64_t* bytes) {
+    Layout L;
+    if (!bytes || rows < 0 || cols < 0) return TL_EINVAL;
+    if (make_tile_layout(elem_bytes, G, block_rows, &L) != TL_OK) return TL_EINVAL;
+    if (cols > kMaxElems || (cols > 0 && rows > kMaxElems / cols)) return TL_EINVAL;
+    *bytes = rows == 0 || cols == 0 ? 0 : packed_bytes(L, rows, cols);
+    return TL_OK;
+}
+
 int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout, int32_t fetch_mode,
                  tl_plan* out) {
     if (!out) return TL_EINVAL;
@@ -327,7 +342,7 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
     if (!A || !W || !C || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
     if (scales && (reinterpret_cast<uintptr_t>(scales) & 3u)) return TL_EINVAL;
     const int64_t c_bytes = M * N * (p.out_bf16 ? 2 : 4);
-    const int64_t w_bytes = N * K * layout->elem_bytes;
+    const int64_t w_bytes = layout->kind == TL_LAYOUT_TILE ? packed_bytes(p.L, N, K) : N * K * layout->elem_bytes;
     if (overlap(C, c_bytes, A, M * K * 2) || overlap(C, c_bytes, W, w_bytes)) return TL_EINVAL;
     if (scales && overlap(C, c_bytes, scales, N * 4)) return TL_EINVAL;
 
@@ -388,15 +403,16 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, con
     if (num_groups < 1 || total_rows < 0 || a_rows < 1) return TL_EINVAL;
     if (total_rows >= (int64_t(1) << 31) || a_rows >= (int64_t(1) << 31)) return TL_EINVAL;
     if (!token_ids && a_rows < total_rows) return TL_EINVAL;
-    if (group_stride < N * K * 2 || group_stride % 16) return TL_EINVAL;
+    const int64_t one_w = layout->kind == TL_LAYOUT_TILE ? packed_bytes(p.L, N, K) : N * K * 2;
+    if (group_stride < one_w || group_stride % 16) return TL_EINVAL;
     if (!A || !W || !C || !group_offsets || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(group_offsets) & 3u) || (reinterpret_cast<uintptr_t>(token_ids) & 3u))
         return TL_EINVAL;
-    const int64_t tiles = N / p.pub.tile_n;
+    const int64_t tiles = (N + p.pub.tile_n - 1) / p.pub.tile_n;
     if (int64_t(num_groups) * tiles >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;
     if (total_rows == 0) return TL_OK;
     const int64_t c_bytes = total_rows * N * (p.out_bf16 ? 2 : 4);
-    const int64_t w_bytes = (int64_t(num_groups) - 1) * group_stride + N * K * 2;
+    const int64_t w_bytes = (int64_t(num_groups) - 1) * group_stride + one_w;
     if (overlap(C, c_bytes, A, a_rows * K * 2) || overlap(C, c_bytes, W, w_bytes)) return TL_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
@@ -475,6 +491,7 @@ int tl_gemm_lgms(const void* A, const void* W, void* C, int64_t M, int64_t N, in
     int rc = plan_gemm(M, N, K, &d1, TL_FETCH_BLOCK, &p);
     if (rc != TL_OK) return rc;
     if (M > 16 || p.pub.kernel != 1) return TL_EUNSUPPORTED;
+    if (N % 32 || K % 64 || N % p.L.br || K % p.L.bc) return TL_EUNSUPPORTED;   // no padded weights here
     if (!A || !W || !C || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
     const int64_t c_bytes = M * N * (p.out_bf16 ? 2 : 4);
     if (overlap(C, c_bytes, A, M * K * 2) || overlap(C, c_bytes, W, N * K * 2)) return TL_EINVAL;
@@ -492,7 +509,7 @@ int tl_gemm_lgms(const void* A, const void* W, void* C, int64_t M, int64_t N, in
     const int64_t ticks = (latency_ns * int64_t(khz) + 999999) / 1000000;
     hipStream_t s = (hipStream_t)stream;
     StreamState* st = nullptr;
-    rc = get_state(s, size_t(S > 1 ? S * M * N * 4 : 0), &st);
+    rc = get_state(s, size_t(S > 1 ? S * ((M * N + 3) / 4 * 4) * 4 : 0), &st);
     if (rc != TL_OK) return rc;
     DecodeLaunch dl;
     dl.A = static_cast<const uint16_t*>(A);

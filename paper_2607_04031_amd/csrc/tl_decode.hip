@@ -16,6 +16,11 @@
 //   (Section 3.2, Eq. 1): strip = n >> log2(br), row-in-tile = n & (br - 1),
 //   memory tile along K = k >> log2(bc), column-in-tile = k & (bc - 1).
 //   With bc >= 8 each 16-byte load stays inside one memory-tile row.
+//   Padded weights (Section 3.3: N or K not a multiple of the memory tile's
+//   sides, strips of ceil(K / bc) tiles): rows past N load row N - 1 and are
+//   never stored; a last 64-wide K step that is partly past K (K % 8 == 0)
+//   runs once, after the streaming loops, with the lanes past K reading
+//   zeros.
 //   Weight loads are non-temporal (read once) and each load instruction reads
 //   whole 128-byte lines (see decode_kernel).
 // Reduction
@@ -74,10 +79,13 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
         split = blockIdx.x - tile * p.split_k;
     }
 
-    // K range of this split in 64-element steps
+    // K range of this split in 64-element steps; steps from kfull on are
+    // partly past K (only the last one, when K % 64 != 0)
     const int u0 = int((int64_t(p.units) * split) / p.split_k);
     const int u1 = int((int64_t(p.units) * (split + 1)) / p.split_k);
-    const int st0 = u0 * p.steps_per_unit, st1 = u1 * p.steps_per_unit;
+    const int st0 = u0 * p.steps_per_unit;
+    const int st1 = min(u1 * p.steps_per_unit, p.ksteps);
+    const int st1f = min(st1, p.kfull);
 
     const int n_base = tile * TN;
     const int g = lane >> 4, q = lane & 15;
@@ -89,7 +97,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     for (int j = 0; j < NS; ++j)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
-            const int n = n_base + j * 16 + hf * 8 + (q & 7);
+            const int n = min(n_base + j * 16 + hf * 8 + (q & 7), p.N - 1);
             int64_t off;
             if (TILE) off = int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << (p.log2_bc + 1));
             else off = int64_t(n) * p.K * 2;
@@ -127,7 +135,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
 
     const bf16x8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
     // steps of this wave: st0 + wave + 4 * i
-    const int nsteps = st1 - st0 - wave > 0 ? (st1 - st0 - wave + kWaves - 1) / kWaves : 0;
+    const int nsteps = st1f - st0 - wave > 0 ? (st1f - st0 - wave + kWaves - 1) / kWaves : 0;
     int st = st0 + wave;
     int i = 0;
     auto exchange = [&](const bf16x8& x0, const bf16x8& x1, bf16x8& o0, bf16x8& o1) {
@@ -217,12 +225,38 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
         compute(x, a);
         st += kWaves;
     }
+    // the last step, partly past K: its owner wave (in the K interleave)
+    // loads the lanes inside K and zeros the rest (addresses of lanes past K
+    // are clamped to column 0, so every access stays inside the buffers)
+    const bool own_partial = p.kfull < st1 && p.kfull >= st0 && (p.kfull - st0) % kWaves == wave;
+    if (own_partial) {
+        const int k = p.kfull * 64;
+        const bool kin = k + kc < p.K;
+        const int64_t ko = w_koff<TILE>(p, kin ? k + kc : 0);
+        bf16x8 x[NS][2], a[MT][2];
+#pragma unroll
+        for (int j = 0; j < NS; ++j)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                const bf16x8 v = load_stream(wrow[j][hf] + ko);
+                x[j][hf] = kin ? v : zero8;
+            }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                const bf16x8 v = *reinterpret_cast<const bf16x8*>(kin ? arow[mt][hf] + k : arow[mt][hf] - kc);
+                a[mt][hf] = kin && aok[mt][hf] ? v : zero8;
+            }
+        compute(x, a);
+    }
 
-    if (p.fetch && lane == 0 && nsteps > 0) {
+    const int issued = nsteps + (own_partial ? 1 : 0);
+    if (p.fetch && lane == 0 && issued > 0) {
         // tile-major / native: each step issues NS subtiles x 2 loads of 64
         // lanes x 16 B; block emulation: whole blocks fetched
         atomicAdd(p.fetch, BLOCKROW ? (unsigned long long)fetched
-                                    : (unsigned long long)nsteps * 2ull * NS * 1024ull);
+                                    : (unsigned long long)issued * 2ull * NS * 1024ull);
     }
     if constexpr (BLOCKROW) {
         // keeps the block loads live; M >= 1 always, so this never stores
@@ -242,7 +276,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     // in split order by splitk_reduce_kernel.
     constexpr int kEntries = MT * NS * 64;   // f32x4 entries per wave
     const bool final_out = p.split_k == 1;
-    float* part = p.ws + int64_t(split) * p.M * p.N;
+    float* part = p.ws + int64_t(split) * p.ws_stride;
     for (int e = threadIdx.x; e < kEntries; e += kThreads) {
         const int mt = e / (NS * 64);
         const int j = (e / 64) % NS;
@@ -254,7 +288,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int m = mt * 16 + (l >> 4) * 4 + r;
-            if (m < crows) {
+            if (m < crows && n < p.N) {
                 const int64_t row = GROUPED ? int64_t(row0 + mc + m) : int64_t(m);
                 if (final_out) store_out(p.C, row * p.N + n, v[r], p.out_bf16);
                 else part[row * p.N + n] = v[r];
@@ -268,22 +302,29 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     }
 }
 
-// C[i] = sum over s = 0..S-1 (ascending) of ws[s][i]; i covers M*N/4 float4s.
-// All S partial loads are issued before the in-order sum (latency-bound
-// kernel); S <= kMaxSplitReduce.
+// C[e] = sum over s = 0..S-1 (ascending) of ws[s * stride + e] for the mn
+// elements of C, four per thread (stride: mn rounded up to 4, so every
+// split's partials start 16-byte aligned; the last thread's group may be
+// short).  All S partial loads are issued before the in-order sum
+// (latency-bound kernel); S <= kMaxSplitReduce.
 constexpr int kMaxSplitReduce = 16;
 template <bool OUT_BF16>
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, void* C, int64_t mn4, int S) {
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, void* C, int64_t mn, int64_t stride,
+                                                            int S) {
     const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
-    if (i >= mn4) return;
+    if (i * 4 >= mn) return;
     f32x4 part[kMaxSplitReduce];
 #pragma unroll
     for (int s = 0; s < kMaxSplitReduce; ++s)
-        if (s < S) part[s] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ws + int64_t(s) * mn4 * 4) + i);
+        if (s < S) part[s] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ws + int64_t(s) * stride) + i);
     f32x4 acc = part[0];
 #pragma unroll
     for (int s = 1; s < kMaxSplitReduce; ++s)
         if (s < S) acc += part[s];
+    if (i * 4 + 4 > mn) {   // short last group: element stores
+        for (int r = 0; i * 4 + r < mn; ++r) store_out(C, i * 4 + r, acc[r], OUT_BF16);
+        return;
+    }
     if (OUT_BF16) {
         uint2 o;
         o.x = uint32_t(f32_to_bf16_rne(acc[0])) | (uint32_t(f32_to_bf16_rne(acc[1])) << 16);
@@ -346,10 +387,13 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.K = int(d.K);
     p.split_k = d.split_k;
     p.steps_per_unit = int(d.k_unit / 64);
-    p.units = int(d.K / d.k_unit);
+    p.units = int((d.K + d.k_unit - 1) / d.k_unit);
+    p.ksteps = int((d.K + 63) / 64);
+    p.kfull = int(d.K / 64);
+    p.ws_stride = (d.M * d.N + 3) / 4 * 4;
     const bool tile = d.L.kind == TL_LAYOUT_TILE;
     const int64_t elem = d.fp8 ? 1 : 2;          // bytes per weight element
-    p.strip_bytes = tile ? d.L.br * d.K * elem : 0;
+    p.strip_bytes = tile ? d.L.br * padded_cols(d.L, d.K) * elem : 0;
     p.log2_br = tile ? d.L.log2_br : 0;
     p.log2_bc = tile ? d.L.log2_bc : 0;
     p.log2_G = tile ? d.L.log2_G : 0;
@@ -359,13 +403,13 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.w_bytes = d.N * d.K * elem;
     p.offsets = d.group_offsets;
     p.token_ids = d.token_ids;
-    p.tiles_per_group = int(d.N / d.tile_n);
+    p.tiles_per_group = int((d.N + d.tile_n - 1) / d.tile_n);
     p.group_stride = d.group_stride;
     p.a_rows = int(d.a_rows);
     p.total_rows = int(d.total_rows);
     p.scales = d.scales;
     const bool grouped = d.num_groups > 0;
-    const int grid = grouped ? d.num_groups * p.tiles_per_group : int(d.N / d.tile_n) * d.split_k;
+    const int grid = grouped ? d.num_groups * p.tiles_per_group : p.tiles_per_group * d.split_k;
     const int ns = d.tile_n / 16;
     hipError_t e;
     if (d.fp8) return launch_splitk_reduce(d, launch_fp8_decode(p, grid, d.m_tiles16, ns, d.waves, tile, stream), stream);
@@ -379,12 +423,14 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
 
 hipError_t launch_splitk_reduce(const DecodeLaunch& d, hipError_t e, hipStream_t stream) {
     if (e != hipSuccess || d.split_k == 1) return e;
-    const int64_t mn4 = d.M * d.N / 4;
-    const int rgrid = int((mn4 + 255) / 256);
+    const int64_t mn = d.M * d.N, stride = (mn + 3) / 4 * 4;
+    const int rgrid = int((stride / 4 + 255) / 256);
     if (d.out_bf16)
-        hipLaunchKernelGGL((splitk_reduce_kernel<true>), dim3(rgrid), dim3(256), 0, stream, d.ws, d.C, mn4, d.split_k);
+        hipLaunchKernelGGL((splitk_reduce_kernel<true>), dim3(rgrid), dim3(256), 0, stream, d.ws, d.C, mn, stride,
+                           d.split_k);
     else
-        hipLaunchKernelGGL((splitk_reduce_kernel<false>), dim3(rgrid), dim3(256), 0, stream, d.ws, d.C, mn4, d.split_k);
+        hipLaunchKernelGGL((splitk_reduce_kernel<false>), dim3(rgrid), dim3(256), 0, stream, d.ws, d.C, mn, stride,
+                           d.split_k);
     return hipGetLastError();
 }
 

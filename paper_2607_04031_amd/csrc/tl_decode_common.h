@@ -23,8 +23,11 @@ struct DecodeParams {
     int M, N, K;
     int split_k;
     int steps_per_unit;      // 64-element steps per split unit
-    int units;               // K / k_unit
-    int64_t strip_bytes;     // br * K * 2 (TILE) -- bytes per strip of br rows
+    int units;               // ceil(K / k_unit)
+    int ksteps;              // ceil(K / 64): 64-element K steps
+    int kfull;               // K / 64: steps wholly inside K (a last partial step is masked)
+    int64_t ws_stride;       // floats between two splits' partials (M * N rounded up to 4)
+    int64_t strip_bytes;     // br * Kp * s (TILE) -- bytes per strip of br rows, Kp = K padded to bc
     int log2_br, log2_bc, log2_G;
     int bc_mask;
     bool out_bf16;

@@ -15,6 +15,9 @@ namespace {
 // MFMA 16x16x32: the first sums k0 + 16 g + 0..7 over the four lane groups,
 // the second k0 + 16 g + 8..15, with the activations loaded in the same
 // grouping.  Per-output-channel scales multiply the fp32 sums.
+// Padded weights (Section 3.3) as in the bf16 decode kernel: rows past N load
+// row N - 1 and are not stored; a last K step partly past K (K % 16 == 0)
+// runs once after the streaming loops with the lanes past K reading zeros.
 __device__ inline bf16x8 fp8x8_to_bf16(uint32_t lo, uint32_t hi) {
     typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
     u32x4v r;
@@ -37,14 +40,16 @@ __global__ __launch_bounds__(64 * WAVES) void decode_fp8_kernel(DecodeParams p) 
     const int split = blockIdx.x - tile * p.split_k;
     const int u0 = int((int64_t(p.units) * split) / p.split_k);
     const int u1 = int((int64_t(p.units) * (split + 1)) / p.split_k);
-    const int st0 = u0 * p.steps_per_unit, st1 = u1 * p.steps_per_unit;
+    const int st0 = u0 * p.steps_per_unit;
+    const int st1 = min(u1 * p.steps_per_unit, p.ksteps);
+    const int st1f = min(st1, p.kfull);
     const int n_base = tile * TN;
     const int g = lane >> 4, q = lane & 15;
     const int kg = g * 16;                     // this lane's 16 K values of a step
     const uint8_t* wrow[NS];
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
-        const int n = n_base + j * 16 + q;
+        const int n = min(n_base + j * 16 + q, p.N - 1);
         wrow[j] = p.W + (TILE ? int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << p.log2_bc)
                               : int64_t(n) * p.K);
     }
@@ -63,7 +68,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_fp8_kernel(DecodeParams p) 
 #pragma unroll
         for (int j = 0; j < NS; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const bf16x8 zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
-    const int nsteps = st1 - st0 - wave > 0 ? (st1 - st0 - wave + kWaves - 1) / kWaves : 0;
+    const int nsteps = st1f - st0 - wave > 0 ? (st1f - st0 - wave + kWaves - 1) / kWaves : 0;
     int st = st0 + wave;
     int i = 0;
     auto koff = [&](int k) -> int64_t {
@@ -113,7 +118,32 @@ __global__ __launch_bounds__(64 * WAVES) void decode_fp8_kernel(DecodeParams p) 
         compute(x, a);
         st += kWaves;
     }
-    if (p.fetch && lane == 0 && nsteps > 0) atomicAdd(p.fetch, (unsigned long long)nsteps * NS * 1024ull);
+    // the last step, partly past K, by its owner wave; lanes past K read
+    // column 0 (in bounds) and use zeros
+    const bool own_partial = p.kfull < st1 && p.kfull >= st0 && (p.kfull - st0) % kWaves == wave;
+    if (own_partial) {
+        const int k = p.kfull * 64;
+        const bool kin = k + kg < p.K;
+        u32x4v x[NS];
+        bf16x8 a[MT][2];
+        const int64_t ko = koff(kin ? k + kg : 0);
+#pragma unroll
+        for (int j = 0; j < NS; ++j) {
+            const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(wrow[j] + ko));
+            x[j] = kin ? v : u32x4v{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const uint16_t* pa = kin ? arow[mt] + k : arow[mt] - kg;
+            const bf16x8 v0 = *reinterpret_cast<const bf16x8*>(pa);
+            const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(pa + 8);
+            a[mt][0] = kin && aok[mt] ? v0 : zero8;
+            a[mt][1] = kin && aok[mt] ? v1 : zero8;
+        }
+        compute(x, a);
+    }
+    const int issued = nsteps + (own_partial ? 1 : 0);
+    if (p.fetch && lane == 0 && issued > 0) atomicAdd(p.fetch, (unsigned long long)issued * NS * 1024ull);
 
     static_assert(WAVES * MT * NS <= 64, "reduction buffer exceeds 64 KB");
     __shared__ f32x4 red[kWaves][MT][NS][64];
@@ -124,7 +154,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_fp8_kernel(DecodeParams p) 
     __syncthreads();
     constexpr int kEntries = MT * NS * 64;
     const bool final_out = p.split_k == 1;
-    float* part = p.ws + int64_t(split) * p.M * p.N;
+    float* part = p.ws + int64_t(split) * p.ws_stride;
     for (int e = threadIdx.x; e < kEntries; e += kThreads) {
         const int mt = e / (NS * 64);
         const int j = (e / 64) % NS;
@@ -133,11 +163,11 @@ __global__ __launch_bounds__(64 * WAVES) void decode_fp8_kernel(DecodeParams p) 
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) v += red[w][mt][j][l];
         const int n = n_base + j * 16 + (l & 15);
-        const float sc = p.scales ? p.scales[n] : 1.0f;
+        const float sc = p.scales && n < p.N ? p.scales[n] : 1.0f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int m = mt * 16 + (l >> 4) * 4 + r;
-            if (m < p.M) {
+            if (m < p.M && n < p.N) {
                 if (final_out) store_out(p.C, int64_t(m) * p.N + n, v[r] * sc, p.out_bf16);
                 else part[int64_t(m) * p.N + n] = v[r] * sc;
             }

@@ -33,6 +33,14 @@ struct Layout {
 // Checks a tile-major description; fills 'out' on success.
 int make_tile_layout(int64_t s, int64_t G, int64_t br, Layout* out);
 
+// Section 3.3: a weight whose dimensions are not multiples of the memory
+// tile's sides is padded to whole memory tiles.  Columns (along K) of the
+// padded copy, and its bytes: ceil(rows / br) strips of ceil(cols / bc) tiles.
+inline int64_t padded_cols(const Layout& L, int64_t cols) { return (cols + L.bc - 1) / L.bc * L.bc; }
+inline int64_t packed_bytes(const Layout& L, int64_t rows, int64_t cols) {
+    return (rows + L.br - 1) / L.br * ((cols + L.bc - 1) / L.bc) * L.G;
+}
+
 // ---------------------------------------------------------------------------
 // Kernel launchers (defined in the .hip files).  Arguments are validated by
 // the callers; these only enqueue.
@@ -45,7 +53,7 @@ struct DecodeLaunch {
     const uint16_t* A;
     const uint8_t* W;
     void* C;
-    float* ws;                  // [split_k][M][N] partials (split_k > 1)
+    float* ws;                  // [split_k][M * N rounded up to 4] partials (split_k > 1)
     unsigned long long* fetch;  // fetch tally (TL_FETCH_COUNT) or nullptr
     int64_t M, N, K;
     Layout L;

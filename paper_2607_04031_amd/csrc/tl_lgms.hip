@@ -94,7 +94,7 @@ __global__ __launch_bounds__(256) void lgms_kernel(DecodeParams p, long long lat
     for (int j = 0; j < NS; ++j) red[wave][j][lane] = acc[j];
     __syncthreads();
     const bool final_out = p.split_k == 1;
-    float* part = p.ws + int64_t(split) * p.M * p.N;
+    float* part = p.ws + int64_t(split) * p.ws_stride;
     for (int e = threadIdx.x; e < NS * 64; e += 256) {
         const int j = e / 64, l = e % 64;
         f32x4 v = red[0][j][l];
@@ -136,6 +136,7 @@ hipError_t launch_lgms(const DecodeLaunch& d, int64_t latency_ticks, int steps_i
     p.N = int(d.N);
     p.K = int(d.K);
     p.split_k = d.split_k;
+    p.ws_stride = (d.M * d.N + 3) / 4 * 4;
     p.steps_per_unit = int(d.k_unit / 64);
     p.units = int(d.K / d.k_unit);
     p.strip_bytes = d.L.br * d.K * 2;

@@ -17,6 +17,9 @@
 // 16-wide sub-step are read while the current sub-step's MFMAs run.  LDS rows
 // are 128 B with 16-byte chunks XOR-swizzled (see swz) so operand reads are
 // free of bank conflicts.
+// Padded weights (Section 3.3; strips of ceil(K / bc) memory tiles): rows
+// past M or N are clamped and never stored; a last K step partly past K
+// (K % 8 == 0) stages zeros for the chunks past K.
 #include <hip/hip_runtime.h>
 
 #include "tl_internal.h"
@@ -118,14 +121,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
         if (TILE) return (uint32_t(k >> p.log2_bc) << p.log2_G) + uint32_t((k & p.bc_mask) << 1);
         return uint32_t(k) << 1;
     };
-    const int KT = p.K / BK;
+    const int KT = (p.K + BK - 1) / BK;
     auto gload = [&](int kstep) {
         const int k0 = kstep * BK;
+        if (k0 + BK <= p.K) {   // uniform: every step but a partial last one
 #pragma unroll
-        for (int i = 0; i < A_CH; ++i) ra[i] = *a_addr(i, k0);
-        const uint32_t ko = w_koff(k0 + w_k);
+            for (int i = 0; i < A_CH; ++i) ra[i] = *a_addr(i, k0);
+            const uint32_t ko = w_koff(k0 + w_k);
 #pragma unroll
-        for (int i = 0; i < W_CH; ++i) rw[i] = *w_addr(i, ko);
+            for (int i = 0; i < W_CH; ++i) rw[i] = *w_addr(i, ko);
+        } else {
+            // chunks past K: load column 0 (in bounds), stage zeros
+            const bool kin = k0 + w_k < p.K;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int i = 0; i < A_CH; ++i) {
+                const u32x4 v = *a_addr(i, kin ? k0 : -w_k);
+                ra[i] = kin ? v : z;
+            }
+            const uint32_t ko = w_koff(kin ? k0 + w_k : 0);
+#pragma unroll
+            for (int i = 0; i < W_CH; ++i) {
+                const u32x4 v = *w_addr(i, ko);
+                rw[i] = kin ? v : z;
+            }
+        }
     };
     auto sstore = [&](int buf) {
         uint8_t* As = smem + buf * STAGE;
@@ -239,15 +259,18 @@ hipError_t launch_t(const PrefillParams& p, int grid, bool tile, hipStream_t s) 
 }
 
 // One launch over columns [n_begin, n_begin + n_cols) of the GEMM with
-// tile_m x tile_n tiles.  The weight rows of that range start n_begin * K * 2
-// bytes into W in both layouts (tile-major strips of block_rows rows are
-// contiguous, and n_begin is a multiple of block_rows).
+// tile_m x tile_n tiles.  The weight rows of that range start n_begin * Kp * 2
+// bytes into W (Kp: K padded to whole memory tiles for tile-major, K for
+// row-major; tile-major strips of block_rows rows are contiguous, and
+// n_begin is a multiple of block_rows).
 hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols, int tile_m, int tile_n,
                         hipStream_t stream) {
     PrefillParams p;
     const int64_t c_elem = q.out_bf16 ? 2 : 4;
+    const bool tile = q.L.kind == TL_LAYOUT_TILE;
+    const int64_t kp = tile ? padded_cols(q.L, q.K) : q.K;   // K of the stored weight
     p.A = q.A;
-    p.W = q.W + n_begin * q.K * 2;
+    p.W = q.W + n_begin * kp * 2;
     p.C = static_cast<uint8_t*>(q.C) + n_begin * c_elem;
     p.fetch = q.fetch;
     p.M = int(q.M);
@@ -255,8 +278,7 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
     p.K = int(q.K);
     p.ldc = q.N;
     p.m_tiles = int((q.M + tile_m - 1) / tile_m);
-    const bool tile = q.L.kind == TL_LAYOUT_TILE;
-    p.strip_bytes = tile ? q.L.br * q.K * 2 : 0;
+    p.strip_bytes = tile ? q.L.br * kp * 2 : 0;
     p.log2_br = tile ? q.L.log2_br : 0;
     p.log2_bc = tile ? q.L.log2_bc : 0;
     p.log2_G = tile ? q.L.log2_G : 0;

@@ -28,15 +28,19 @@ inline int64_t elem_off(const Geometry& g, int64_t n, int64_t k) {
         case TL_LAYOUT_KN_ROW: return (k * g.N + n) * g.s;
         default: {
             const tl::Layout& L = g.L;
+            // strips of ceil(K / bc) memory tiles (padded, Section 3.3)
             int64_t strip = n >> L.log2_br, r = n & (L.br - 1);
             int64_t kb = k >> L.log2_bc, c = k & (L.bc - 1);
-            return ((strip * (g.K >> L.log2_bc) + kb) << L.log2_G) + ((r << L.log2_bc) + c) * g.s;
+            return ((strip * ((g.K + L.bc - 1) >> L.log2_bc) + kb) << L.log2_G) + ((r << L.log2_bc) + c) * g.s;
         }
     }
 }
 
 // Blocks per tile from a closed form, or -1 if the case is not covered.
 // Requires full tiles (N % tn == 0, K % tk == 0) and power-of-two G, tn, tk.
+// A padded tile-major weight is covered too: tiles narrower than a memory
+// tile stay inside one, and wider ones (power-of-two multiples of its sides)
+// dividing N or K leave nothing to pad along that dimension.
 int64_t closed_form_blocks(const Geometry& g, int64_t tn, int64_t tk, int64_t G) {
     if (!tl::is_pow2(G) || !tl::is_pow2(tn) || !tl::is_pow2(tk)) return -1;
     if (g.N % tn || g.K % tk) return -1;
@@ -80,14 +84,16 @@ extern "C" int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int3
         return TL_EINVAL;
     if (g.kind == TL_LAYOUT_TILE) {
         if (tl::make_tile_layout(g.s, layout->G, layout->block_rows, &g.L) != TL_OK) return TL_EINVAL;
-        if (N % g.L.br || K % g.L.bc) return TL_EINVAL;
     }
+    if (N > (int64_t(1) << 40) / K) return TL_EINVAL;
     const int64_t tm = tile_m, tn = tile_n, tk = tile_k;
     const int64_t m_tiles = (M + tm - 1) / tm;
     const int64_t n_tiles = (N + tn - 1) / tn;
     const int64_t k_steps = (K + tk - 1) / tk;
-    const int64_t total_bytes = N * K * g.s;
-    const int64_t nblocks = (total_bytes + G - 1) / G;
+    const int64_t total_bytes = N * K * g.s;   // the matrix's own bytes
+    // bytes the stored weight spans: the padded copy for tile-major
+    const int64_t span = g.kind == TL_LAYOUT_TILE ? tl::packed_bytes(g.L, N, K) : total_bytes;
+    const int64_t nblocks = (span + G - 1) / G;
 
     tl_amp r;
     std::memset(&r, 0, sizeof r);

@@ -1,10 +1,18 @@
 // Row-major <-> tile-major repack (TileLens Eq. 2, Section 3.2).
 //
 // The kernel walks the TILE-MAJOR buffer in order, CH bytes per lane
-// (CH = min(16, bytes per memory-tile row)), so the tile-major side is always
-// read or written with fully coalesced 16-byte accesses; the row-major side is
-// accessed in runs of block_cols * s bytes (128 B for the (64, 32) BF16 memory
-// tile: one cache line per run).  Byte-exact and dtype-agnostic.
+// (CH = min(16, bytes per memory-tile row), reduced until it divides a
+// row-major row's bytes), so the tile-major side is always read or written
+// with fully coalesced accesses; the row-major side is accessed in runs of
+// block_cols * s bytes (128 B for the (64, 32) BF16 memory tile: one cache
+// line per run).  Byte-exact and dtype-agnostic.
+//
+// Padding (Section 3.3): the tile-major copy holds whole memory tiles,
+// ceil(rows / br) strips of ceil(cols / bc) tiles.  A chunk whose element
+// lies outside the rows x cols matrix is padding: the forward repack writes
+// zeros there and the inverse does not read it.  Because CH divides both a
+// memory-tile row and a row-major row, a chunk is entirely inside or entirely
+// outside the matrix.
 #include <hip/hip_runtime.h>
 
 #include "tl_internal.h"
@@ -15,9 +23,10 @@ namespace {
 struct RepackParams {
     const uint8_t* src;
     uint8_t* dst;
-    int64_t total_chunks;   // bytes / CH
+    int64_t total_chunks;   // tile-major bytes / CH
     int64_t cols_bytes;     // bytes per row-major row
-    uint32_t kblocks;       // memory tiles per strip = cols / bc
+    int64_t rows;           // rows of the matrix (rows past it are padding)
+    uint32_t kblocks;       // memory tiles per strip = ceil(cols / bc)
     int log2_G;
     int log2_rowbytes;      // log2(bc * s): bytes per memory-tile row
     int log2_br;
@@ -57,11 +66,18 @@ __global__ __launch_bounds__(256) void repack_kernel(RepackParams p) {
             const int64_t c_byte = in_blk & row_mask;        // byte inside that row
             const uint32_t strip = block / p.kblocks;
             const uint32_t kb = block - strip * p.kblocks;
-            const int64_t rm = ((int64_t(strip) << p.log2_br) + r_in) * p.cols_bytes +
-                               (int64_t(kb) << p.log2_rowbytes) + c_byte;
-            const int64_t from = p.inverse ? tm : rm;
-            dst_off[u] = p.inverse ? rm : tm;
-            v[u] = *reinterpret_cast<const T*>(p.src + from);
+            const int64_t r = (int64_t(strip) << p.log2_br) + r_in;
+            const int64_t cb = (int64_t(kb) << p.log2_rowbytes) + c_byte;   // byte along the row
+            const bool inside = r < p.rows && cb < p.cols_bytes;
+            const int64_t rm = r * p.cols_bytes + cb;
+            if (p.inverse) {
+                dst_off[u] = inside ? rm : -1;
+                if (inside) v[u] = *reinterpret_cast<const T*>(p.src + tm);
+            } else {
+                dst_off[u] = tm;
+                if (inside) v[u] = *reinterpret_cast<const T*>(p.src + rm);
+                else v[u] = T(0);
+            }
         }
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
@@ -87,10 +103,14 @@ hipError_t launch_repack(const void* src, void* dst, int64_t rows, int64_t cols,
     p.src = static_cast<const uint8_t*>(src);
     p.dst = static_cast<uint8_t*>(dst);
     const int64_t row_bytes = L.bc * L.s;                 // power of two
-    const int64_t ch = row_bytes < 16 ? row_bytes : 16;
-    p.total_chunks = rows * cols * L.s / ch;
+    int64_t ch = row_bytes < 16 ? row_bytes : 16;
+    while ((cols * L.s) % ch) ch >>= 1;                   // aligned row-major chunks
+    const int64_t kblocks = (cols + L.bc - 1) / L.bc;
+    const int64_t strips = (rows + L.br - 1) / L.br;
+    p.total_chunks = strips * kblocks * L.G / ch;
     p.cols_bytes = cols * L.s;
-    p.kblocks = uint32_t(cols / L.bc);
+    p.rows = rows;
+    p.kblocks = uint32_t(kblocks);
     p.log2_G = L.log2_G;
     p.log2_rowbytes = ilog2(row_bytes);
     p.log2_br = L.log2_br;

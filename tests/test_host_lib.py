@@ -54,9 +54,12 @@ def test_read_amp_matches_oracle_random_shapes():
         if s * br > layout_G:
             continue
         bc = layout_G // (s * br)
-        if kind == oracle.TILE:
+        if kind == oracle.TILE and rng.random() < 0.5:
             N = br * int(rng.integers(1, 5)) * (1 if br > 8 else 4)
             K = bc * int(rng.integers(1, 5))
+        elif kind == oracle.TILE:                 # padded to whole memory tiles
+            N = int(rng.integers(1, 70))
+            K = int(rng.integers(1, 300))
         else:
             N = int(rng.integers(1, 70))
             K = int(rng.integers(1, 300))
@@ -105,9 +108,29 @@ def test_read_amp_rejects_bad_arguments():
     bad = tl.layout(G=3000)
     with pytest.raises(tl.TLError):
         tl.tl_read_amp(1, 64, 64, 1, 1, 1, bad, 4096)
-    # TILE requires N % br == 0 and K % bc == 0
-    with pytest.raises(tl.TLError):
-        tl.tl_read_amp(1, 48, 64, 1, 1, 1, tl.layout(block_rows=32), 4096)
+    # a tile-major weight the memory tile does not divide is the padded copy
+    got = tl.tl_read_amp(1, 48, 100, 1, 16, 64, tl.layout(block_rows=32), 4096)
+    want = oracle.read_amp(1, 48, 100, 1, 16, 64, oracle.TILE, 4096, s=2, layout_G=4096, block_rows=32)
+    assert got == {k: (pytest.approx(v) if k == "amp" else v) for k, v in want.items()}
+
+
+def test_tile_bytes_matches_oracle():
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        s = int(rng.choice([1, 2, 4, 8]))
+        G = int(rng.choice([64, 512, 4096, 16384]))
+        br = int(rng.choice([1, 2, 8, 32, 64]))
+        if s * br > G:
+            continue
+        rows, cols = int(rng.integers(1, 3000)), int(rng.integers(1, 3000))
+        assert tl.tl_tile_bytes(rows, cols, s, G, br) == oracle.packed_bytes(rows, cols, s, G, br)
+    assert tl.tl_tile_bytes(8192, 28672, 2, 4096, 32) == 8192 * 28672 * 2     # divisible: no padding
+    assert tl.tl_tile_bytes(0, 100, 2, 4096, 32) == 0
+    for args in [(-1, 8, 2, 4096, 32), (8, 8, 3, 4096, 32), (8, 8, 2, 3000, 32), (8, 8, 2, 4096, 4096),
+                 (1 << 21, 1 << 21, 2, 4096, 32)]:
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_tile_bytes(*args)
+        assert e.value.status == tl.TL_EINVAL
 
 
 def test_gemm_plan_decode_and_prefill_shapes():
@@ -183,8 +206,9 @@ def test_gemm_plan_error_codes():
     cases = [
         ((0, 64, 64, d), tl.TL_EINVAL),
         ((8, 64, 64, tl.layout(G=1000)), tl.TL_EINVAL),
-        ((8, 48, 64, d), tl.TL_EINVAL),                      # N % br
-        ((8, 64, 96, d), tl.TL_EINVAL),                      # K % bc
+        ((8, 64, 100, d), tl.TL_EUNSUPPORTED),               # K % 8: rows of A not 16-byte aligned
+        ((2048, 64, 100, d), tl.TL_EUNSUPPORTED),
+        ((8, 64, 72, tl.layout(elem_bytes=1, block_rows=64)), tl.TL_EUNSUPPORTED),   # FP8: K % 16
         ((8, 64, 64, tl.layout(elem_bytes=4)), tl.TL_EUNSUPPORTED),    # only bf16 and FP8 weights
         ((8, 64, 64, tl.layout(kind=tl.TL_LAYOUT_KN_ROW)), tl.TL_EUNSUPPORTED),
         ((8, 64, 64, tl.layout(G=512, block_rows=64)), tl.TL_EUNSUPPORTED),   # bc = 4
@@ -209,6 +233,25 @@ def test_gemm_plan_error_codes():
     with pytest.raises(tl.TLError) as e:
         tl.tl_gemm_plan(256, 64, 64, rm, tl.TL_FETCH_BLOCK)
     assert e.value.status == tl.TL_EUNSUPPORTED
+    for N, K in ((64, 96), (40, 64)):          # the block emulation needs whole 64-wide steps and 32-row tiles
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_plan(8, N, K, rm, tl.TL_FETCH_BLOCK)
+        assert e.value.status == tl.TL_EUNSUPPORTED
+
+
+def test_gemm_plan_padded_weights():
+    """N and K that the memory tile does not divide (padded copies, Section
+    3.3): ceil-sized grids, same kernels."""
+    d = tl.layout()
+    p = tl.tl_gemm_plan(8, 100, 200, d)
+    assert p["kernel"] == 1 and p["tile_n"] == 32 and p["workgroups"] == 4 * p["split_k"]
+    p = tl.tl_gemm_plan(8, 8200, 28680, d)
+    assert p["kernel"] == 1 and p["workgroups"] == 257 * p["split_k"]
+    p = tl.tl_gemm_plan(2048, 1000, 1000, d)
+    assert p["kernel"] == 2 and p["workgroups"] == 8 * 8
+    fp8 = tl.layout(elem_bytes=1, block_rows=64)
+    assert tl.tl_gemm_plan(8, 100, 208, fp8)["tile_n"] == 64
+    assert tl.tl_gemm_plan(8, 100, 200, tl.layout(kind=tl.TL_LAYOUT_NK_ROW), tl.TL_FETCH_NATIVE)["kernel"] == 1
 
 
 def test_entry_points_reject_before_device_work():
@@ -227,9 +270,18 @@ def test_entry_points_reject_before_device_work():
     with pytest.raises(tl.TLError) as e:
         tl.tl_repack(4096, 8192, 64, 64, 3, 4096, 32, stream=0)          # elem_bytes
     assert e.value.status == tl.TL_EINVAL
-    with pytest.raises(tl.TLError) as e:
-        tl.tl_repack(4096, 8192, 48, 64, 2, 4096, 32, stream=0)          # rows % br
+    with pytest.raises(tl.TLError) as e:        # overlaps only the padding of the 64 x 64 tile-major copy
+        tl.tl_repack(11264, 4096, 48, 64, 2, 4096, 32, stream=0)
     assert e.value.status == tl.TL_EINVAL
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_unpack(4096, 11264, 48, 64, 2, 4096, 32, stream=0)
+    assert e.value.status == tl.TL_EINVAL
+    # a 6144-byte row-major source directly followed by its 8192-byte copy is
+    # not an overlap (validation passes; the launch then fails without a GPU)
+    for fn, a, b in ((tl.tl_repack, 4096, 4096 + 6144), (tl.tl_unpack, 4096 + 6144, 4096)):
+        with pytest.raises(tl.TLError) as e:
+            fn(a, b, 48, 64, 2, 4096, 32, stream=0)
+        assert e.value.status == tl.TL_EHIP
     with pytest.raises(tl.TLError) as e:                                  # overlap
         tl.tl_repack(4096, 4096 + 1024, 64, 64, 2, 4096, 32, stream=0)
     assert e.value.status == tl.TL_EINVAL
@@ -266,7 +318,7 @@ def test_gemm_grouped_rejects_before_device_work():
         (dict(A=(1 << 12) + 8), tl.TL_EINVAL),
         (dict(C=(1 << 12) + 64), tl.TL_EINVAL),                   # C overlaps A
         (dict(C=(1 << 24) + 4096), tl.TL_EINVAL),                 # C overlaps W
-        (dict(N=48), tl.TL_EINVAL),                               # N % block_rows
+        (dict(N=48, K=136), tl.TL_EINVAL),                        # group_stride < the padded copy
         (dict(layout=tl.layout(split_k=2)), tl.TL_EUNSUPPORTED),
         (dict(layout=tl.layout(tile_m=128)), tl.TL_EUNSUPPORTED),
         (dict(layout=tl.layout(kind=tl.TL_LAYOUT_NK_ROW)), None),  # valid: checked by its own case below
