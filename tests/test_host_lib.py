@@ -239,6 +239,22 @@ def test_gemm_plan_error_codes():
         assert e.value.status == tl.TL_EUNSUPPORTED
 
 
+def test_gemm_plan_maximum_sizes():
+    """The prefill kernel addresses A and W with 32-bit byte offsets: a weight
+    just below 4 GB is planned, one of 4 GB is rejected; the decode kernel has
+    64-bit weight offsets and takes larger weights; sizes are int32."""
+    d = tl.layout()
+    assert tl.tl_gemm_plan(256, 131072, 16320, d)["kernel"] == 2          # 4,278,190,080 bytes
+    for N, K in ((131072, 16384), (131072, 16328)):                        # 2^32 bytes; padded copy of 2^32
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_plan(256, N, K, d)
+        assert e.value.status == tl.TL_EUNSUPPORTED
+    assert tl.tl_gemm_plan(8, 131072, 32768, d)["kernel"] == 1            # 8 GiB weight, decode
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm_plan(8, (1 << 31) + 1, 64, d)
+    assert e.value.status == tl.TL_EINVAL
+
+
 def test_gemm_plan_padded_weights():
     """N and K that the memory tile does not divide (padded copies, Section
     3.3): ceil-sized grids, same kernels."""
