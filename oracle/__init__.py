@@ -21,6 +21,9 @@ What each function follows (TileLens, arxiv 2607.04031):
   view_offsets   Section 4.3: tile-major byte offsets of the elements of a
                  box of a multi-dimensional view (linear index -> (i, j) ->
                  Eq. 2), in the order a TMA load visits them
+  silu / swiglu_f64 / grouped_swiglu_f64  the gated expert activation of
+                 fused_moe (Sections 2.3 and 6.2): silu(x W_gate^T) * (x W_up^T)
+                 with gate and up stacked in one [2I, K] weight, per group
   fp8_e4m3 / gemm_w8_f64  the FP8 weights the paper's 64 x 64 memory tile
                  holds (Section 3.1): OCP E4M3 decoded by its definition, and
                  the GEMM over them with per-output-channel scales, fp64
@@ -87,6 +90,10 @@ def _load():
     lib.orc_fp8_e4m3.argtypes = [ctypes.c_uint8]
     lib.orc_gemm_w8_f64.restype = None
     lib.orc_gemm_w8_f64.argtypes = [p, p, p, p, i64, i64, i64]
+    lib.orc_silu.restype = ctypes.c_double
+    lib.orc_silu.argtypes = [ctypes.c_double]
+    lib.orc_swiglu_f64.restype = None
+    lib.orc_swiglu_f64.argtypes = [p, p, p, i64, i64, i64]
     lib.orc_view_offsets.restype = i64
     lib.orc_view_offsets.argtypes = [ctypes.c_int, p, p, p, i64, i64, i64, i64, p]
     lib.orc_read_amp.restype = ctypes.c_int
@@ -194,6 +201,37 @@ def grouped_gemm_f64(A_bf16: np.ndarray, token_ids, offsets, W_list) -> np.ndarr
         rows = np.arange(r0, r1) if token_ids is None else np.asarray(token_ids[r0:r1], dtype=np.int64)
         Y[r0:r1] = gemm_f64(A_bf16[rows], W)
     return Y
+
+
+def silu(x: float) -> float:
+    return _load().orc_silu(float(x))
+
+
+def swiglu_f64(A_bf16: np.ndarray, W_bf16: np.ndarray) -> np.ndarray:
+    """A: uint16 bf16 bits [M,K]; W: [2I,K] (gate rows then up rows) -> fp64 [M,I]."""
+    A = np.ascontiguousarray(A_bf16, dtype=np.uint16)
+    W = np.ascontiguousarray(W_bf16, dtype=np.uint16)
+    M, K = A.shape
+    I2, K2 = W.shape
+    assert K == K2 and I2 % 2 == 0
+    H = np.empty((M, I2 // 2), dtype=np.float64)
+    _load().orc_swiglu_f64(_ptr(A), _ptr(W), _ptr(H), M, I2 // 2, K)
+    return H
+
+
+def grouped_swiglu_f64(A_bf16: np.ndarray, token_ids, offsets, W_list) -> np.ndarray:
+    """Rows [offsets[e], offsets[e+1]) are swiglu_f64(A[token_ids[r]], W_list[e]) (token_ids None: A[r])."""
+    offsets = [int(x) for x in offsets]
+    assert len(offsets) == len(W_list) + 1 and offsets[0] == 0
+    I = W_list[0].shape[0] // 2
+    H = np.zeros((offsets[-1], I), dtype=np.float64)
+    for e, W in enumerate(W_list):
+        r0, r1 = offsets[e], offsets[e + 1]
+        if r1 <= r0:
+            continue
+        rows = np.arange(r0, r1) if token_ids is None else np.asarray(token_ids[r0:r1], dtype=np.int64)
+        H[r0:r1] = swiglu_f64(A_bf16[rows], W)
+    return H
 
 
 def fp8_e4m3(v: int) -> float:

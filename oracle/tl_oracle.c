@@ -179,6 +179,31 @@ void orc_gemm_w8_f64(const uint16_t* A, const uint8_t* W8, const double* scale, 
     }
 }
 
+/* SiLU (swish with beta = 1): silu(x) = x / (1 + e^-x). */
+double orc_silu(double x) { return x / (1.0 + exp(-x)); }
+
+/* Gated expert activation of a mixture-of-experts layer (the fused_moe
+ * convention of the paper's main workload, Sections 2.3 and 6.2): with the
+ * expert's gate and up projections stacked as W[2I][K] (rows [0, I) gate,
+ * [I, 2I) up), H[m][i] = silu(sum_k A[m][k] W[i][k]) * sum_k A[m][k] W[I+i][k];
+ * each sum in fp64, k ascending. */
+void orc_swiglu_f64(const uint16_t* A, const uint16_t* W, double* H, int64_t M, int64_t I, int64_t K) {
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < I; ++i) {
+        const uint16_t* wg = W + i * K;
+        const uint16_t* wu = W + (I + i) * K;
+        for (int64_t m = 0; m < M; ++m) {
+            const uint16_t* a = A + m * K;
+            double g = 0.0, u = 0.0;
+            for (int64_t k = 0; k < K; ++k) {
+                g += orc_bf16_to_f64(a[k]) * orc_bf16_to_f64(wg[k]);
+                u += orc_bf16_to_f64(a[k]) * orc_bf16_to_f64(wu[k]);
+            }
+            H[m * I + i] = orc_silu(g) * u;
+        }
+    }
+}
+
 void orc_gemm_f64_points(const uint16_t* A, const uint16_t* W,
                          const int64_t* ms, const int64_t* ns, double* y,
                          int64_t count, int64_t K) {

@@ -331,6 +331,40 @@ def test_moe_routing_tables():
         assert all(e in routing[t] for t in g.tolist())
 
 
+def test_silu_values():
+    """silu(x) = x * sigmoid(x): closed-form points and limits."""
+    assert oracle.silu(0.0) == 0.0
+    assert oracle.silu(1.0) == pytest.approx(1.0 / (1.0 + math.exp(-1.0)), rel=1e-15)
+    assert oracle.silu(-1.0) == pytest.approx(-1.0 / (1.0 + math.e), rel=1e-15)
+    assert oracle.silu(40.0) == pytest.approx(40.0, rel=1e-15)      # sigmoid -> 1
+    assert abs(oracle.silu(-40.0)) < 1e-15                            # sigmoid -> 0
+    for x in np.linspace(-6, 6, 25):                                  # silu(x) - silu(-x) = x
+        assert oracle.silu(x) - oracle.silu(-x) == pytest.approx(x, abs=1e-14)
+
+
+def test_swiglu_equals_gemm_halves_through_numpy():
+    """The gated activation against the plain GEMM on the stacked weight, split
+    into its gate and up halves and combined with numpy's exp: pins which half
+    is the gate and that rows are not shifted or swapped."""
+    M, I, K = 7, 48, 160
+    A = synth.normal_bf16((M, K), seed=401)
+    W = synth.normal_bf16((2 * I, K), seed=402, sigma=synth.W_SIGMA * 20)
+    Y = oracle.gemm_f64(A, W)
+    g, u = Y[:, :I], Y[:, I:]
+    want = g / (1.0 + np.exp(-g)) * u
+    got = oracle.swiglu_f64(A, W)
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-14)
+    assert not np.allclose(got, u / (1.0 + np.exp(-u)) * g)          # gate/up not interchangeable
+    # grouped: each group's rows use its own weight
+    Ws = [W, synth.normal_bf16((2 * I, K), seed=403, sigma=synth.W_SIGMA * 20)]
+    offs = [0, 3, 3, 7]
+    Ws3 = [Ws[0], Ws[1], Ws[1]]
+    ids = np.array([6, 0, 2, 1, 1, 5, 4])
+    Hg = oracle.grouped_swiglu_f64(A, ids, offs, Ws3)
+    assert np.allclose(Hg[0:3], oracle.swiglu_f64(A[ids[0:3]], Ws[0]), rtol=1e-15)
+    assert np.allclose(Hg[3:7], oracle.swiglu_f64(A[ids[3:7]], Ws[1]), rtol=1e-15)
+
+
 def test_fp8_e4m3_decode_against_torch_and_special_values():
     """The oracle's E4M3 decode (written from the format) equals torch's
     float8_e4m3fn for all 256 bytes; spot values of the format."""
