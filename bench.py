@@ -222,10 +222,12 @@ def prefill_layer(ctx, weights):
 def moe_layer(ctx, steps, warmup):
     """Qwen-3-30B-A3B-shaped layer at 64 tokens: attention q, k, v, o at M = 64
     and, for every expert the seeded top-8 routing touches, its gate+up and
-    down GEMMs at that expert's token count; tile-major weights.  Timed three
-    ways: one tl_gemm per GEMM (eager, and replayed as one HIP graph), and
-    the experts as two tl_gemm_grouped launches (gate+up over all experts,
-    then down) beside the four attention calls."""
+    down GEMMs at that expert's token count; tile-major weights.  Timed four
+    ways: one tl_gemm per GEMM (eager, and replayed as one HIP graph), the
+    experts as two tl_gemm_grouped launches (gate+up over all experts, then
+    down) beside the four attention calls, and the fused expert path: gate+up
+    with the gated activation (tl_gemm_grouped_swiglu, bf16 out) feeding the
+    grouped down projection."""
     tl, torch, synth, np = ctx.tl, ctx.torch, ctx.synth, ctx.np
     d = tl.layout(G=G, block_rows=BR)
     Mt, H, E = synth.QWEN_TOKENS, synth.QWEN_HIDDEN, synth.QWEN_EXPERTS
@@ -269,6 +271,9 @@ def moe_layer(ctx, steps, warmup):
     d_ids, d_off = (torch.from_numpy(x).to(ctx.dev) for x in (ids, offsets))
     C_gu = torch.empty((total, Ngu), dtype=torch.float32, device=ctx.dev)
     C_d = torch.empty((total, Nd), dtype=torch.float32, device=ctx.dev)
+    I_act = Ngu // 2                          # gate rows [0, I), up rows [I, 2I) of each gate+up weight
+    H_act = torch.empty((total, I_act), dtype=torch.bfloat16, device=ctx.dev)
+    d_bf = tl.layout(G=G, block_rows=BR, out_dtype=tl.TL_OUT_BF16)
     torch.cuda.synchronize()
     calls = attn + per_expert
     step_bytes = sum(launch_bytes(M, N, K) for (_, _, _, M, N, K) in calls)
@@ -286,13 +291,27 @@ def moe_layer(ctx, steps, warmup):
         tl.tl_gemm_grouped(down_in, total, None, d_off, E, total, max_rows, d_stack, Nd * Kd * 2, C_d,
                            Nd, Kd, d, tl.TL_FETCH_BLOCK)
 
+    def step_fused():
+        for (A, W, C, M, N, K) in attn:
+            tl.tl_gemm(A, W, C, M, N, K, d, tl.TL_FETCH_BLOCK)
+        tl.tl_gemm_grouped_swiglu(hidden, Mt, d_ids, d_off, E, total, max_rows, gu_stack, Ngu * Kgu * 2, H_act,
+                                  I_act, Kgu, d_bf, tl.TL_FETCH_BLOCK)
+        tl.tl_gemm_grouped(H_act, total, None, d_off, E, total, max_rows, d_stack, Nd * Kd * 2, C_d,
+                           Nd, Kd, d, tl.TL_FETCH_BLOCK)
+
+    # bytes of the fused step: the same weights, the activation written once in bf16 and read by down
+    fused_bytes = (sum(launch_bytes(M, N, K) for (_, _, _, M, N, K) in attn)
+                   + touched * 2 * (Ngu * Kgu + Nd * Kd) + 2 * total * Kgu + 2 * total * I_act
+                   + 2 * total * I_act + 4 * total * Nd)
     res = {"tokens": Mt, "experts_touched": touched, "expert_rows": total, "weight_bytes": wbytes,
            "step_bytes": step_bytes}
-    for name, fn in (("per_expert_eager", step_per_expert), ("grouped_eager", step_grouped)):
+    for name, fn, byts in (("per_expert_eager", step_per_expert, step_bytes),
+                           ("grouped_eager", step_grouped, step_bytes),
+                           ("grouped_swiglu_fused_eager", step_fused, fused_bytes)):
         for _ in range(warmup):
             fn()
         wall = wall_time(ctx, fn, steps)
-        res[name] = {"GB/s": round(step_bytes * steps / wall / 1e9, 1), "ms_per_layer": round(wall * 1e3 / steps, 4)}
+        res[name] = {"GB/s": round(byts * steps / wall / 1e9, 1), "ms_per_layer": round(wall * 1e3 / steps, 4)}
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=ctx.stream):
         step_per_expert()
@@ -302,7 +321,7 @@ def moe_layer(ctx, steps, warmup):
     res["per_expert_graph"] = {"GB/s": round(step_bytes * steps / wall / 1e9, 1),
                                "ms_per_layer": round(wall * 1e3 / steps, 4)}
     # the grouped launches alone, event-timed (the experts' share of the layer)
-    ev = ctx.event_pairs(2)
+    ev = ctx.event_pairs(3)
     ev[0][0].record(ctx.stream)
     for _ in range(steps):
         tl.tl_gemm_grouped(hidden, Mt, d_ids, d_off, E, total, max_rows, gu_stack, Ngu * Kgu * 2, C_gu,
@@ -313,7 +332,15 @@ def moe_layer(ctx, steps, warmup):
         tl.tl_gemm_grouped(down_in, total, None, d_off, E, total, max_rows, d_stack, Nd * Kd * 2, C_d,
                            Nd, Kd, d, tl.TL_FETCH_BLOCK)
     ev[1][1].record(ctx.stream)
+    ev[2][0].record(ctx.stream)
+    for _ in range(steps):
+        tl.tl_gemm_grouped_swiglu(hidden, Mt, d_ids, d_off, E, total, max_rows, gu_stack, Ngu * Kgu * 2, H_act,
+                                  I_act, Kgu, d_bf, tl.TL_FETCH_BLOCK)
+    ev[2][1].record(ctx.stream)
     torch.cuda.synchronize()
+    us = ev[2][0].elapsed_time(ev[2][1]) * 1e3 / steps
+    byts = touched * 2 * Ngu * Kgu + 2 * total * Kgu + 2 * total * I_act
+    res["grouped_gate_up_swiglu_launch"] = {"us": round(us, 2), "GB/s": round(byts / (us * 1e-6) / 1e9, 1)}
     for j, (name, N, K) in enumerate((("gate_up", Ngu, Kgu), ("down", Nd, Kd))):
         us = ev[j][0].elapsed_time(ev[j][1]) * 1e3 / steps
         byts = touched * 2 * N * K + 2 * total * K + 4 * total * N   # as the per-expert calls count it

@@ -256,6 +256,30 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
                     void* stream);
 
 /*
+ * tl_gemm_grouped_swiglu -- the gated expert activation of a mixture-of-experts
+ * layer fused into the grouped gate+up projection (the paper's fused_moe
+ * workload, Sections 2.3 and 6.2).  Every group's weight W_e stacks its gate
+ * projection (rows [0, I)) and its up projection (rows [I, 2I)) as one
+ * [2I][K] matrix (tile-major: repacked as one matrix of 2I rows), and
+ *      H[r][i] = silu(sum_k A[t][k] * W_e[i][k]) * sum_k A[t][k] * W_e[I + i][k]
+ * for rows r of group e as in tl_gemm_grouped (t = token_ids[r] or r), with
+ * silu(x) = x / (1 + e^-x) evaluated in fp32 on the fp32 sums.  H: device
+ * [total_rows][I] row-major, fp32 or bf16 per layout->out_dtype.  Every
+ * workgroup reads 32 gate rows and the 32 matching up rows -- whole memory
+ * tiles when block_rows divides 32 -- so the [total_rows][2I] projection is
+ * never written.  Arguments, ownership and errors as tl_gemm_grouped with
+ * N = I for C and 2I weight rows (group_stride >= the bytes of a [2I][K]
+ * weight: tl_tile_bytes(2I, K, ...) for tile-major); in addition
+ * TL_EUNSUPPORTED for I % 32 != 0 or a tile-major block_rows that does not
+ * divide 32, TL_EINVAL for I > 2^30.
+ */
+int tl_gemm_grouped_swiglu(const void* A, int64_t a_rows, const int32_t* token_ids,
+                           const int32_t* group_offsets, int32_t num_groups, int64_t total_rows,
+                           int64_t max_group_rows, const void* W_gate_up, int64_t group_stride, void* H,
+                           int64_t I, int64_t K, const tl_layout_desc* layout, int32_t fetch_mode,
+                           void* stream);
+
+/*
  * tl_read_amp -- host only, exact integer count of the bytes a tiled GEMM
  * fetches at granularity G (Sections 1, 2.5; the per-tile request counts of
  * Section 6.4).  Model: the grid has ceil(M/tile_m) x ceil(N/tile_n) tiles,

@@ -10,6 +10,7 @@ the C names and argument order of ``include/tl.h``:
     tl_unpack(src_tm, dst, rows, cols, elem_bytes, G, block_rows, stream=None)
     tl_gemm(A, W, C, M, N, K, layout, fetch_mode, stream=None)
     tl_gemm_plan(M, N, K, layout, fetch_mode) -> dict
+    tl_gemm_grouped / tl_gemm_grouped_swiglu (..., layout, fetch_mode, stream=None)
     tl_read_amp(M, N, K, tile_m, tile_n, tile_k, layout, G) -> dict
     tl_fetch_counter_read(stream=None) -> int
     tl_release()
@@ -36,7 +37,7 @@ TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE = 0, 1, 2
 TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
-EXPORTED = ("tl_tile_bytes", "tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_read_amp",
+EXPORTED = ("tl_tile_bytes", "tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_gemm_grouped_swiglu", "tl_read_amp",
             "tl_view_offsets", "tl_view_load", "tl_prefetch_degree", "tl_gemm_lgms", "tl_lgms_occupancy",
             "tl_fetch_counter_read", "tl_release", "tl_strerror")
 TL_VIEW_MAX_RANK = 5
@@ -131,6 +132,9 @@ def load_library():
     lib.tl_gemm_grouped.restype = ctypes.c_int
     lib.tl_gemm_grouped.argtypes = [p, i64, p, p, i32, i64, i64, p, i64, p, i64, i64,
                                     ctypes.POINTER(LayoutDesc), i32, p]
+    lib.tl_gemm_grouped_swiglu.restype = ctypes.c_int
+    lib.tl_gemm_grouped_swiglu.argtypes = [p, i64, p, p, i32, i64, i64, p, i64, p, i64, i64,
+                                           ctypes.POINTER(LayoutDesc), i32, p]
     lib.tl_prefetch_degree.restype = ctypes.c_int
     lib.tl_prefetch_degree.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, i64, ctypes.c_double,
                                        ctypes.POINTER(i64)]
@@ -241,6 +245,16 @@ def tl_gemm_grouped(A, a_rows, token_ids, group_offsets, num_groups, total_rows,
     _check(load_library().tl_gemm_grouped(_ptr(A), a_rows, _ptr(token_ids), _ptr(group_offsets), num_groups,
                                           total_rows, max_group_rows, _ptr(W), group_stride, _ptr(C), N, K,
                                           ctypes.byref(d), fetch_mode, _stream(stream)), "tl_gemm_grouped")
+
+
+def tl_gemm_grouped_swiglu(A, a_rows, token_ids, group_offsets, num_groups, total_rows, max_group_rows, W_gate_up,
+                           group_stride, H, I, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):
+    """H [total_rows, I] = silu(A W_gate^T) * (A W_up^T) per group; W_gate_up stacks [2I, K] per group."""
+    d = _desc(layout)
+    _check(load_library().tl_gemm_grouped_swiglu(_ptr(A), a_rows, _ptr(token_ids), _ptr(group_offsets), num_groups,
+                                                 total_rows, max_group_rows, _ptr(W_gate_up), group_stride, _ptr(H),
+                                                 I, K, ctypes.byref(d), fetch_mode, _stream(stream)),
+           "tl_gemm_grouped_swiglu")
 
 
 def tl_prefetch_degree(bandwidth, latency, bytes_per_iteration, k_iterations, collision_factor=1.0) -> int:

@@ -393,22 +393,32 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
     return e == hipSuccess ? TL_OK : TL_EHIP;
 }
 
-int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, const int32_t* group_offsets,
-                    int32_t num_groups, int64_t total_rows, int64_t max_group_rows, const void* W,
-                    int64_t group_stride, void* C, int64_t N, int64_t K, const tl_layout_desc* layout,
-                    int32_t fetch_mode, void* stream) {
+// One grouped launch.  swiglu: every weight stacks gate rows [0, N) and up
+// rows [N, 2N) and C receives silu(gate) * up, N columns.
+static int grouped_impl(const void* A, int64_t a_rows, const int32_t* token_ids, const int32_t* group_offsets,
+                        int32_t num_groups, int64_t total_rows, int64_t max_group_rows, const void* W,
+                        int64_t group_stride, void* C, int64_t N, int64_t K, const tl_layout_desc* layout,
+                        int32_t fetch_mode, void* stream, bool swiglu) {
     Plan p;
-    int rc = plan_grouped(max_group_rows, N, K, layout, fetch_mode, &p);
+    if (swiglu && N > (int64_t(1) << 30)) return TL_EINVAL;
+    const int64_t w_rows = swiglu ? 2 * N : N;
+    int rc = plan_grouped(max_group_rows, w_rows, K, layout, fetch_mode, &p);
     if (rc != TL_OK) return rc;
+    if (swiglu) {
+        // a tile is 32 gate rows + the 32 matching up rows: whole memory-tile
+        // strips when block_rows divides 32
+        if (N % 32 || (layout->kind == TL_LAYOUT_TILE && 32 % p.L.br)) return TL_EUNSUPPORTED;
+        p.pub.tile_n = 64;
+    }
     if (num_groups < 1 || total_rows < 0 || a_rows < 1) return TL_EINVAL;
     if (total_rows >= (int64_t(1) << 31) || a_rows >= (int64_t(1) << 31)) return TL_EINVAL;
     if (!token_ids && a_rows < total_rows) return TL_EINVAL;
-    const int64_t one_w = layout->kind == TL_LAYOUT_TILE ? packed_bytes(p.L, N, K) : N * K * 2;
+    const int64_t one_w = layout->kind == TL_LAYOUT_TILE ? packed_bytes(p.L, w_rows, K) : w_rows * K * 2;
     if (group_stride < one_w || group_stride % 16) return TL_EINVAL;
     if (!A || !W || !C || !group_offsets || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(group_offsets) & 3u) || (reinterpret_cast<uintptr_t>(token_ids) & 3u))
         return TL_EINVAL;
-    const int64_t tiles = (N + p.pub.tile_n - 1) / p.pub.tile_n;
+    const int64_t tiles = swiglu ? N / 32 : (N + p.pub.tile_n - 1) / p.pub.tile_n;
     if (int64_t(num_groups) * tiles >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;
     if (total_rows == 0) return TL_OK;
     const int64_t c_bytes = total_rows * N * (p.out_bf16 ? 2 : 4);
@@ -443,7 +453,24 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, con
     d.group_stride = group_stride;
     d.a_rows = a_rows;
     d.total_rows = total_rows;
+    d.swiglu = swiglu;
     return launch_decode(d, s) == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids, const int32_t* group_offsets,
+                    int32_t num_groups, int64_t total_rows, int64_t max_group_rows, const void* W,
+                    int64_t group_stride, void* C, int64_t N, int64_t K, const tl_layout_desc* layout,
+                    int32_t fetch_mode, void* stream) {
+    return grouped_impl(A, a_rows, token_ids, group_offsets, num_groups, total_rows, max_group_rows, W, group_stride,
+                        C, N, K, layout, fetch_mode, stream, false);
+}
+
+int tl_gemm_grouped_swiglu(const void* A, int64_t a_rows, const int32_t* token_ids, const int32_t* group_offsets,
+                           int32_t num_groups, int64_t total_rows, int64_t max_group_rows, const void* W_gate_up,
+                           int64_t group_stride, void* H, int64_t I, int64_t K, const tl_layout_desc* layout,
+                           int32_t fetch_mode, void* stream) {
+    return grouped_impl(A, a_rows, token_ids, group_offsets, num_groups, total_rows, max_group_rows, W_gate_up,
+                        group_stride, H, I, K, layout, fetch_mode, stream, true);
 }
 
 int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,

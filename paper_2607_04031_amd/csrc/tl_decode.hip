@@ -55,8 +55,16 @@ namespace {
 // clamped to [0, total_rows]; row r reads A row token_ids[r] (or r), and an
 // id outside [0, a_rows) reads zeros.  Rows are processed in chunks of
 // 16 MT, each chunk streaming the tile's weights again.
-template <int MT, int NS, int U, int WAVES, bool TILE, bool BLOCKROW, bool GROUPED>
+//
+// Gated expert activation (SWIGLU, grouped, NS = 4): each group's weight
+// stacks its gate projection (rows [0, I)) and up projection (rows [I, 2I)),
+// the fused_moe convention.  Workgroup tile t takes gate rows [32 t, 32 t + 32)
+// as subtiles 0-1 and the up rows I + [32 t, 32 t + 32) as subtiles 2-3 --
+// two whole 32-row strips -- and writes C[r][32 t + c] = silu(g) * u for its
+// 32 columns (C has I columns).
+template <int MT, int NS, int U, int WAVES, bool TILE, bool BLOCKROW, bool GROUPED, bool SWIGLU = false>
 __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
+    static_assert(!SWIGLU || (GROUPED && NS == 4), "gated launches are grouped, 32 gate + 32 up rows");
     constexpr int kWaves = WAVES;
     constexpr int kThreads = 64 * WAVES;
     constexpr int TN = 16 * NS;
@@ -87,7 +95,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     const int st1 = min(u1 * p.steps_per_unit, p.ksteps);
     const int st1f = min(st1, p.kfull);
 
-    const int n_base = tile * TN;
+    const int n_base = SWIGLU ? tile * 32 : tile * TN;   // first output column of the tile
     const int g = lane >> 4, q = lane & 15;
     const bool lo = q < 8;
     const int kc = (((q >> 3) << 2) + g) << 3;   // k offset of this lane's weight chunk in a step
@@ -97,7 +105,9 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     for (int j = 0; j < NS; ++j)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
-            const int n = min(n_base + j * 16 + hf * 8 + (q & 7), p.N - 1);
+            int n;
+            if constexpr (SWIGLU) n = (j < 2 ? n_base + j * 16 : p.swiglu_up + n_base + (j - 2) * 16) + hf * 8 + (q & 7);
+            else n = min(n_base + j * 16 + hf * 8 + (q & 7), p.N - 1);
             int64_t off;
             if (TILE) off = int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << (p.log2_bc + 1));
             else off = int64_t(n) * p.K * 2;
@@ -277,6 +287,29 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     constexpr int kEntries = MT * NS * 64;   // f32x4 entries per wave
     const bool final_out = p.split_k == 1;
     float* part = p.ws + int64_t(split) * p.ws_stride;
+    if constexpr (SWIGLU) {
+        // subtile j (gate) pairs with subtile j + 2 (up) of the same columns
+        for (int e = threadIdx.x; e < MT * 2 * 64; e += kThreads) {
+            const int mt = e / 128;
+            const int j = (e / 64) % 2;
+            const int l = e % 64;
+            f32x4 vg = red[0][mt][j][l], vu = red[0][mt][j + 2][l];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) {
+                vg += red[w][mt][j][l];
+                vu += red[w][mt][j + 2][l];
+            }
+            const int n = n_base + j * 16 + (l & 15);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = mt * 16 + (l >> 4) * 4 + r;
+                if (m < crows) {
+                    const float h = vg[r] / (1.0f + expf(-vg[r])) * vu[r];
+                    store_out(p.C, int64_t(row0 + mc + m) * p.N + n, h, p.out_bf16);
+                }
+            }
+        }
+    } else
     for (int e = threadIdx.x; e < kEntries; e += kThreads) {
         const int mt = e / (NS * 64);
         const int j = (e / 64) % NS;
@@ -335,7 +368,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, voi
     }
 }
 
-template <int MT, int NS, int WAVES, bool TILE, bool GROUPED>
+template <int MT, int NS, int WAVES, bool TILE, bool GROUPED, bool SWIGLU = false>
 hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
     constexpr int U = MT >= 2 ? 2 : 4;   // steps in flight per wave; fewer for larger M (registers)
     if constexpr (!TILE && !GROUPED) {
@@ -345,7 +378,7 @@ hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
             return hipGetLastError();
         }
     }
-    hipLaunchKernelGGL((decode_kernel<MT, NS, U, WAVES, TILE, false, GROUPED>), dim3(grid), dim3(64 * WAVES), 0,
+    hipLaunchKernelGGL((decode_kernel<MT, NS, U, WAVES, TILE, false, GROUPED, SWIGLU>), dim3(grid), dim3(64 * WAVES), 0,
                        stream, p);
     return hipGetLastError();
 }
@@ -355,6 +388,9 @@ hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
 // launches use 4 waves.
 template <int MT, int NS, bool TILE>
 hipError_t launch_w(const DecodeParams& p, int grid, int waves, bool grouped, hipStream_t stream) {
+    if constexpr (NS == 4) {
+        if (grouped && p.swiglu_up > 0) return launch_t<MT, 4, 4, TILE, true, true>(p, grid, stream);
+    }
     if (grouped) return launch_t<MT, NS, 4, TILE, true>(p, grid, stream);
     if constexpr (MT * NS <= 2) {
         if (waves == 16) return launch_t<MT, NS, 16, TILE, false>(p, grid, stream);
@@ -403,7 +439,8 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.w_bytes = d.N * d.K * elem;
     p.offsets = d.group_offsets;
     p.token_ids = d.token_ids;
-    p.tiles_per_group = int((d.N + d.tile_n - 1) / d.tile_n);
+    p.tiles_per_group = d.swiglu ? int(d.N / 32) : int((d.N + d.tile_n - 1) / d.tile_n);
+    p.swiglu_up = d.swiglu ? int(d.N) : 0;
     p.group_stride = d.group_stride;
     p.a_rows = int(d.a_rows);
     p.total_rows = int(d.total_rows);

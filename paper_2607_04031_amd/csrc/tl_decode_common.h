@@ -41,6 +41,7 @@ struct DecodeParams {
     int a_rows;              // rows of A; token ids outside [0, a_rows) read zeros
     int total_rows;          // rows of C; group offsets are clamped to [0, total_rows]
     const float* scales;     // FP8 weights: per-output-channel scale [N], or nullptr (1)
+    int swiglu_up;           // gated grouped launch: row of the first up row (I); C has N = I columns
 };
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {

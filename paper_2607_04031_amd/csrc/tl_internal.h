@@ -73,6 +73,9 @@ struct DecodeLaunch {
     int64_t group_stride = 0;
     int64_t a_rows = 0;
     int64_t total_rows = 0;
+    // gated expert activation (grouped only): W_e stacks gate rows [0, N) and
+    // up rows [N, 2N); C[r][n] = silu(gate) * up, N columns; tile_n = 64
+    bool swiglu = false;
     // FP8 (E4M3) weight, bf16 activations; optional per-output-channel scales [N]
     bool fp8 = false;
     const float* scales = nullptr;

@@ -9,7 +9,7 @@ import pytest
 import oracle
 import paper_2607_04031_amd as tl
 from paper_2607_04031_amd import synth
-from tests._gpu import banner, dev_bf16, host_f32, parity
+from tests._gpu import banner, dev_bf16, host_bits, host_f32, parity, parity_bf16_out
 
 pytestmark = pytest.mark.gpu
 
@@ -196,3 +196,121 @@ def test_grouped_graph_replay():
             side.synchronize()
             assert torch.equal(C, eager), f"replay {rep}"
     parity(host_f32(eager), oracle.grouped_gemm_f64(A, ids, offsets, Ws), "graph")
+
+
+# ---------------------------------------------------------------------------
+# Gated expert activation fused into the gate+up projection
+# ---------------------------------------------------------------------------
+
+def run_swiglu(A_bits, ids, offsets, Ws, max_rows, desc=None, fetch=tl.TL_FETCH_BLOCK, stack=None):
+    """Ws: stacked [2I, K] gate+up weights per group -> H [T, I] from tl_gemm_grouped_swiglu."""
+    import torch
+    desc = desc or tl.layout()
+    E = len(Ws)
+    I2, K = Ws[0].shape
+    I = I2 // 2
+    T = int(offsets[-1])
+    stride = tl.tl_tile_bytes(I2, K, 2, desc.G, desc.block_rows) if desc.kind == tl.TL_LAYOUT_TILE else I2 * K * 2
+    if stack is None:
+        stack = torch.empty((E * stride // 2,), dtype=torch.bfloat16, device="cuda")
+        for e, W in enumerate(Ws):
+            seg = stack[e * stride // 2:(e + 1) * stride // 2]
+            if desc.kind == tl.TL_LAYOUT_TILE:
+                tl.tl_repack(dev_bf16(W), seg, I2, K, 2, desc.G, desc.block_rows)
+            else:
+                seg.copy_(dev_bf16(W).view(-1))
+    out_dt = torch.bfloat16 if desc.out_dtype == tl.TL_OUT_BF16 else torch.float32
+    H = torch.full((max(T, 1), I), float("nan"), dtype=out_dt, device="cuda")
+    d_ids = None if ids is None else dev_i32(ids)
+    tl.tl_gemm_grouped_swiglu(dev_bf16(A_bits), A_bits.shape[0], d_ids, dev_i32(offsets), E, T, max_rows, stack,
+                              stride, H, I, K, desc, fetch)
+    torch.cuda.synchronize()
+    return H[:T]
+
+
+def test_swiglu_qwen_moe_experts_full():
+    """All 128 Qwen experts' gate+up [1536, 2048] as gate [768] + up [768]:
+    the fused activation of every routed row against the oracle."""
+    routing = synth.moe_routing()
+    offsets, ids = synth.moe_tables(routing)
+    max_rows = int(np.diff(offsets).max())
+    N2, K = synth.QWEN_GATE_UP
+    A = synth.normal_bf16((synth.QWEN_TOKENS, K), seed=synth.QWEN_SEED_HIDDEN)
+    Ws = [synth.normal_bf16((N2, K), seed=synth.qwen_gate_up_seed(e), sigma=synth.W_SIGMA)
+          for e in range(synth.QWEN_EXPERTS)]
+    banner(f"grouped swiglu qwen: E=128 rows={offsets[-1]} I={N2 // 2} K={K}")
+    H = run_swiglu(A, ids, offsets, Ws, max_rows)
+    parity(host_f32(H), oracle.grouped_swiglu_f64(A, ids, offsets, Ws), "swiglu qwen")
+    Hb = run_swiglu(A, ids, offsets, Ws, max_rows, desc=tl.layout(out_dtype=tl.TL_OUT_BF16))
+    parity_bf16_out(host_bits(Hb), oracle.grouped_swiglu_f64(A, ids, offsets, Ws), "swiglu qwen bf16")
+
+
+@pytest.mark.parametrize("max_rows", [16, 64])
+@pytest.mark.parametrize("G,br", [(4096, 32), (4096, 16), (1024, 8)])
+def test_swiglu_edge_groups_and_memory_tiles(max_rows, G, br):
+    """Empty groups, a 40-row group (passes of the M tile), repeated ids,
+    memory tiles of 32, 16 and 8 rows, a K that is not a multiple of 64."""
+    I, K = 96, 520
+    counts = [0, 3, 40, 0, 1, 17, 0]
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    T = int(offsets[-1])
+    ids = np.random.default_rng(9).integers(0, 24, size=T).astype(np.int32)
+    A = synth.normal_bf16((24, K), seed=10)
+    Ws = [synth.normal_bf16((2 * I, K), seed=120 + e, sigma=synth.W_SIGMA * 10) for e in range(len(counts))]
+    banner(f"grouped swiglu edges max_rows={max_rows} G={G} br={br}")
+    H = run_swiglu(A, ids, offsets, Ws, max_rows, desc=tl.layout(G=G, block_rows=br))
+    parity(host_f32(H), oracle.grouped_swiglu_f64(A, ids, offsets, Ws), f"swiglu G={G} br={br}")
+
+
+def test_swiglu_row_major_and_rejections():
+    import torch
+    I, K = 64, 256
+    counts = [2, 5, 0, 3]
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    T = int(offsets[-1])
+    A = synth.normal_bf16((T, K), seed=16)
+    Ws = [synth.normal_bf16((2 * I, K), seed=130 + e, sigma=synth.W_SIGMA * 10) for e in range(len(counts))]
+    banner("grouped swiglu row-major")
+    H = run_swiglu(A, None, offsets, Ws, 8, desc=tl.layout(kind=tl.TL_LAYOUT_NK_ROW), fetch=tl.TL_FETCH_NATIVE)
+    parity(host_f32(H), oracle.grouped_swiglu_f64(A, None, offsets, Ws), "swiglu row-major")
+    stack = torch.zeros((4, 2 * 64, K), dtype=torch.bfloat16, device="cuda")   # as large as the calls describe
+    Hs = torch.zeros((T, 64), dtype=torch.float32, device="cuda")
+    for kw, status in ((dict(I=48), tl.TL_EUNSUPPORTED),                               # I % 32
+                       (dict(desc=tl.layout(block_rows=64)), tl.TL_EUNSUPPORTED)):     # 64-row memory tiles
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_grouped_swiglu(dev_bf16(A), T, None, dev_i32(offsets), 4, T, 8, stack, 2 * 64 * K * 2, Hs,
+                                      kw.get("I", 64), K, kw.get("desc", tl.layout()), tl.TL_FETCH_BLOCK)
+        assert e.value.status == status
+
+
+def test_swiglu_graph_replay():
+    import torch
+    I, K = 128, 1024
+    routing = synth.moe_routing(M=16, E=8, topk=2, seed=4)
+    offsets, ids = synth.moe_tables(routing, E=8)
+    T = int(offsets[-1])
+    A = synth.normal_bf16((16, K), seed=17)
+    Ws = [synth.normal_bf16((2 * I, K), seed=140 + e, sigma=synth.W_SIGMA) for e in range(8)]
+    banner("grouped swiglu graph replay")
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        stack = torch.empty((8, 2 * I, K), dtype=torch.bfloat16, device="cuda")
+        for e, W in enumerate(Ws):
+            tl.tl_repack(dev_bf16(W), stack[e], 2 * I, K, 2, 4096, 32)
+        dA, dids, doff = dev_bf16(A), dev_i32(ids), dev_i32(offsets)
+        H = torch.zeros((T, I), dtype=torch.float32, device="cuda")
+        args = (dA, 16, dids, doff, 8, T, int(np.diff(offsets).max()), stack, 2 * I * K * 2, H, I, K, tl.layout(),
+                tl.TL_FETCH_BLOCK)
+        tl.tl_gemm_grouped_swiglu(*args)
+        side.synchronize()
+        eager = H.clone()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            tl.tl_gemm_grouped_swiglu(*args)
+        for rep in range(4):
+            H.fill_(float("nan"))
+            side.synchronize()
+            g.replay()
+            side.synchronize()
+            assert torch.equal(H, eager), f"replay {rep}"
+    parity(host_f32(eager), oracle.grouped_swiglu_f64(A, ids, offsets, Ws), "swiglu graph")
