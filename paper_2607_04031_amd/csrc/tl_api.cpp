@@ -195,7 +195,11 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         const int64_t n_tiles = (N + tn - 1) / tn;
         const int64_t units = (K + p.k_unit - 1) / p.k_unit;
         // Balance: every CU should stream the same number of bytes.
-        //  - at least two tiles per CU: one workgroup per tile, K not split;
+        //  - at least two tiles per CU: one workgroup per tile, K not split
+        //    -- except between two and four rounds of the CUs that do not
+        //    come out even (896 tiles: 3.5 per CU), where two K splits even
+        //    them out if their fp32 partials (written and read back) stay
+        //    within 2 % of the weight bytes (FP8 gate+up at M = 8: -9 %);
         //  - tiles that divide the CUs or fill them a whole number of times
         //    (N = 8192: 256 tiles of 32 rows, 128 of 64): one workgroup per
         //    CU, whose 8 or 16 waves split K among themselves (reduced in
@@ -211,6 +215,9 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
             const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(units / min_units, kMaxSplitK));
             if (n_tiles >= 2 * kCUs) {
                 S = 1;
+                const int64_t w_bytes = N * K * s;
+                if (n_tiles < 4 * kCUs && n_tiles % kCUs != 0 && max_s >= 2 && 2 * 2 * M * N * 4 * 50 <= w_bytes)
+                    S = 2;
             } else if (kCUs % n_tiles == 0 || n_tiles % kCUs == 0) {
                 S = std::max<int64_t>(1, kCUs / n_tiles);
                 if (K / (4 * S) >= 4096) S *= 4;
