@@ -186,7 +186,10 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * 16 / elem_bytes (one 16-byte load: keeps rows of A 16-byte aligned),
  * block_cols * elem_bytes < 16, a combination of layout, fetch mode and tile
  * that no kernel implements (NK_ROW with BLOCK above 64 rows, with FP8, or
- * with K % 64 or N % 32 != 0; FP8 above 64 rows), or TL_LAYOUT_KN_ROW.
+ * with K % 64 or N % 32 != 0; FP8 above 64 rows), TL_LAYOUT_KN_ROW, or sizes
+ * past the kernels' 32-bit byte offsets: for M <= 64, 2 * M * K or the bytes
+ * of tile_n weight rows (tile_n * K * elem_bytes, K padded for tile-major)
+ * of 2^31 or more; above 64 rows, A or W of 2^32 bytes or more.
  * TL_ENOMEM if the split-K workspace cannot be allocated; TL_EHIP if the
  * launch fails.
  */
@@ -246,8 +249,8 @@ int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout,
  * beyond 2^31 - 1, a short or misaligned group_stride, NULL or misaligned
  * pointers (offsets and ids 4-byte aligned), overlap of C with A or W, or a
  * descriptor tl_gemm rejects with TL_EINVAL; TL_EUNSUPPORTED for split_k > 1,
- * tile_m > 64, and what tl_gemm rejects with TL_EUNSUPPORTED.  total_rows == 0
- * enqueues nothing.
+ * tile_m > 64, a_rows * K * 2 >= 2^31, and what tl_gemm rejects with
+ * TL_EUNSUPPORTED.  total_rows == 0 enqueues nothing.
  */
 int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
                     const int32_t* group_offsets, int32_t num_groups, int64_t total_rows,
@@ -270,8 +273,9 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
  * never written.  Arguments, ownership and errors as tl_gemm_grouped with
  * N = I for C and 2I weight rows (group_stride >= the bytes of a [2I][K]
  * weight: tl_tile_bytes(2I, K, ...) for tile-major); in addition
- * TL_EUNSUPPORTED for I % 32 != 0 or a tile-major block_rows that does not
- * divide 32, TL_EINVAL for I > 2^30.
+ * TL_EUNSUPPORTED for I % 32 != 0, a tile-major block_rows that does not
+ * divide 32, or a [2I][K] weight of 2^31 bytes or more; TL_EINVAL for
+ * I > 2^30.
  */
 int tl_gemm_grouped_swiglu(const void* A, int64_t a_rows, const int32_t* token_ids,
                            const int32_t* group_offsets, int32_t num_groups, int64_t total_rows,

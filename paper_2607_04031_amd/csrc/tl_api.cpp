@@ -227,6 +227,10 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
             }
         }
         if (S < 1 || S > units || S > kMaxSplitK) return TL_EUNSUPPORTED;
+        // the decode kernels address a tile's weight rows and the activations
+        // with 32-bit byte offsets from a uniform base
+        const int64_t kp = tile ? padded_cols(p.L, K) : K;
+        if (int64_t(tn) * kp * s >= (int64_t(1) << 31) || M * K * 2 >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;
         const int64_t wgs = n_tiles * S;
         const int ns = tn / 16;
         int waves = wgs <= kCUs ? 16 : (wgs <= 2 * kCUs ? 8 : 4);
@@ -420,6 +424,11 @@ static int grouped_impl(const void* A, int64_t a_rows, const int32_t* token_ids,
     if (num_groups < 1 || total_rows < 0 || a_rows < 1) return TL_EINVAL;
     if (total_rows >= (int64_t(1) << 31) || a_rows >= (int64_t(1) << 31)) return TL_EINVAL;
     if (!token_ids && a_rows < total_rows) return TL_EINVAL;
+    // 32-bit byte offsets inside the kernel: A, and the rows one tile reads
+    // (gate and up halves together for swiglu)
+    if (a_rows * K * 2 >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;
+    if (swiglu && 2 * N * (layout->kind == TL_LAYOUT_TILE ? padded_cols(p.L, K) : K) * 2 >= (int64_t(1) << 31))
+        return TL_EUNSUPPORTED;
     const int64_t one_w = layout->kind == TL_LAYOUT_TILE ? packed_bytes(p.L, w_rows, K) : w_rows * K * 2;
     if (group_stride < one_w || group_stride % 16) return TL_EINVAL;
     if (!A || !W || !C || !group_offsets || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;

@@ -100,7 +100,14 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     const bool lo = q < 8;
     const int kc = (((q >> 3) << 2) + g) << 3;   // k offset of this lane's weight chunk in a step
 
-    const uint8_t* wrow[NS][2];
+    // Weight addresses: the tile's first row as a uniform 64-bit base (scalar
+    // registers) plus a per-lane 32-bit byte offset -- the rows of one tile
+    // span less than 2^31 bytes (the planner checks it) -- so a load is a
+    // scalar base + 32-bit vector offset and needs no 64-bit vector pointers
+    // (fewer registers: more resident waves).
+    const int64_t tile_off = TILE ? int64_t(n_base >> p.log2_br) * p.strip_bytes : int64_t(n_base) * p.K * 2;
+    const uint8_t* wtile = W + tile_off;
+    uint32_t woff[NS][2];
 #pragma unroll
     for (int j = 0; j < NS; ++j)
 #pragma unroll
@@ -111,7 +118,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
             int64_t off;
             if (TILE) off = int64_t(n >> p.log2_br) * p.strip_bytes + (int64_t(n & ((1 << p.log2_br) - 1)) << (p.log2_bc + 1));
             else off = int64_t(n) * p.K * 2;
-            wrow[j][hf] = W + off;
+            woff[j][hf] = uint32_t(off - tile_off);
         }
     for (int mc = 0;;) {   // row chunks: one pass unless GROUPED
     const int crows = rows - mc;
@@ -119,7 +126,9 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     // instruction, then the lane exchange): lane (g, q) reads row
     // 16 mt + 8 hf + (q & 7) at this lane's chunk kc.  Rows past M read zeros;
     // a half-tile that is entirely past M is not loaded at all.
-    const uint16_t* arow[MT][2];
+    // activation rows: byte offsets from A (A spans less than 2^31 bytes)
+    const uint8_t* Ab = reinterpret_cast<const uint8_t*>(p.A);
+    uint32_t aoff[MT][2];
     bool aok[MT][2], aany[MT][2];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -134,7 +143,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
                 if (aok[mt][hf] && p.token_ids) arow_idx = p.token_ids[arow_idx];
                 aok[mt][hf] = aok[mt][hf] && arow_idx >= 0 && arow_idx < p.a_rows;
             }
-            arow[mt][hf] = p.A + int64_t(aok[mt][hf] ? arow_idx : 0) * p.K + kc;
+            aoff[mt][hf] = uint32_t((aok[mt][hf] ? arow_idx : 0) * p.K + kc) * 2u;
         }
 
     f32x4 acc[MT][NS];
@@ -175,7 +184,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
 #pragma unroll
             for (int hf = 0; hf < 2; ++hf)
                 if (aany[mt][hf])   // uniform: skips the load when the half-tile is past M
-                    xa[mt][hf] = aok[mt][hf] ? *reinterpret_cast<const bf16x8*>(arow[mt][hf] + k) : zero8;
+                    xa[mt][hf] = aok[mt][hf] ? *reinterpret_cast<const bf16x8*>(Ab + (aoff[mt][hf] + uint32_t(k) * 2u)) : zero8;
                 else
                     xa[mt][hf] = zero8;
     };
@@ -214,7 +223,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
 #pragma unroll
             for (int j = 0; j < NS; ++j)
 #pragma unroll
-                for (int hf = 0; hf < 2; ++hf) x[u][j][hf] = load_stream(wrow[j][hf] + ko);
+                for (int hf = 0; hf < 2; ++hf) x[u][j][hf] = load_stream(wtile + (woff[j][hf] + uint32_t(ko)));
             load_a(k, a[u]);
             fetch_blocks(k);
         }
@@ -229,7 +238,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
 #pragma unroll
         for (int j = 0; j < NS; ++j)
 #pragma unroll
-            for (int hf = 0; hf < 2; ++hf) x[j][hf] = load_stream(wrow[j][hf] + ko);
+            for (int hf = 0; hf < 2; ++hf) x[j][hf] = load_stream(wtile + (woff[j][hf] + uint32_t(ko)));
         load_a(k, a);
         fetch_blocks(k);
         compute(x, a);
@@ -248,14 +257,15 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
         for (int j = 0; j < NS; ++j)
 #pragma unroll
             for (int hf = 0; hf < 2; ++hf) {
-                const bf16x8 v = load_stream(wrow[j][hf] + ko);
+                const bf16x8 v = load_stream(wtile + (woff[j][hf] + uint32_t(ko)));
                 x[j][hf] = kin ? v : zero8;
             }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int hf = 0; hf < 2; ++hf) {
-                const bf16x8 v = *reinterpret_cast<const bf16x8*>(kin ? arow[mt][hf] + k : arow[mt][hf] - kc);
+                const bf16x8 v = *reinterpret_cast<const bf16x8*>(Ab + (kin ? aoff[mt][hf] + uint32_t(k) * 2u
+                                                                             : aoff[mt][hf] - uint32_t(kc) * 2u));
                 a[mt][hf] = kin && aok[mt][hf] ? v : zero8;
             }
         compute(x, a);
