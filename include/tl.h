@@ -29,6 +29,12 @@
  *  - Calls are thread-safe.  The library owns, per (device, stream), a split-K
  *    workspace and a fetch counter; concurrent calls on the SAME stream from
  *    several host threads are serialised by the stream, as usual.
+ *  - HIP graphs: the GEMM and repack calls enqueue kernels only (no memset or
+ *    copy nodes) and may be captured, once the stream's library state exists:
+ *    the first call on a stream, and a call that needs a larger split-K
+ *    workspace than any before it on that stream, allocate device memory
+ *    (hipMalloc) and must be made outside capture.  tl_fetch_counter_read
+ *    synchronises its stream and cannot be captured.
  */
 #ifndef TL_H_
 #define TL_H_

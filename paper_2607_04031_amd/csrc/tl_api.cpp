@@ -60,7 +60,7 @@ int get_state(hipStream_t stream, size_t ws_bytes, StreamState** out) {
     StreamState& st = g_state[{dev, (void*)stream}];
     if (!st.fetch) {
         if (hipMalloc(&st.fetch, sizeof(unsigned long long)) != hipSuccess) { st.fetch = nullptr; return TL_ENOMEM; }
-        if (hipMemsetAsync(st.fetch, 0, sizeof(unsigned long long), stream) != hipSuccess) return TL_EHIP;
+        if (launch_zero_u64(st.fetch, stream) != hipSuccess) return TL_EHIP;
     }
     if (ws_bytes > st.ws_bytes) {
         if (st.ws) {
@@ -609,7 +609,7 @@ int tl_fetch_counter_read(void* stream, int64_t* bytes) {
     unsigned long long v = 0;
     if (hipStreamSynchronize(s) != hipSuccess) return TL_EHIP;
     if (hipMemcpy(&v, st->fetch, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return TL_EHIP;
-    if (hipMemsetAsync(st->fetch, 0, sizeof v, s) != hipSuccess) return TL_EHIP;
+    if (launch_zero_u64(st->fetch, s) != hipSuccess) return TL_EHIP;
     if (hipStreamSynchronize(s) != hipSuccess) return TL_EHIP;
     *bytes = int64_t(v);
     return TL_OK;

@@ -378,6 +378,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* ws, voi
     }
 }
 
+__global__ void zero_u64_kernel(unsigned long long* p) { *p = 0ull; }
+
 template <int MT, int NS, int WAVES, bool TILE, bool GROUPED, bool SWIGLU = false>
 hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
     constexpr int U = MT >= 2 ? 2 : 4;   // steps in flight per wave; fewer for larger M (registers)
@@ -420,6 +422,11 @@ hipError_t launch_m(const DecodeParams& p, int grid, int ns, int waves, bool til
 }
 
 }  // namespace
+
+hipError_t launch_zero_u64(unsigned long long* p, hipStream_t stream) {
+    hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(1), 0, stream, p);
+    return hipGetLastError();
+}
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     DecodeParams p;

@@ -82,6 +82,9 @@ struct DecodeLaunch {
 };
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream);
+// *p = 0, enqueued on 'stream' as a one-thread kernel (not a memset node, so
+// the clear behaves like any kernel inside a captured graph)
+hipError_t launch_zero_u64(unsigned long long* p, hipStream_t stream);
 // the fixed-order split-K reduce that follows a decode launch with split_k > 1
 // (passes 'e' through when it is an error or split_k is 1)
 hipError_t launch_splitk_reduce(const DecodeLaunch& d, hipError_t e, hipStream_t stream);
