@@ -195,7 +195,8 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * with K % 64 or N % 32 != 0; FP8 above 64 rows), TL_LAYOUT_KN_ROW, or sizes
  * past the kernels' 32-bit byte offsets: for M <= 64, 2 * M * K or the bytes
  * of tile_n weight rows (tile_n * K * elem_bytes, K padded for tile-major)
- * of 2^31 or more; above 64 rows, A or W of 2^32 bytes or more.
+ * of 2^31 or more; above 64 rows, A or W of 2^32 bytes or more, or more
+ * than 2^31 - 1 workgroups.  M, N or K above 2^30: TL_EINVAL.
  * TL_ENOMEM if the split-K workspace cannot be allocated; TL_EHIP if the
  * launch fails.
  */
@@ -281,7 +282,7 @@ int tl_gemm_grouped(const void* A, int64_t a_rows, const int32_t* token_ids,
  * weight: tl_tile_bytes(2I, K, ...) for tile-major); in addition
  * TL_EUNSUPPORTED for I % 32 != 0, a tile-major block_rows that does not
  * divide 32, or a [2I][K] weight of 2^31 bytes or more; TL_EINVAL for
- * I > 2^30.
+ * I > 2^29 (2I weight rows).
  */
 int tl_gemm_grouped_swiglu(const void* A, int64_t a_rows, const int32_t* token_ids,
                            const int32_t* group_offsets, int32_t num_groups, int64_t total_rows,
@@ -302,8 +303,12 @@ int tl_gemm_grouped_swiglu(const void* A, int64_t a_rows, const int32_t* token_i
  * tile does not divide N or K, as tl_repack writes it; useful bytes count the
  * N x K matrix only); G here is the memory system's granularity and may
  * differ from layout->G.  Other descriptor fields are ignored.
- * Errors: TL_EINVAL for non-positive sizes or tiles, G < 1, N * K > 2^40, a
- * bad TILE descriptor, or NULL pointers.
+ * Errors: TL_EINVAL for non-positive sizes or tiles, G < 1 or G > 2^40,
+ * N * K > 2^40, a bad TILE descriptor, NULL pointers, or a count past
+ * 2^63 - 1; TL_EUNSUPPORTED when no closed form applies (non-power-of-two
+ * tiles or G, ragged tiles, segments that straddle blocks) and the weight
+ * spans more than 2^28 G-byte blocks (the exact enumerator's block table);
+ * TL_ENOMEM if that table cannot be allocated.
  */
 int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
                 int32_t tile_k, const tl_layout_desc* layout, int64_t G, tl_amp* out);
@@ -376,9 +381,10 @@ typedef struct tl_view {
  * intra-tile offset.  *count (if not NULL) receives the element count; with
  * offsets == NULL nothing else is written.
  * Errors: TL_EINVAL for a bad layout (see tl_repack), K % block_cols or
- * N % block_rows != 0, rank outside 1..5, strides[0] != 1, a non-positive
- * stride or box, a negative coordinate, a stride >= K that is not a multiple
- * of K, a box reaching outside the K x N matrix, or capacity < count;
+ * N % block_rows != 0, K * N > 2^40, rank outside 1..5, strides[0] != 1, a
+ * non-positive stride or box, a negative coordinate, a stride >= K that is
+ * not a multiple of K or above K * N, a box reaching outside the K x N
+ * matrix, or capacity < count;
  * TL_EUNSUPPORTED when the view breaks the invariants the hardware relies on:
  * box[0] not a power of two, a box not starting on a memory-tile boundary, a
  * row-index stride that is not a whole number of memory tiles, or a column

@@ -60,7 +60,11 @@ int get_state(hipStream_t stream, size_t ws_bytes, StreamState** out) {
     StreamState& st = g_state[{dev, (void*)stream}];
     if (!st.fetch) {
         if (hipMalloc(&st.fetch, sizeof(unsigned long long)) != hipSuccess) { st.fetch = nullptr; return TL_ENOMEM; }
-        if (launch_zero_u64(st.fetch, stream) != hipSuccess) return TL_EHIP;
+        if (launch_zero_u64(st.fetch, stream) != hipSuccess) {   // the next call allocates and clears again
+            (void)hipFree(st.fetch);
+            st.fetch = nullptr;
+            return TL_EHIP;
+        }
     }
     if (ws_bytes > st.ws_bytes) {
         if (st.ws) {
@@ -129,6 +133,7 @@ struct Plan {
 };
 
 constexpr int kDecodeMaxM = 64;
+constexpr int64_t kMaxDim = int64_t(1) << 30;   // largest M, N or K
 constexpr int kTargetWorkgroups = 1024;   // 4 per CU on 256 CUs
 constexpr int kMaxSplitK = 16;            // partials the reduce kernel sums
 constexpr int kCUs = 256;                  // MI355X compute units
@@ -144,7 +149,8 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         return TL_EINVAL;
     if (d->elem_bytes != 2 && d->elem_bytes != 1) return d->elem_bytes < 1 ? TL_EINVAL : TL_EUNSUPPORTED;
     const int s = d->elem_bytes;
-    if (M > (int64_t(1) << 31) || N > (int64_t(1) << 31) || K > (int64_t(1) << 31)) return TL_EINVAL;
+    // kernel-side row and column indices are 32-bit, with room for a tile past the edge
+    if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return TL_EINVAL;
 
     Plan p;
     std::memset(&p.pub, 0, sizeof p.pub);
@@ -283,6 +289,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.pub.waves = tm == 256 && tn == 256 ? 8 : 4;
         p.pub.workgroups = mt * (p.n_main / tn + (p.n_main % tn ? 1 : 0)) +
                            ((M + 127) / 128) * ((N - p.n_main) / 128);
+        if (p.pub.workgroups >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;   // one launch's grid
         p.pub.workspace_bytes = 0;
     }
     *P = p;
@@ -411,7 +418,7 @@ static int grouped_impl(const void* A, int64_t a_rows, const int32_t* token_ids,
                         int64_t group_stride, void* C, int64_t N, int64_t K, const tl_layout_desc* layout,
                         int32_t fetch_mode, void* stream, bool swiglu) {
     Plan p;
-    if (swiglu && N > (int64_t(1) << 30)) return TL_EINVAL;
+    if (swiglu && N > kMaxDim / 2) return TL_EINVAL;
     const int64_t w_rows = swiglu ? 2 * N : N;
     int rc = plan_grouped(max_group_rows, w_rows, K, layout, fetch_mode, &p);
     if (rc != TL_OK) return rc;

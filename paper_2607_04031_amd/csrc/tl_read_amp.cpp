@@ -9,11 +9,15 @@
 //    sub-tile, unioned per tile with a stamp array, for everything else.
 #include <algorithm>
 #include <cstring>
+#include <new>
 #include <vector>
 
 #include "tl_internal.h"
 
 namespace {
+
+// Largest block table the enumerator allocates (8 bytes per block: 2 GB).
+constexpr int64_t kMaxEnumBlocks = int64_t(1) << 28;
 
 struct Geometry {
     int kind;
@@ -72,7 +76,7 @@ int64_t closed_form_blocks(const Geometry& g, int64_t tn, int64_t tk, int64_t G)
 extern "C" int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int32_t tile_n,
                            int32_t tile_k, const tl_layout_desc* layout, int64_t G, tl_amp* out) {
     if (!layout || !out) return TL_EINVAL;
-    if (M < 1 || N < 1 || K < 1 || tile_m < 1 || tile_n < 1 || tile_k < 1 || G < 1)
+    if (M < 1 || N < 1 || K < 1 || tile_m < 1 || tile_n < 1 || tile_k < 1 || G < 1 || G > (int64_t(1) << 40))
         return TL_EINVAL;
     Geometry g;
     g.kind = layout->kind;
@@ -95,26 +99,36 @@ extern "C" int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int3
     const int64_t span = g.kind == TL_LAYOUT_TILE ? tl::packed_bytes(g.L, N, K) : total_bytes;
     const int64_t nblocks = (span + G - 1) / G;
 
+    // every count below must fit in int64
+    auto mul = [](int64_t a, int64_t b, int64_t* out) { return !__builtin_mul_overflow(a, b, out); };
     tl_amp r;
     std::memset(&r, 0, sizeof r);
-    r.compute_tiles = m_tiles * n_tiles * k_steps;
-    r.useful_bytes = m_tiles * total_bytes;
+    int64_t nk = 0;
+    if (!mul(n_tiles, k_steps, &nk) || !mul(m_tiles, nk, &r.compute_tiles) ||
+        !mul(m_tiles, total_bytes, &r.useful_bytes))
+        return TL_EINVAL;
 
     int64_t per_tile = closed_form_blocks(g, tn, tk, G);
     if (per_tile > 0) {
-        r.requests = m_tiles * n_tiles * k_steps * per_tile;
+        if (!mul(r.compute_tiles, per_tile, &r.requests)) return TL_EINVAL;
         r.min_blocks_per_tile = r.max_blocks_per_tile = per_tile;
         r.unique_blocks = nblocks;   // every element is touched by some tile
     } else {
-        std::vector<int64_t> stamp(size_t(nblocks), -1);
-        std::vector<uint8_t> seen(size_t(nblocks), 0);
+        // stamp[b]: last (n-tile, k-step) that touched block b, -1 if none yet
+        if (nblocks > kMaxEnumBlocks) return TL_EUNSUPPORTED;
+        std::vector<int64_t> stamp;
+        try {
+            stamp.assign(size_t(nblocks), -1);
+        } catch (const std::bad_alloc&) {
+            return TL_ENOMEM;
+        }
         int64_t requests = 0, unique = 0, bmin = -1, bmax = 0, tile_id = 0;
         auto visit = [&](int64_t begin_byte, int64_t end_byte, int64_t& count) {
             for (int64_t b = begin_byte / G; b <= (end_byte - 1) / G; ++b) {
                 if (stamp[size_t(b)] != tile_id) {
+                    if (stamp[size_t(b)] < 0) ++unique;
                     stamp[size_t(b)] = tile_id;
                     ++count;
-                    if (!seen[size_t(b)]) { seen[size_t(b)] = 1; ++unique; }
                 }
             }
         };
@@ -144,12 +158,12 @@ extern "C" int tl_read_amp(int64_t M, int64_t N, int64_t K, int32_t tile_m, int3
                 bmax = std::max(bmax, count);
             }
         }
-        r.requests = requests * m_tiles;
+        if (!mul(requests, m_tiles, &r.requests)) return TL_EINVAL;
         r.unique_blocks = unique;
         r.min_blocks_per_tile = bmin;
         r.max_blocks_per_tile = bmax;
     }
-    r.fetched_bytes = r.requests * G;
+    if (!mul(r.requests, G, &r.fetched_bytes)) return TL_EINVAL;
     r.amp = double(r.fetched_bytes) / double(r.useful_bytes);
     *out = r;
     return TL_OK;

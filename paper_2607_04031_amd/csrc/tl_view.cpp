@@ -20,6 +20,8 @@
 
 namespace tl {
 
+constexpr int64_t kMaxView = int64_t(1) << 40;
+
 int make_view_program(const tl_view* v, int64_t K, int64_t N, int32_t s, int64_t G, int32_t block_rows,
                       ViewProgram* out) {
     if (!v || !out) return TL_EINVAL;
@@ -27,13 +29,15 @@ int make_view_program(const tl_view* v, int64_t K, int64_t N, int32_t s, int64_t
     if (make_tile_layout(s, G, block_rows, &L) != TL_OK) return TL_EINVAL;
     const int64_t a = L.bc, b = L.br;
     if (K < 1 || N < 1 || K % a || N % b) return TL_EINVAL;
+    if (K > kMaxView || N > kMaxView || K > kMaxView / N) return TL_EINVAL;   // K N <= 2^40
     if (v->rank < 1 || v->rank > TL_VIEW_MAX_RANK) return TL_EINVAL;
     if (v->strides[0] != 1) return TL_EINVAL;
     int64_t elements = 1;
     int64_t i_max = 0, j_max = 0, i0 = 0, kj0 = 0;
     for (int d = 0; d < v->rank; ++d) {
         const int64_t st = v->strides[d], c = v->coords[d], n = v->box[d];
-        if (st < 1 || c < 0 || n < 1) return TL_EINVAL;
+        // coordinates, extents and strides inside the matrix (no 64-bit overflow below)
+        if (st < 1 || c < 0 || n < 1 || c >= kMaxView || n > kMaxView || st > K * N) return TL_EINVAL;
         if (st >= K && st % K) return TL_EINVAL;          // a column step is a whole number of columns
         elements *= n;
         if (elements > (int64_t(1) << 40)) return TL_EINVAL;

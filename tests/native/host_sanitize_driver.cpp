@@ -18,6 +18,7 @@ hipError_t launch_lgms(const DecodeLaunch&, int64_t, int, hipStream_t) { std::ab
 int lgms_ctas_per_cu(int) { std::abort(); }
 hipError_t launch_prefill(const PrefillLaunch&, hipStream_t) { std::abort(); }
 hipError_t launch_view_load(const uint8_t*, int64_t, const ViewProgram&, uint8_t*, hipStream_t) { std::abort(); }
+hipError_t launch_zero_u64(unsigned long long*, hipStream_t) { std::abort(); }
 }  // namespace tl
 
 int main() {
@@ -27,7 +28,8 @@ int main() {
     d.G = 4096;
     d.block_rows = 32;
     tl_amp a;
-    // read amplification: every layout, ragged tiles and shapes, G != memory-tile size
+    // read amplification: every layout, ragged tiles and shapes (padded
+    // tile-major copies), G != memory-tile size -- all valid
     for (int kind : {TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE})
         for (int64_t M : {1, 7, 64})
             for (int64_t N : {32, 96, 1024})
@@ -36,10 +38,14 @@ int main() {
                         for (int tk : {32, 64, 160})
                             for (int64_t G : {512, 4096, 16384}) {
                                 d.kind = kind;
-                                const bool tile_ok = kind != TL_LAYOUT_TILE || (N % 32 == 0 && K % 64 == 0);
-                                const int rc = tl_read_amp(M, N, K, 16, tn, tk, &d, G, &a);
-                                if ((rc == TL_OK) != tile_ok) ++bad;
+                                if (tl_read_amp(M, N, K, 16, tn, tk, &d, G, &a) != TL_OK) ++bad;
                             }
+    // counts past 2^63 - 1 and oversized enumerations are rejected, not wrapped
+    d.kind = TL_LAYOUT_TILE;
+    if (tl_read_amp(int64_t(1) << 40, 1 << 20, 1 << 20, 1, 32, 64, &d, 4096, &a) != TL_EINVAL) ++bad;
+    if (tl_read_amp(8, 1 << 20, 1 << 20, 16, 32, 64, &d, int64_t(1) << 41, &a) != TL_EINVAL) ++bad;
+    d.kind = TL_LAYOUT_NK_ROW;
+    if (tl_read_amp(8, 1 << 20, 1 << 20, 16, 48, 48, &d, 16, &a) != TL_EUNSUPPORTED) ++bad;
     // views: 2-D to 4-D, Case 1, Case 2 and wider-than-tile boxes
     d.kind = TL_LAYOUT_TILE;
     std::vector<int64_t> offs(1 << 16);
@@ -63,6 +69,12 @@ int main() {
     bad_desc.G = 1000;
     if (tl_gemm_plan(8, 512, 512, &bad_desc, TL_FETCH_BLOCK, &p) != TL_EINVAL) ++bad;
     if (tl_gemm(nullptr, nullptr, nullptr, 8, 512, 512, &d, TL_FETCH_BLOCK, nullptr) != TL_EINVAL) ++bad;
+    if (tl_gemm_plan(8, (int64_t(1) << 30) + 1, 64, &d, TL_FETCH_BLOCK, &p) != TL_EINVAL) ++bad;
+    // a prefill grid of 2^31 workgroups or more (A and W each 2^31 bytes)
+    tl_layout_desc rm = d;
+    rm.kind = TL_LAYOUT_NK_ROW;
+    if (tl_gemm_plan(int64_t(1) << 26, int64_t(1) << 26, 16, &rm, TL_FETCH_NATIVE, &p) != TL_EUNSUPPORTED) ++bad;
+    if (tl_gemm_plan(int64_t(1) << 16, int64_t(1) << 16, 16, &rm, TL_FETCH_NATIVE, &p) != TL_OK) ++bad;
     int64_t deg = -1;
     if (tl_prefetch_degree(8e12, 5e-6, 16777216.0, 128, 1.0, &deg) != TL_OK || deg != 2) ++bad;
     std::printf("host sanitize driver: %d unexpected results, last view %lld elements\n", bad, (long long)n);
