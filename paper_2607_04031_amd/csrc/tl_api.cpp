@@ -130,6 +130,7 @@ struct Plan {
     int64_t fetch_G = 0;
     int64_t n_main = 0;          // prefill: columns covered by the main tiles (rest: 128 x 128)
     bool fp8 = false;            // 1-byte (OCP E4M3) weight, decode kernel
+    int lds_tiles = 0;           // > 0: decode with activations staged in LDS, tiles per workgroup
 };
 
 constexpr int kDecodeMaxM = 64;
@@ -246,12 +247,36 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         if (waves == 16 && mn > 1) waves = 8;
         if (waves == 8 && mn > 4) waves = 4;
         p.waves = waves;
+        // 17 <= M <= 32 on whole tile-major strips: stage the activations in
+        // LDS, one 8-wave workgroup per CU taking T of the 32-row tiles and
+        // one of S K ranges, when the (T, S) grid covers the CUs in whole
+        // rounds (A crosses L2 -> CU once per T tiles instead of once per tile)
+        if (tile && !p.fp8 && p.m_tiles16 == 2 && !d->tile_n && !d->split_k && N % 32 == 0 && K % 512 == 0 &&
+            p.L.br <= 32 && 512 % p.k_unit == 0) {
+            const int64_t strips = N / 32, chunks = K / 512;
+            for (int T = 7; T >= 4 && !p.lds_tiles; --T) {
+                if (strips % T) continue;
+                for (int64_t s2 = 1; s2 <= 8 && chunks / s2 >= 4; s2 *= 2) {
+                    const int64_t w = strips / T * s2;
+                    if (w % kCUs == 0 && w <= 4 * kCUs) {
+                        p.lds_tiles = T;
+                        S = s2;
+                        break;
+                    }
+                }
+            }
+            if (p.lds_tiles) {
+                tn = 32;
+                p.waves = 8;
+            }
+        }
+        const int64_t wgs_final = p.lds_tiles ? N / 32 / p.lds_tiles * S : wgs;
         p.pub.tile_m = 16 * p.m_tiles16;
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
         p.pub.split_k = int(S);
-        p.pub.waves = waves;
-        p.pub.workgroups = wgs;
+        p.pub.waves = p.waves;
+        p.pub.workgroups = wgs_final;
         p.pub.workspace_bytes = S > 1 ? S * ((M * N + 3) / 4 * 4) * 4 : 0;
     } else {
         p.pub.kernel = 2;
@@ -391,6 +416,7 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
         d.fetch_G = p.fetch_G;
         d.fp8 = p.fp8;
         d.scales = scales;
+        d.lds_tiles = p.lds_tiles;
         e = launch_decode(d, s);
     } else {
         PrefillLaunch q;

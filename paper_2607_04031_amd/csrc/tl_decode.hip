@@ -462,6 +462,12 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     p.a_rows = int(d.a_rows);
     p.total_rows = int(d.total_rows);
     p.scales = d.scales;
+    if (d.lds_tiles > 0) {   // chunks of 512 columns; workgroup = lds_tiles tiles x one K range
+        p.units = int(d.K / 512);
+        p.steps_per_unit = 8;
+        const int grid = int(d.N / 32 / d.lds_tiles) * d.split_k;
+        return launch_splitk_reduce(d, launch_lds_decode(p, d.lds_tiles, grid, stream), stream);
+    }
     const bool grouped = d.num_groups > 0;
     const int grid = grouped ? d.num_groups * p.tiles_per_group : p.tiles_per_group * d.split_k;
     const int ns = d.tile_n / 16;

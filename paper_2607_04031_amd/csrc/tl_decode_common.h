@@ -83,4 +83,9 @@ __device__ inline bf16x8 load_stream(const uint8_t* p) {
 hipError_t launch_fp8_decode(const DecodeParams& p, int grid, int m_tiles16, int ns, int waves, bool tile,
                              hipStream_t stream);
 
+// Decode with activations staged in LDS (tl_decode_lds.hip): M <= 32,
+// tile-major, tiles_per_wg (4..7) 32-row tiles per workgroup, p.units
+// chunks of 512 columns split p.split_k ways.
+hipError_t launch_lds_decode(const DecodeParams& p, int tiles_per_wg, int grid, hipStream_t stream);
+
 }  // namespace tl

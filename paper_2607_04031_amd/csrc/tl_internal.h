@@ -79,6 +79,9 @@ struct DecodeLaunch {
     // FP8 (E4M3) weight, bf16 activations; optional per-output-channel scales [N]
     bool fp8 = false;
     const float* scales = nullptr;
+    // > 0: the LDS-staged activation kernel with this many 32-row tiles per
+    // workgroup (17 <= M <= 32, tile-major, N % 32 == 0, K % 512 == 0)
+    int lds_tiles = 0;
 };
 
 hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream);

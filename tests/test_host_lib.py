@@ -147,10 +147,25 @@ def test_gemm_plan_decode_and_prefill_shapes():
     # 512 tiles -> 8 waves; registers cap waves as M and tile_n grow
     assert tl.tl_gemm_plan(8, 16384, 1024, d)["waves"] == 8
     assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 64      # M > 16: 64-row tiles
-    # 128 tiles of 64 rows: K split in two, one 8-wave workgroup per CU
-    p = tl.tl_gemm_plan(32, 8192, 8192, d)
+    # 17 <= M <= 32 on the Llama shapes: activations staged in LDS, one 8-wave
+    # workgroup per CU taking T 32-row tiles (whole strips) x one of S K ranges
+    for N, K, S in [(10240, 8192, 4), (8192, 8192, 4), (57344, 8192, 1), (8192, 28672, 4)]:
+        for M in (17, 32):
+            p = tl.tl_gemm_plan(M, N, K, d)
+            assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (32, S, 8, 256)
+            amp = tl.tl_read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, 4096)
+            assert amp["amp"] == 1.0
+    # a fixed tile or split keeps the streaming kernel: 128 tiles of 64 rows,
+    # K split in two, one 8-wave workgroup per CU
+    p = tl.tl_gemm_plan(32, 8192, 8192, tl.layout(tile_n=64))
     assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (64, 2, 8, 256)
-    assert tl.tl_gemm_plan(32, 57344, 8192, d)["split_k"] == 1      # >= 2 tiles per CU: no split
+    assert tl.tl_gemm_plan(32, 57344, 8192, tl.layout(tile_n=64))["split_k"] == 1   # >= 2 tiles per CU
+    p = tl.tl_gemm_plan(32, 8192, 8192, tl.layout(split_k=2))
+    assert (p["tile_n"], p["split_k"], p["workgroups"]) == (64, 2, 256)
+    # no whole-round (T, S) grid (257 strips), or K / 512 < 4: streaming kernel
+    p = tl.tl_gemm_plan(32, 8192 + 32, 8192, d)
+    assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (32, 4, 4, 1028)
+    assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 64
     assert tl.tl_gemm_plan(32, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64))["waves"] == 4
