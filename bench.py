@@ -597,9 +597,14 @@ def main():
     if not args.no_extras:
         extras = {}
         for M in (1, 32):
-            r = decode_layer(ctx, weights, M, args.steps, 2, desc)
+            r = decode_layer(ctx, weights, M, args.steps, 2, desc, event_pass=True)
             extras[f"decode_layer_M{M}_GB/s"] = round(r["GB/s"], 1)
-            log(f"decode layer M={M}: {r['GB/s']:.1f} GB/s")
+            # per call, from HIP events around each tl_gemm (which add ~4 us)
+            extras[f"decode_layer_M{M}_per_shape"] = {
+                name: {"us": round(ms * 1e3, 2), "split_k": tl.tl_gemm_plan(M, N, K, desc)["split_k"],
+                       "waves": tl.tl_gemm_plan(M, N, K, desc)["waves"]}
+                for (name, N, K, _), ms in zip(weights, r["per_launch_ms"])}
+            log(f"decode layer M={M}: {r['GB/s']:.1f} GB/s {extras[f'decode_layer_M{M}_per_shape']}")
         extras["layouts_M8"] = layout_comparison(ctx, weights, weights_rm)
         del weights_rm
         torch.cuda.empty_cache()
