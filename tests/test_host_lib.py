@@ -146,7 +146,13 @@ def test_gemm_plan_decode_and_prefill_shapes():
         assert amp["amp"] == 1.0
     # 512 tiles -> 8 waves; registers cap waves as M and tile_n grow
     assert tl.tl_gemm_plan(8, 16384, 1024, d)["waves"] == 8
-    assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 64      # M > 16: 64-row tiles
+    assert tl.tl_gemm_plan(32, 8192, 4096, d)["tile_n"] == 64      # M > 16: 64-row tiles
+    # a weight under 32 MB is latency-bound: 32-row tiles, splits down to 256 K
+    for M in (8, 32, 64):
+        p = tl.tl_gemm_plan(M, 512, 2048, d)                        # Qwen k/v projection
+        assert (p["tile_n"], p["split_k"], p["workgroups"]) == (32, 8, 128)
+        p = tl.tl_gemm_plan(M, 4096, 2048, d)                       # Qwen q projection
+        assert (p["tile_n"], p["split_k"], p["workgroups"]) == (32, 2, 256)
     # 17 <= M <= 32 on the Llama shapes: activations staged in LDS, one 8-wave
     # workgroup per CU taking T 32-row tiles (whole strips) x one of S K ranges
     for N, K, S in [(10240, 8192, 4), (8192, 8192, 4), (57344, 8192, 1), (8192, 28672, 4)]:
@@ -165,7 +171,7 @@ def test_gemm_plan_decode_and_prefill_shapes():
     # no whole-round (T, S) grid (257 strips), or K / 512 < 4: streaming kernel
     p = tl.tl_gemm_plan(32, 8192 + 32, 8192, d)
     assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (32, 4, 4, 1028)
-    assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 64
+    assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 32          # 16 MB: small
     assert tl.tl_gemm_plan(32, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64))["waves"] == 4
