@@ -192,8 +192,9 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.m_tiles16 = int((M + 15) / 16);
         if (p.m_tiles16 == 3) p.m_tiles16 = 4;
         // A small weight (under 32 MB: a few microseconds of HBM time) is
-        // latency-bound: 32-row tiles and K splits down to 256 columns give
-        // more workgroups.  Otherwise 64-row tiles halve the activation
+        // latency-bound: 32-row tiles and K splits down to 512 columns give
+        // more workgroups (shorter splits cost more in the reduce launch than
+        // they gain).  Otherwise 64-row tiles halve the activation
         // reloads per weight byte, which pays off once M exceeds one 16-row
         // MFMA tile.  (Measured on the Qwen attention projections at M = 8,
         // 32 and 64 and the Llama-70B shapes.)
@@ -219,11 +220,11 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         //    (the reduce launch then costs a few per cent at most);
         //  - otherwise split K until there are about 1024 workgroups.
         // K splits write fp32 partials that a fixed-order reduce kernel sums;
-        // every split covers >= 1024 K (>= 256 for a small weight).  (Chosen
+        // every split covers >= 1024 K (>= 512 for a small weight).  (Chosen
         // from measurements of the Llama-70B decode shapes at M = 1, 8 and 32.)
         int64_t S = d->split_k;
         if (S == 0) {
-            const int64_t min_units = std::max<int64_t>(1, (small ? 256 : 1024) / p.k_unit);
+            const int64_t min_units = std::max<int64_t>(1, (small ? 512 : 1024) / p.k_unit);
             const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(units / min_units, kMaxSplitK));
             if (n_tiles >= 2 * kCUs) {
                 S = 1;

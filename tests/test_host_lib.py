@@ -147,10 +147,12 @@ def test_gemm_plan_decode_and_prefill_shapes():
     # 512 tiles -> 8 waves; registers cap waves as M and tile_n grow
     assert tl.tl_gemm_plan(8, 16384, 1024, d)["waves"] == 8
     assert tl.tl_gemm_plan(32, 8192, 4096, d)["tile_n"] == 64      # M > 16: 64-row tiles
-    # a weight under 32 MB is latency-bound: 32-row tiles, splits down to 256 K
+    # a weight under 32 MB is latency-bound: 32-row tiles, splits down to 512 K
     for M in (8, 32, 64):
         p = tl.tl_gemm_plan(M, 512, 2048, d)                        # Qwen k/v projection
-        assert (p["tile_n"], p["split_k"], p["workgroups"]) == (32, 8, 128)
+        assert (p["tile_n"], p["split_k"], p["workgroups"]) == (32, 4, 64)
+        p = tl.tl_gemm_plan(M, 2048, 768, d)                        # one Qwen expert's down projection
+        assert (p["tile_n"], p["split_k"], p["workgroups"]) == (32, 1, 64)
         p = tl.tl_gemm_plan(M, 4096, 2048, d)                       # Qwen q projection
         assert (p["tile_n"], p["split_k"], p["workgroups"]) == (32, 2, 256)
     # 17 <= M <= 32 on the Llama shapes: activations staged in LDS, one 8-wave
