@@ -220,9 +220,10 @@ def prefill_layer(ctx, weights):
 
 
 def moe_layer(ctx, steps, warmup):
-    """Qwen-3-30B-A3B-shaped layer at 64 tokens: attention q, k, v, o at M = 64
-    and, for every expert the seeded top-8 routing touches, its gate+up and
-    down GEMMs at that expert's token count; tile-major weights.  Timed four
+    """Qwen-3-30B-A3B-shaped layer at 64 tokens: attention q, k, v (one call
+    over the stacked [q; k; v] weight) and o at M = 64 and, for every expert
+    the seeded top-8 routing touches, its gate+up and down GEMMs at that
+    expert's token count; tile-major weights.  Timed four
     ways: one tl_gemm per GEMM (eager, and replayed as one HIP graph), the
     experts as two tl_gemm_grouped launches (gate+up over all experts, then
     down) beside the four attention calls, and the fused expert path: gate+up
@@ -247,10 +248,20 @@ def moe_layer(ctx, steps, warmup):
         tl.tl_repack(W, Wt, N, K, 2, G, BR)
         return Wt
 
+    # attention: q, k and v read the same hidden states, so their tile-major
+    # weights are laid end to end as one [q; k; v] weight (each projection's
+    # rows are whole strips of memory tiles, so the concatenation of the three
+    # copies is the copy of the stacked matrix) and run as one call, as the
+    # Llama QKV projection is; then o.
     attn = []           # (A, W tile-major, C, M, N, K)
-    for i, (name, N, K) in enumerate(synth.QWEN_ATTN):
-        attn.append((hidden if K == H else attn_out, tile_major(N, K, synth.qwen_attn_seed(i)),
-                     torch.empty((Mt, N), dtype=torch.float32, device=ctx.dev), Mt, N, K))
+    qkv_parts = [tile_major(N, K, synth.qwen_attn_seed(i)) for i, (_, N, K) in enumerate(synth.QWEN_ATTN[:3])]
+    n_qkv = sum(N for (_, N, _) in synth.QWEN_ATTN[:3])
+    attn.append((hidden, torch.cat([w.reshape(-1) for w in qkv_parts]).view(n_qkv, H),
+                 torch.empty((Mt, n_qkv), dtype=torch.float32, device=ctx.dev), Mt, n_qkv, H))
+    del qkv_parts
+    _, No, Ko = synth.QWEN_ATTN[3]
+    attn.append((attn_out, tile_major(No, Ko, synth.qwen_attn_seed(3)),
+                 torch.empty((Mt, No), dtype=torch.float32, device=ctx.dev), Mt, No, Ko))
     # expert weights stacked [E, N, K], each expert tile-major; untouched experts are never read
     gu_stack = torch.empty((E, Ngu, Kgu), dtype=torch.bfloat16, device=ctx.dev)
     d_stack = torch.empty((E, Nd, Kd), dtype=torch.bfloat16, device=ctx.dev)

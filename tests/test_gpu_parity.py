@@ -523,3 +523,29 @@ def test_moe_attention_projections(i):
     A = synth.normal_bf16((synth.QWEN_TOKENS, K), seed=seed)
     W = synth.normal_bf16((N, K), seed=synth.qwen_attn_seed(i), sigma=synth.W_SIGMA)
     parity(host_f32(run_gemm(A, W, tl.layout())), oracle.gemm_f64(A, W), f"attn {name}")
+
+
+def test_moe_attention_stacked_qkv():
+    """q, k and v repacked one by one and laid end to end are the tile-major
+    copy of the stacked [q; k; v] weight (each has whole strips of 32 rows),
+    and one call over them equals the three projections (the bench's path)."""
+    import torch
+    K, M = synth.QWEN_HIDDEN, synth.QWEN_TOKENS
+    banner("moe attention stacked qkv")
+    Ws = [synth.normal_bf16((N, K), seed=synth.qwen_attn_seed(i), sigma=synth.W_SIGMA)
+          for i, (_, N, _) in enumerate(synth.QWEN_ATTN[:3])]
+    parts = []
+    for W in Ws:
+        Wd = dev_bf16(W)
+        Wt = torch.empty_like(Wd)
+        tl.tl_repack(Wd, Wt, W.shape[0], K, 2, 4096, 32)
+        parts.append(Wt.reshape(-1))
+    stacked = np.vstack(Ws)
+    cat = torch.cat(parts).view(stacked.shape[0], K)
+    _sync()
+    assert np.array_equal(host_bits(cat), oracle.repack(stacked, 4096, 32))
+    A = synth.normal_bf16((M, K), seed=synth.QWEN_SEED_HIDDEN)
+    C = torch.empty((M, stacked.shape[0]), dtype=torch.float32, device="cuda")
+    tl.tl_gemm(dev_bf16(A), cat, C, M, stacked.shape[0], K, tl.layout(), tl.TL_FETCH_BLOCK)
+    _sync()
+    parity(host_f32(C), oracle.gemm_f64(A, stacked), "stacked qkv")

@@ -572,3 +572,19 @@ def test_granularity_sweep_expectations_on_slice():
         assert oracle.read_amp(32, N, K, 32, 64, 64, NK_ROW, G)["amp"] == want
     # tile-major (G = 4 KB, br = 8 -> bc = 256): 4x at tk = 64
     assert oracle.read_amp(32, N, K, 32, 64, 64, TILE, 4096, layout_G=4096, block_rows=8)["amp"] == 4.0
+
+
+def test_stacked_strips_are_contiguous():
+    """Eq. 2 orders memory tiles along K within a strip of block_rows rows, so
+    a strip is one contiguous run of bytes: the tile-major copy of matrices
+    stacked along N (each a whole number of strips) is the concatenation of
+    their copies, checked against numpy's reshape of the stacked matrix."""
+    rng = np.random.default_rng(21)
+    for G, br in ((4096, 32), (512, 8), (16384, 64)):
+        bc = G // (2 * br)
+        parts = [rng.integers(0, 1 << 16, size=(br * r, bc * 3), dtype=np.uint16) for r in (1, 3, 2)]
+        stacked = np.vstack(parts)
+        want = stacked.reshape(stacked.shape[0] // br, br, 3, bc).transpose(0, 2, 1, 3).reshape(-1)
+        got = np.concatenate([oracle.repack(x, G, br).reshape(-1) for x in parts])
+        assert np.array_equal(got, want)
+        assert np.array_equal(oracle.repack(stacked, G, br).reshape(-1), want)
