@@ -341,6 +341,14 @@ int plan_grouped(int64_t max_group_rows, int64_t N, int64_t K, const tl_layout_d
     int rc = plan_gemm(std::min<int64_t>(max_group_rows, kDecodeMaxM), N, K, &d1, fetch_mode, P);
     if (rc != TL_OK) return rc;
     if (P->pub.kernel != 1 || P->block_row || P->fp8) return TL_EUNSUPPORTED;
+    // A 32-row tile of a short weight (K < 1024: under 64 KB per tile, e.g. a
+    // Qwen expert's down projection, K = 768) is little work per workgroup;
+    // 64-row tiles halve the workgroups and their fixed costs (down: -3 %).
+    if (!d->tile_n && P->pub.tile_n == 32 && K < 1024 && N % 64 == 0 &&
+        (d->kind != TL_LAYOUT_TILE || P->L.br <= 64)) {
+        P->pub.tile_n = 64;
+        P->pub.workgroups = (N + 63) / 64;
+    }
     P->waves = 4;
     P->pub.waves = 4;
     P->pub.workspace_bytes = 0;
