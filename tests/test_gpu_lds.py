@@ -94,10 +94,11 @@ def test_lds_decode_bf16_output():
     parity_bf16_out(host_bits(run(A, W, d)), oracle.gemm_f64(A, W), "lds bf16")
 
 
-@pytest.mark.parametrize("G,br", [(4096, 8), (4096, 16), (16384, 32), (1024, 8), (512, 4)])
+@pytest.mark.parametrize("G,br", [(4096, 8), (4096, 16), (16384, 32), (1024, 8), (512, 4), (512, 32), (1024, 16)])
 def test_lds_decode_memory_tile_shapes(G, br):
     """Memory tiles narrower or wider than a 64-column step (block_cols 256,
-    128, 256, 64, 64): a 32-row tile spans 32 / block_rows strips."""
+    128, 256, 64, 64, 8, 32): a 32-row tile spans 32 / block_rows strips, and
+    a step spans several memory tiles when block_cols < 64."""
     M, N, K = 32, 32768, 2048
     d = tl.layout(G=G, block_rows=br)
     lds_plan(M, N, K, d)
