@@ -405,6 +405,22 @@ int tl_view_offsets(const tl_view* view, int64_t K, int64_t N, int32_t elem_byte
 int tl_view_load(const void* src_tm, const tl_view* view, int64_t K, int64_t N, int32_t elem_bytes,
                  int64_t G, int32_t block_rows, void* dst, void* stream);
 
+/*
+ * tl_stream_read -- the HBM read ceiling the GEMM kernels are measured
+ * against (the decode path is bound by reading every weight byte once,
+ * Section 2.1): reads the 'bytes' bytes at src once, with the decode kernel's
+ * load pattern (64 lanes x 16 B, whole 128-byte lines, non-temporal), and
+ * XORs its little-endian 32-bit words into *checksum (the caller clears it;
+ * unchanged for bytes = 0), so the reads cannot be elided and the result is
+ * checkable.  src: device, 16-byte aligned; bytes: a multiple of 16, < 2^48;
+ * checksum: device uint32, 4-byte aligned, not inside src.  One kernel
+ * enqueued on 'stream' (none for bytes = 0).
+ * Errors: TL_EINVAL for NULL or misaligned pointers, bytes < 0, not a
+ * multiple of 16 or too large, or checksum inside src; TL_EHIP if a launch
+ * fails.
+ */
+int tl_stream_read(const void* src, int64_t bytes, uint32_t* checksum, void* stream);
+
 /* tl_fetch_counter_read -- synchronises 'stream', stores the weight bytes
  * tallied by tl_gemm calls made on it with TL_FETCH_COUNT since the last read
  * into *bytes, and resets the tally to zero.  Errors: TL_EINVAL for NULL

@@ -39,7 +39,7 @@ TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
 EXPORTED = ("tl_tile_bytes", "tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_gemm_grouped_swiglu", "tl_read_amp",
             "tl_view_offsets", "tl_view_load", "tl_prefetch_degree", "tl_gemm_lgms", "tl_lgms_occupancy",
-            "tl_fetch_counter_read", "tl_release", "tl_strerror")
+            "tl_stream_read", "tl_fetch_counter_read", "tl_release", "tl_strerror")
 TL_VIEW_MAX_RANK = 5
 
 
@@ -149,6 +149,8 @@ def load_library():
     lib.tl_read_amp.restype = ctypes.c_int
     lib.tl_read_amp.argtypes = [i64, i64, i64, i32, i32, i32, ctypes.POINTER(LayoutDesc), i64,
                                 ctypes.POINTER(Amp)]
+    lib.tl_stream_read.restype = ctypes.c_int
+    lib.tl_stream_read.argtypes = [p, i64, p, p]
     lib.tl_fetch_counter_read.restype = ctypes.c_int
     lib.tl_fetch_counter_read.argtypes = [p, ctypes.POINTER(i64)]
     lib.tl_release.restype = ctypes.c_int
@@ -301,6 +303,11 @@ def tl_read_amp(M, N, K, tile_m, tile_n, tile_k, layout, G) -> dict:
     _check(load_library().tl_read_amp(M, N, K, tile_m, tile_n, tile_k, ctypes.byref(d), G,
                                       ctypes.byref(out)), "tl_read_amp")
     return _struct_dict(out)
+
+
+def tl_stream_read(src, nbytes, checksum, stream=None):
+    """checksum: a device uint32/int32 tensor of one element; the XOR of src's 32-bit words is XORed into it."""
+    _check(load_library().tl_stream_read(_ptr(src), nbytes, _ptr(checksum), _stream(stream)), "tl_stream_read")
 
 
 def tl_fetch_counter_read(stream=None) -> int:

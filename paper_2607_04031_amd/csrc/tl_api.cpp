@@ -647,6 +647,14 @@ int tl_view_load(const void* src_tm, const tl_view* view, int64_t K, int64_t N, 
     return e == hipSuccess ? TL_OK : TL_EHIP;
 }
 
+int tl_stream_read(const void* src, int64_t bytes, uint32_t* checksum, void* stream) {
+    if (!checksum || (reinterpret_cast<uintptr_t>(checksum) & 3u)) return TL_EINVAL;
+    if (bytes < 0 || bytes % 16 || bytes >= (int64_t(1) << 48)) return TL_EINVAL;
+    if (bytes > 0 && (!src || !aligned16(src) || overlap(src, bytes, checksum, 4))) return TL_EINVAL;
+    hipError_t e = launch_stream_read(static_cast<const uint8_t*>(src), bytes, checksum, (hipStream_t)stream);
+    return e == hipSuccess ? TL_OK : TL_EHIP;
+}
+
 int tl_fetch_counter_read(void* stream, int64_t* bytes) {
     if (!bytes) return TL_EINVAL;
     hipStream_t s = (hipStream_t)stream;

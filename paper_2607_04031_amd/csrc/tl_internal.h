@@ -153,6 +153,9 @@ __host__ __device__ inline int64_t view_offset(const ViewProgram& P, int64_t e) 
     return off;
 }
 
+// reads bytes (a multiple of 16) of src once and XORs its 32-bit words
+// into *checksum (one kernel; nothing for bytes = 0)
+hipError_t launch_stream_read(const uint8_t* src, int64_t bytes, unsigned* checksum, hipStream_t stream);
 hipError_t launch_view_load(const uint8_t* src, int64_t src_bytes, const ViewProgram& P, uint8_t* dst,
                             hipStream_t stream);
 

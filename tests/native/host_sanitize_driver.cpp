@@ -19,6 +19,7 @@ int lgms_ctas_per_cu(int) { std::abort(); }
 hipError_t launch_prefill(const PrefillLaunch&, hipStream_t) { std::abort(); }
 hipError_t launch_view_load(const uint8_t*, int64_t, const ViewProgram&, uint8_t*, hipStream_t) { std::abort(); }
 hipError_t launch_zero_u64(unsigned long long*, hipStream_t) { std::abort(); }
+hipError_t launch_stream_read(const uint8_t*, int64_t, unsigned*, hipStream_t) { std::abort(); }
 }  // namespace tl
 
 int main() {
@@ -75,6 +76,14 @@ int main() {
     rm.kind = TL_LAYOUT_NK_ROW;
     if (tl_gemm_plan(int64_t(1) << 26, int64_t(1) << 26, 16, &rm, TL_FETCH_NATIVE, &p) != TL_EUNSUPPORTED) ++bad;
     if (tl_gemm_plan(int64_t(1) << 16, int64_t(1) << 16, 16, &rm, TL_FETCH_NATIVE, &p) != TL_OK) ++bad;
+    // tl_stream_read argument checks (no device work)
+    uint32_t* ck = reinterpret_cast<uint32_t*>(uintptr_t(1) << 40);
+    const void* src = reinterpret_cast<const void*>(uintptr_t(1) << 41);
+    if (tl_stream_read(src, 4096, nullptr, nullptr) != TL_EINVAL) ++bad;
+    if (tl_stream_read(src, 4095, ck, nullptr) != TL_EINVAL) ++bad;
+    if (tl_stream_read(src, -16, ck, nullptr) != TL_EINVAL) ++bad;
+    if (tl_stream_read(static_cast<const char*>(src) + 8, 4096, ck, nullptr) != TL_EINVAL) ++bad;
+    if (tl_stream_read(src, 4096, reinterpret_cast<uint32_t*>(uintptr_t(src) + 64), nullptr) != TL_EINVAL) ++bad;
     int64_t deg = -1;
     if (tl_prefetch_degree(8e12, 5e-6, 16777216.0, 128, 1.0, &deg) != TL_OK || deg != 2) ++bad;
     std::printf("host sanitize driver: %d unexpected results, last view %lld elements\n", bad, (long long)n);
