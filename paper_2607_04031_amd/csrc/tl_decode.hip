@@ -382,7 +382,10 @@ __global__ void zero_u64_kernel(unsigned long long* p) { *p = 0ull; }
 
 template <int MT, int NS, int WAVES, bool TILE, bool GROUPED, bool SWIGLU = false>
 hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
-    constexpr int U = MT >= 2 ? 2 : 4;   // steps in flight per wave; fewer for larger M (registers)
+    // steps in flight per wave: fewer for larger M, and for the grouped
+    // 64-row tile (4 steps there take all 256 VGPRs: one wave per SIMD; with
+    // 2 the kernel fits three -- Qwen expert down projection 66.5 -> 61.3 us)
+    constexpr int U = (MT >= 2 || (GROUPED && NS == 4 && !SWIGLU)) ? 2 : 4;
     if constexpr (!TILE && !GROUPED) {
         if (p.log2_fetch > 0) {   // block emulation: fewer steps in flight leave room for the block loop
             hipLaunchKernelGGL((decode_kernel<MT, NS, 2, WAVES, false, true, false>), dim3(grid), dim3(64 * WAVES), 0,
