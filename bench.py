@@ -140,6 +140,73 @@ def decode_layer(ctx, weights, M, steps, warmup, desc, event_pass=False):
     return res
 
 
+def cpu_oracle_timings(ctx, weights_host, threads):
+    """The CPU oracle (fp64, OpenMP over output elements) timed on the host
+    beside each GPU number: decode with all threads and with one, prefill on a
+    64-row sample extrapolated to M = 2048, the whole MoE layer, a repack and
+    an exact read-amplification enumeration.  Baselines, not targets."""
+    import oracle
+    synth, np = ctx.synth, ctx.np
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), model)
+    except OSError:
+        pass
+    res = {"host": {"cpu_model": model, "logical_cpus": os.cpu_count(), "threads": threads}}
+
+    def timed(fn):
+        t0 = time.perf_counter()
+        fn()
+        return time.perf_counter() - t0
+
+    (qkv_name, Nq, Kq), (_, No, Ko) = synth.LLAMA70B[0], synth.LLAMA70B[1]
+    Wq, Wo = weights_host[0], weights_host[1]
+    a8 = synth.normal_bf16((DECODE_M, Kq), seed=synth.llama_decode_act_seed(0, DECODE_M))
+    oracle.set_threads(1)
+    dt1 = timed(lambda: oracle.gemm_f64(a8, Wq))
+    oracle.set_threads(threads)
+    dtn = timed(lambda: oracle.gemm_f64(a8, Wq))
+    b = launch_bytes(DECODE_M, Nq, Kq)
+    res["decode_qkv_M8"] = {"GB/s_all_threads": round(b / dtn / 1e9, 3), "GB/s_1_thread": round(b / dt1 / 1e9, 3)}
+    # prefill: 64 of the 2048 rows through the O projection, extrapolated
+    a64 = synth.normal_bf16((64, Ko), seed=synth.llama_prefill_act_seed(1))[:64]
+    dt = timed(lambda: oracle.gemm_f64(a64, Wo))
+    res["prefill_o_M2048_extrapolated"] = {"TFLOP/s": round(2 * 64 * No * Ko / dt / 1e12, 5),
+                                           "sample": "64 rows of M = 2048, O projection"}
+    # the Qwen MoE layer at 64 tokens: attention q, k, v, o and every routed expert
+    Mt, H = synth.QWEN_TOKENS, synth.QWEN_HIDDEN
+    routing = synth.moe_routing()
+    offsets, ids = synth.moe_tables(routing)
+    hidden = synth.normal_bf16((Mt, H), seed=synth.QWEN_SEED_HIDDEN)
+    attn_out = synth.normal_bf16((Mt, 4096), seed=synth.QWEN_SEED_ATTN_O_IN)
+    down_in = synth.normal_bf16((int(offsets[-1]), synth.QWEN_DOWN[1]), seed=synth.QWEN_SEED_DOWN_IN)
+    attn = [synth.normal_bf16((N, K), seed=synth.qwen_attn_seed(i), sigma=synth.W_SIGMA)
+            for i, (_, N, K) in enumerate(synth.QWEN_ATTN)]
+    touched = [e for e in range(synth.QWEN_EXPERTS) if offsets[e + 1] > offsets[e]]
+    gu = {e: synth.normal_bf16(synth.QWEN_GATE_UP, seed=synth.qwen_gate_up_seed(e), sigma=synth.W_SIGMA)
+          for e in touched}
+    dn = {e: synth.normal_bf16(synth.QWEN_DOWN, seed=synth.qwen_down_seed(e), sigma=synth.W_SIGMA) for e in touched}
+    Wg = [gu.get(e, gu[touched[0]]) for e in range(synth.QWEN_EXPERTS)]
+    Wd = [dn.get(e, dn[touched[0]]) for e in range(synth.QWEN_EXPERTS)]
+
+    def moe():
+        for W, (_, N, K) in zip(attn, synth.QWEN_ATTN):
+            oracle.gemm_f64(hidden if K == H else attn_out, W)
+        oracle.grouped_swiglu_f64(hidden, ids, offsets, Wg)
+        oracle.grouped_gemm_f64(down_in, None, offsets, Wd)
+    dt = timed(moe)
+    moe_bytes = sum(2 * W.size for W in attn) + len(touched) * 2 * (Wg[touched[0]].size + Wd[touched[0]].size)
+    res["moe_qwen3_30b_a3b_layer"] = {"GB/s": round(moe_bytes / dt / 1e9, 3), "s": round(dt, 2)}
+    # repack of the O weight (byte permutation, Eq. 2)
+    dt = timed(lambda: oracle.repack(Wo, G, BR))
+    res["repack_o"] = {"GB/s": round(4 * No * Ko / dt / 1e9, 3)}
+    # exact read amplification by enumeration: the tiny config's row-major case
+    dt = timed(lambda: oracle.read_amp(16, 1024, 1024, 64, 64, 64, oracle.NK_ROW, G, s=2, layout_G=G, block_rows=BR))
+    res["read_amp_enumeration_tiny_ms"] = round(dt * 1e3, 2)
+    return res
+
+
 def layout_comparison(ctx, weights_tm, weights_rm):
     """The M = 8 layer over tile-major weights (block fetch), row-major weights
     read natively, and row-major weights read in whole 4 KB blocks.  Each case
@@ -701,6 +768,9 @@ def main():
                "kind": "oracle",
                "sample": f"{layers} full decode layers (4 GEMMs each, M={DECODE_M}, row-major weights), fp64, "
                          f"{dt:.1f} s"}
+        if extras is not None:
+            extras["cpu_oracle"] = cpu_oracle_timings(ctx, weights_host, threads)
+            log(f"cpu oracle timings: {extras['cpu_oracle']}")
 
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4),

@@ -103,6 +103,13 @@ def _load():
     return lib
 
 
+def set_threads(n: int) -> None:
+    """OpenMP threads of the oracle's parallel loops (for timing only: every
+    output element is summed by one thread in a fixed order, so results do
+    not depend on it)."""
+    _load().omp_set_num_threads(ctypes.c_int(int(n)))
+
+
 def _ptr(a: np.ndarray) -> int:
     assert a.flags["C_CONTIGUOUS"]
     return a.ctypes.data
