@@ -3,6 +3,7 @@ than itself -- a value the paper prints, a numpy library routine, a closed form,
 or an invariant -- so that a dropped term, a wrong sign or index, or a transposed
 operand in the oracle fails at least one of them.  CPU only."""
 import itertools
+import os
 import math
 
 import numpy as np
@@ -588,3 +589,18 @@ def test_stacked_strips_are_contiguous():
         got = np.concatenate([oracle.repack(x, G, br).reshape(-1) for x in parts])
         assert np.array_equal(got, want)
         assert np.array_equal(oracle.repack(stacked, G, br).reshape(-1), want)
+
+
+def test_oracle_thread_count_does_not_change_results():
+    """Each output element is summed by one thread in ascending k, so the
+    oracle's fp64 results are bit-identical for any OpenMP thread count."""
+    A = synth.normal_bf16((5, 777), seed=91)
+    W = synth.normal_bf16((301, 777), seed=92, sigma=synth.W_SIGMA)
+    try:
+        oracle.set_threads(1)
+        one = oracle.gemm_f64(A, W)
+        oracle.set_threads(4)
+        four = oracle.gemm_f64(A, W)
+    finally:
+        oracle.set_threads(os.cpu_count() or 1)
+    assert np.array_equal(one, four)
