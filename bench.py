@@ -170,7 +170,7 @@ def cpu_oracle_timings(ctx, weights_host, threads):
     b = launch_bytes(DECODE_M, Nq, Kq)
     res["decode_qkv_M8"] = {"GB/s_all_threads": round(b / dtn / 1e9, 3), "GB/s_1_thread": round(b / dt1 / 1e9, 3)}
     # prefill: 64 of the 2048 rows through the O projection, extrapolated
-    a64 = synth.normal_bf16((64, Ko), seed=synth.llama_prefill_act_seed(1))[:64]
+    a64 = synth.normal_bf16((64, Ko), seed=synth.llama_prefill_act_seed(1))
     dt = timed(lambda: oracle.gemm_f64(a64, Wo))
     res["prefill_o_M2048_extrapolated"] = {"TFLOP/s": round(2 * 64 * No * Ko / dt / 1e12, 5),
                                            "sample": "64 rows of M = 2048, O projection"}
