@@ -1,0 +1,95 @@
+"""Seeded random sweep of tl_gemm against the oracle: shapes (ragged M, N and K,
+padded tile-major copies), memory tiles, layouts, fetch modes, tiles, split
+counts and output types drawn together, so that combinations the targeted
+tests do not name are exercised too.  Cases the planner rejects
+(TL_EUNSUPPORTED) are counted and skipped; everything it accepts must pass the
+parity gate (fp32 out) or match the bf16 rounding of the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_04031_amd as tl
+from paper_2607_04031_amd import synth
+from tests._gpu import banner, dev_bf16, host_bits, host_f32, parity, parity_bf16_out
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+    assert torch.cuda.is_available()
+    tl.load_library()
+    yield
+    torch.cuda.empty_cache()
+
+
+def draw(rng, decode):
+    G = int(rng.choice([512, 1024, 4096, 16384]))
+    br = int(rng.choice([b for b in (4, 8, 16, 32, 64) if G // (2 * b) >= 8]))
+    M = int(rng.integers(1, 65)) if decode else int(rng.integers(65, 1500))
+    N = int(rng.integers(1, 3000))
+    K = 8 * int(rng.integers(1, 600))
+    kind = tl.TL_LAYOUT_TILE if rng.random() < 0.8 else tl.TL_LAYOUT_NK_ROW
+    fetch = tl.TL_FETCH_BLOCK if rng.random() < 0.7 else tl.TL_FETCH_NATIVE
+    out = tl.TL_OUT_BF16 if rng.random() < 0.3 else tl.TL_OUT_F32
+    tile_n = int(rng.choice([0, 0, 32, 64] if decode else [0, 0, 128, 256]))
+    split_k = int(rng.choice([0, 0, 0, 1, 2, 3, 5])) if decode else 0
+    d = tl.layout(kind=kind, G=G, block_rows=br, out_dtype=out, tile_n=tile_n, split_k=split_k)
+    return M, N, K, d, fetch
+
+
+def run_case(M, N, K, d, fetch, seed):
+    import torch
+    A = synth.normal_bf16((M, K), seed=seed)
+    W = synth.normal_bf16((N, K), seed=seed + 1, sigma=synth.W_SIGMA)
+    Wd = dev_bf16(W)
+    if d.kind == tl.TL_LAYOUT_TILE:
+        Wt = torch.empty(tl.padded_shape(N, K, 2, d.G, d.block_rows), dtype=torch.bfloat16, device="cuda")
+        tl.tl_repack(Wd, Wt, N, K, 2, d.G, d.block_rows)
+        Wd = Wt
+    bf16 = d.out_dtype == tl.TL_OUT_BF16
+    C = torch.full((M, N), float("nan"), dtype=torch.bfloat16 if bf16 else torch.float32, device="cuda")
+    tl.tl_gemm(dev_bf16(A), Wd, C, M, N, K, d, fetch)
+    torch.cuda.synchronize()
+    y_ref = oracle.gemm_f64(A, W)
+    what = f"M={M} N={N} K={K} kind={d.kind} G={d.G} br={d.block_rows} tn={d.tile_n} S={d.split_k} bf16={bf16}"
+    if bf16:
+        parity_bf16_out(host_bits(C), y_ref, what)
+    else:
+        parity(host_f32(C), y_ref, what)
+
+
+@pytest.mark.parametrize("decode", [True, False])
+def test_random_gemm_cases(decode):
+    rng = np.random.default_rng(2024 if decode else 2025)
+    ran = skipped = 0
+    for case in range(60 if decode else 24):
+        M, N, K, d, fetch = draw(rng, decode)
+        try:
+            p = tl.tl_gemm_plan(M, N, K, d, fetch)
+        except tl.TLError as e:
+            assert e.status == tl.TL_EUNSUPPORTED, (M, N, K, e)
+            skipped += 1
+            continue
+        banner(f"random {'decode' if decode else 'prefill'} case {case}: M={M} N={N} K={K} G={d.G} "
+               f"br={d.block_rows} kind={d.kind} plan={p}")
+        run_case(M, N, K, d, fetch, seed=7000 + case)
+        ran += 1
+    assert ran >= (40 if decode else 12), (ran, skipped)
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_random_lds_staged_cases(case):
+    """17 <= M <= 32 on weights whose 32-row tiles fill the CUs in whole rounds
+    (the LDS-staged kernel), random M, memory tile and output type."""
+    rng = np.random.default_rng(3000 + case)
+    M = int(rng.integers(17, 33))
+    N, K = [(32768, 2048), (8192, 8192), (10240, 8192), (8192, 4096 * 7)][case % 4]
+    G = int(rng.choice([1024, 4096, 16384]))
+    br = int(rng.choice([b for b in (8, 16, 32) if G // (2 * b) <= 512]))
+    d = tl.layout(G=G, block_rows=br, out_dtype=tl.TL_OUT_BF16 if case % 3 == 2 else tl.TL_OUT_F32)
+    p = tl.tl_gemm_plan(M, N, K, d)
+    assert p["waves"] == 8 and p["tile_n"] == 32, p
+    banner(f"random lds case {case}: M={M} N={N} K={K} G={G} br={br} plan={p}")
+    run_case(M, N, K, d, tl.TL_FETCH_BLOCK, seed=8000 + case)
