@@ -1,4 +1,4 @@
-"""Seeded random sweep of tl_gemm against the oracle: shapes (ragged M, N and K,
+"""Seeded random sweeps against the oracle.  tl_gemm: shapes (ragged M, N and K,
 padded tile-major copies), memory tiles, layouts, fetch modes, tiles, split
 counts and output types drawn together, so that combinations the targeted
 tests do not name are exercised too.  Cases the planner rejects
@@ -93,3 +93,54 @@ def test_random_lds_staged_cases(case):
     assert p["waves"] == 8 and p["tile_n"] == 32, p
     banner(f"random lds case {case}: M={M} N={N} K={K} G={G} br={br} plan={p}")
     run_case(M, N, K, d, tl.TL_FETCH_BLOCK, seed=8000 + case)
+
+
+def dev_i32(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+
+
+@pytest.mark.parametrize("swiglu", [False, True])
+def test_random_grouped_cases(swiglu):
+    """Random group tables (empty groups, groups larger than the M tile), ids,
+    weight shapes, memory tiles and output types for tl_gemm_grouped and
+    tl_gemm_grouped_swiglu."""
+    import torch
+    rng = np.random.default_rng(4000 + swiglu)
+    for case in range(12):
+        E = int(rng.integers(1, 10))
+        counts = [int(rng.choice([0, 1, 3, 9, 17, 40])) for _ in range(E)]
+        offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+        T = int(offsets[-1])
+        if T == 0:
+            continue
+        a_rows = int(rng.integers(1, 50))
+        ids = rng.integers(0, a_rows, size=T).astype(np.int32)
+        G = int(rng.choice([1024, 4096]))
+        br = int(rng.choice([8, 16, 32]))
+        K = 8 * int(rng.integers(1, 300))
+        N = 32 * int(rng.integers(1, 20)) if swiglu else int(rng.integers(1, 700))
+        rows_w = 2 * N if swiglu else N
+        bf16 = rng.random() < 0.4
+        d = tl.layout(G=G, block_rows=br, out_dtype=tl.TL_OUT_BF16 if bf16 else tl.TL_OUT_F32)
+        max_rows = max(counts) + int(rng.integers(0, 5))
+        A = synth.normal_bf16((a_rows, K), seed=9000 + case)
+        Ws = [synth.normal_bf16((rows_w, K), seed=9100 + 10 * case + e, sigma=synth.W_SIGMA) for e in range(E)]
+        stride = tl.tl_tile_bytes(rows_w, K, 2, G, br)
+        stride = (stride + 15) // 16 * 16
+        stack = torch.zeros(E * stride // 2, dtype=torch.bfloat16, device="cuda")
+        for e, W in enumerate(Ws):
+            part = stack[e * stride // 2:(e + 1) * stride // 2]
+            tl.tl_repack(dev_bf16(W), part, rows_w, K, 2, G, br)
+        C = torch.full((T, N), float("nan"), dtype=torch.bfloat16 if bf16 else torch.float32, device="cuda")
+        banner(f"random grouped swiglu={swiglu} case {case}: E={E} counts={counts} N={N} K={K} G={G} br={br}")
+        fn = tl.tl_gemm_grouped_swiglu if swiglu else tl.tl_gemm_grouped
+        fn(dev_bf16(A), a_rows, dev_i32(ids), dev_i32(offsets), E, T, max_rows, stack, stride, C, N, K, d,
+           tl.TL_FETCH_BLOCK)
+        torch.cuda.synchronize()
+        ref = (oracle.grouped_swiglu_f64 if swiglu else oracle.grouped_gemm_f64)(A, ids, offsets, Ws)
+        what = f"grouped swiglu={swiglu} case {case}"
+        if bf16:
+            parity_bf16_out(host_bits(C), ref, what)
+        else:
+            parity(host_f32(C), ref, what)
