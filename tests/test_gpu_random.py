@@ -3,7 +3,8 @@ padded tile-major copies), memory tiles, layouts, fetch modes, tiles, split
 counts and output types drawn together, so that combinations the targeted
 tests do not name are exercised too.  Cases the planner rejects
 (TL_EUNSUPPORTED) are counted and skipped; everything it accepts must pass the
-parity gate (fp32 out) or match the bf16 rounding of the oracle."""
+parity gate (fp32 out) or match the bf16 rounding of the oracle.  The grouped
+launches: random group tables, ids, weights and memory tiles."""
 import numpy as np
 import pytest
 
