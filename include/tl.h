@@ -180,9 +180,11 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  *      every layout->G-byte block a K step touches, whole (decode kernel only;
  *      G a power of two, 128 <= G <= 2^30): the amplification of Section 2.5
  *      paid as real HBM traffic, and tallied by TL_FETCH_COUNT.
- * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound); larger M runs the
- * prefill kernel (bf16 MFMA tiles 256x256x64, 256x128x64 or 128x128x64,
- * MFMA-bound).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
+ * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound; at 17 <= M <= 32
+ * on tile-major weights whose 32-row tiles and 512-column K chunks fill the
+ * CUs in whole rounds, a variant that stages the activations in LDS and
+ * shares them across several tiles); larger M runs the prefill kernel (bf16
+ * MFMA tiles 256x256x64, 256x128x64 or 128x128x64, MFMA-bound).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
  * byte per element, e.g. 64 x 64 memory tiles of 4 KB, Section 3.1): decode
  * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
  * per-channel scales).
