@@ -1,0 +1,89 @@
+"""Library state per (device, stream): split-K calls from several host threads,
+each on its own stream with its own workspace, run concurrently and give the
+results of the same calls made alone; tl_release frees that state and the
+next call re-creates it."""
+import threading
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_04031_amd as tl
+from paper_2607_04031_amd import synth
+from tests._gpu import banner, dev_bf16, host_f32, parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+    assert torch.cuda.is_available()
+    tl.load_library()
+    yield
+    torch.cuda.synchronize()
+
+
+def _case(i):
+    M, N, K = [(8, 1024, 4096), (32, 8192, 8192), (1, 512, 8192), (17, 2048, 4096)][i % 4]
+    A = synth.normal_bf16((M, K), seed=500 + i)
+    W = synth.normal_bf16((N, K), seed=600 + i, sigma=synth.W_SIGMA)
+    return M, N, K, A, W
+
+
+def test_threads_on_separate_streams():
+    import torch
+    banner("split-K calls from 4 host threads on 4 streams")
+    cases = [_case(i) for i in range(4)]
+    dev = []
+    for (M, N, K, A, W) in cases:
+        Wd = dev_bf16(W)
+        Wt = torch.empty_like(Wd)
+        tl.tl_repack(Wd, Wt, N, K, 2, 4096, 32)
+        dev.append((dev_bf16(A), Wt))
+    torch.cuda.synchronize()
+    want = [oracle.gemm_f64(A, W) for (_, _, _, A, W) in cases]
+    outs = [None] * 4
+    errors = []
+
+    def worker(i):
+        try:
+            M, N, K, _, _ = cases[i]
+            A, Wt = dev[i]
+            s = torch.cuda.Stream()
+            C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+            with torch.cuda.stream(s):
+                for _ in range(20):                     # repeated: the workspace is reused on its stream
+                    tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(split_k=4), tl.TL_FETCH_BLOCK, stream=s)
+            s.synchronize()
+            outs[i] = host_f32(C)
+        except Exception as e:                          # reported on the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for i in range(4):
+        parity(outs[i], want[i], f"thread {i}")
+
+
+def test_release_then_reuse():
+    import torch
+    banner("tl_release, then a split-K call re-creates the state")
+    M, N, K, A, W = _case(0)
+    Wd = dev_bf16(W)
+    Wt = torch.empty_like(Wd)
+    tl.tl_repack(Wd, Wt, N, K, 2, 4096, 32)
+    C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    tl.tl_gemm(dev_bf16(A), Wt, C, M, N, K, tl.layout(split_k=4), tl.TL_FETCH_BLOCK)
+    torch.cuda.synchronize()
+    first = host_f32(C)
+    tl.tl_release()
+    C2 = torch.empty_like(C)
+    tl.tl_gemm(dev_bf16(A), Wt, C2, M, N, K, tl.layout(split_k=4), tl.TL_FETCH_BLOCK)
+    torch.cuda.synchronize()
+    assert np.array_equal(host_f32(C2), first)
+    parity(first, oracle.gemm_f64(A, W), "after release")
