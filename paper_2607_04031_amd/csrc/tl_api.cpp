@@ -256,18 +256,26 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         // 17 <= M <= 32 on whole tile-major strips: stage the activations in
         // LDS, one 8-wave workgroup per CU taking T of the 32-row tiles and
         // one of S K ranges, when the (T, S) grid covers the CUs in whole
-        // rounds (A crosses L2 -> CU once per T tiles instead of once per tile)
+        // rounds (A crosses L2 -> CU once per T tiles instead of once per
+        // tile) -- unless its K ranges are short (under 8 chunks, so its
+        // staging and wave reduction weigh more) while the streaming plan
+        // already has one or two workgroups per CU (Llama O at M = 32:
+        // 29.8 vs 29.0 us; QKV, whose streaming plan needs 1120 workgroups,
+        // 35.6 vs 43.0; down 81.7 vs 84.1; gate+up 150.9 vs 181.4)
         if (tile && !p.fp8 && p.m_tiles16 == 2 && !d->tile_n && !d->split_k && N % 32 == 0 && K % 512 == 0 &&
             p.L.br <= 32 && 512 % p.k_unit == 0) {
             const int64_t strips = N / 32, chunks = K / 512;
-            for (int T = 7; T >= 4 && !p.lds_tiles; --T) {
+            bool found = false;   // the first whole-round (T, S) decides
+            for (int T = 7; T >= 4 && !found; --T) {
                 if (strips % T) continue;
-                for (int64_t s2 = 1; s2 <= 8 && chunks / s2 >= 4; s2 *= 2) {
+                for (int64_t s2 = 1; s2 <= 8 && chunks / s2 >= 4 && !found; s2 *= 2) {
                     const int64_t w = strips / T * s2;
                     if (w % kCUs == 0 && w <= 4 * kCUs) {
-                        p.lds_tiles = T;
-                        S = s2;
-                        break;
+                        found = true;
+                        if (s2 == 1 || chunks / s2 >= 8 || wgs > 2 * kCUs) {
+                            p.lds_tiles = T;
+                            S = s2;
+                        }
                     }
                 }
             }

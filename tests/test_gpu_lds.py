@@ -48,7 +48,7 @@ def run(A_bits, W_bits, d, fetch=tl.TL_FETCH_BLOCK):
 # (M, N, K): tiles per workgroup T and K splits S the planner picks
 LDS_SHAPES = [
     (32, 32768, 2048),     # T = 4, S = 1
-    (17, 8192, 8192),      # T = 4, S = 4 (Llama O at M = 17)
+    (17, 8192, 16384),     # T = 4, S = 4, 8 chunks per split
     (24, 10240, 8192),     # T = 5, S = 4 (Llama QKV)
     (32, 57344, 2048),     # T = 7, S = 1 (Llama gate+up rows)
     (20, 8192, 28672),     # T = 4, S = 4, 14 chunks per split (Llama down)
@@ -70,7 +70,7 @@ def test_lds_decode_exact_inputs_and_reproducible(M):
     """Small integers: every partial sum is an exact fp32 integer, so the
     result equals the oracle bit for bit (split-K partials included); one-hot
     rows pick single weights; two runs are bitwise identical."""
-    N, K = 8192, 8192
+    N, K = 8192, 16384
     d = tl.layout()
     lds_plan(M, N, K, d)
     banner(f"lds decode exact M={M}")
@@ -85,7 +85,7 @@ def test_lds_decode_exact_inputs_and_reproducible(M):
 
 
 def test_lds_decode_bf16_output():
-    M, N, K = 32, 8192, 8192
+    M, N, K = 32, 8192, 16384
     d = tl.layout(out_dtype=tl.TL_OUT_BF16)
     lds_plan(M, N, K, d)
     banner("lds decode bf16 out")

@@ -455,7 +455,7 @@ def test_graph_replay_matches_eager():
     side = torch.cuda.Stream()
     # the last two take the LDS-staged decode kernel (split-K 4 with its reduce, and unsplit)
     cases = [(8, 1024, 2048, 1), (8, 1024, 2048, 4), (32, 512, 4096, 3), (256, 512, 1024, 0),
-             (32, 8192, 8192, 0), (24, 32768, 2048, 0)]
+             (32, 8192, 16384, 0), (24, 32768, 2048, 0)]
     with torch.cuda.stream(side):
         tensors = []
         for i, (M, N, K, S) in enumerate(cases):

@@ -86,7 +86,7 @@ def test_random_lds_staged_cases(case):
     (the LDS-staged kernel), random M, memory tile and output type."""
     rng = np.random.default_rng(3000 + case)
     M = int(rng.integers(17, 33))
-    N, K = [(32768, 2048), (8192, 8192), (10240, 8192), (8192, 4096 * 7)][case % 4]
+    N, K = [(32768, 2048), (8192, 16384), (10240, 8192), (8192, 4096 * 7)][case % 4]
     G = int(rng.choice([1024, 4096, 16384]))
     br = int(rng.choice([b for b in (8, 16, 32) if G // (2 * b) <= 512]))
     d = tl.layout(G=G, block_rows=br, out_dtype=tl.TL_OUT_BF16 if case % 3 == 2 else tl.TL_OUT_F32)

@@ -157,12 +157,17 @@ def test_gemm_plan_decode_and_prefill_shapes():
         assert (p["tile_n"], p["split_k"], p["workgroups"]) == (32, 2, 256)
     # 17 <= M <= 32 on the Llama shapes: activations staged in LDS, one 8-wave
     # workgroup per CU taking T 32-row tiles (whole strips) x one of S K ranges
-    for N, K, S in [(10240, 8192, 4), (8192, 8192, 4), (57344, 8192, 1), (8192, 28672, 4)]:
+    for N, K, S in [(10240, 8192, 4), (57344, 8192, 1), (8192, 28672, 4), (8192, 16384, 4)]:
         for M in (17, 32):
             p = tl.tl_gemm_plan(M, N, K, d)
             assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (32, S, 8, 256)
             amp = tl.tl_read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, 4096)
             assert amp["amp"] == 1.0
+    # ... but not when its K ranges are short (4 chunks of 512) and the
+    # streaming plan already fills the CUs once: Llama O
+    for M in (17, 32):
+        p = tl.tl_gemm_plan(M, 8192, 8192, d)
+        assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (64, 2, 8, 256)
     # a fixed tile or split keeps the streaming kernel: 128 tiles of 64 rows,
     # K split in two, one 8-wave workgroup per CU
     p = tl.tl_gemm_plan(32, 8192, 8192, tl.layout(tile_n=64))
