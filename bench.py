@@ -19,7 +19,8 @@ library's plan, and tiles 256x256x64, 256x128x64, 128x128x64 pinned; bf16 out); 
 layer (64 tokens, top-8 of 128 experts, plus the attention projections);
 the layer with FP8 weights (64 x 64 memory tiles); the TileLens-HW view load
 of an 8192 x 8192 box (2-D and 4-D views); the
-gate+up GEMM on an emulated fixed-latency memory against Eq. 6;
+gate+up GEMM on an emulated fixed-latency memory against Eq. 6; one GPU's
+share of the M = 8 layer under tensor parallelism of degree 2, 4 and 8;
 read amplification of the decode tile and of the paper's 128 x 256 tile;
 repack GB/s; the decode kernel's roofline; the CPU oracle on a bounded sample.
 
@@ -509,6 +510,119 @@ def lgms_sweep(ctx, weights):
     return res
 
 
+TP_DEGREES = (2, 4, 8)
+
+
+def tp_shard_layers(ctx, weights, steps, warmup):
+    """One GPU's share of the M = 8 decode layer under tensor parallelism of
+    degree TP = 2, 4 and 8: QKV and gate+up split by output rows, O and down
+    by input columns; the all-reduce after O and down is not one GPU's work
+    and is left out.  A row shard of a tile-major weight is a zero-copy byte
+    range (a strip of block_rows rows is contiguous); a column shard is
+    repacked on its own from the row-major column block (unpacked from the
+    tile-major weight on the GPU).  Step s runs rank s mod TP's share, so
+    consecutive steps read different weights: every TP steps read the whole
+    layer (1.71 GB) once, and no share is still in the 256 MB last-level cache
+    when it comes round again.  Per TP: eager and graph-replayed GB/s
+    (algorithmic bytes), per-shape microseconds from HIP events, the plans,
+    and the same shares read by tl_stream_read (graph-replayed) as the
+    ceiling."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    M = DECODE_M
+    desc = tl.layout(G=G, block_rows=BR)
+    ck = torch.zeros(1, dtype=torch.int32, device=ctx.dev)
+    res = {}
+    for tp in TP_DEGREES:
+        shards = []      # per shape: (name, Nr, Kr, [rank weights], A, C)
+        for i, (name, N, K, Wt) in enumerate(weights):
+            if name in ("qkv", "gate_up"):
+                Nr, Kr = N // tp, K
+                parts = [Wt.view(-1).narrow(0, r * Nr * K, Nr * K) for r in range(tp)]
+            else:
+                Nr, Kr = N, K // tp
+                rm = torch.empty_like(Wt)
+                tl.tl_unpack(Wt, rm, N, K, 2, G, BR)
+                parts = []
+                for r in range(tp):
+                    blk = rm[:, r * Kr:(r + 1) * Kr].contiguous()
+                    part = torch.empty_like(blk)
+                    tl.tl_repack(blk, part, N, Kr, 2, G, BR)
+                    parts.append(part)
+                    del blk
+                del rm
+            A = ctx.to_dev(synth.normal_bf16((M, Kr), seed=synth.llama_decode_act_seed(i, M)))
+            C = torch.empty((M, Nr), dtype=torch.float32, device=ctx.dev)
+            shards.append((name, Nr, Kr, parts, A, C))
+        step_bytes = sum(launch_bytes(M, Nr, Kr) for (_, Nr, Kr, _, _, _) in shards)
+
+        def rank_step(r, ev=None):
+            for j, (_, Nr, Kr, parts, A, C) in enumerate(shards):
+                if ev is not None:
+                    ev[j][0].record(ctx.stream)
+                tl.tl_gemm(A, parts[r], C, M, Nr, Kr, desc, tl.TL_FETCH_BLOCK)
+                if ev is not None:
+                    ev[j][1].record(ctx.stream)
+
+        def round_all():
+            for r in range(tp):
+                rank_step(r)
+
+        def round_read():
+            for r in range(tp):
+                for (_, Nr, Kr, parts, _, _) in shards:
+                    tl.tl_stream_read(parts[r], 2 * Nr * Kr, ck)
+
+        rounds = max(1, steps // tp)
+        for _ in range(max(1, warmup // tp)):
+            round_all()
+        wall = wall_time(ctx, round_all, rounds)
+
+        def graph_ms(fn):
+            fn()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=ctx.stream):
+                fn()
+            for _ in range(3):
+                g.replay()
+            ev = ctx.event_pairs(1)[0]
+            ev[0].record(ctx.stream)
+            for _ in range(rounds):
+                g.replay()
+            ev[1].record(ctx.stream)
+            torch.cuda.synchronize()
+            del g
+            return ev[0].elapsed_time(ev[1]) / (rounds * tp)
+
+        gemm_ms = graph_ms(round_all)
+        read_ms = graph_ms(round_read)
+        # per call: HIP events around each tl_gemm over the timed rounds,
+        # launched back to back so the queue stays ahead of the GPU
+        evs = [ctx.event_pairs(len(shards)) for _ in range(rounds * tp)]
+        for n, e in enumerate(evs):
+            rank_step(n % tp, e)
+        torch.cuda.synchronize()
+        per_shape = {}
+        for j, (name, Nr, Kr, _, _, _) in enumerate(shards):
+            p = tl.tl_gemm_plan(M, Nr, Kr, desc)
+            per_shape[name] = {"shape": [Nr, Kr],
+                               "us": round(sum(e[j][0].elapsed_time(e[j][1]) for e in evs) / len(evs) * 1e3, 2),
+                               "tile_n": p["tile_n"], "split_k": p["split_k"], "waves": p["waves"],
+                               "workgroups": p["workgroups"]}
+        graph_gbs = step_bytes / (gemm_ms * 1e-3) / 1e9
+        read_gbs = sum(2 * Nr * Kr for (_, Nr, Kr, _, _, _) in shards) / (read_ms * 1e-3) / 1e9
+        res[f"tp{tp}"] = {"weight_MB_per_gpu": round(sum(2 * Nr * Kr for (_, Nr, Kr, _, _, _) in shards) / 1e6, 1),
+                          "eager_GB/s": round(step_bytes * rounds * tp / wall / 1e9, 1),
+                          "graph_GB/s": round(graph_gbs, 1), "us_per_step_graph": round(gemm_ms * 1e3, 2),
+                          "frac_hbm_peak": round(graph_gbs / HBM_PEAK_GBS, 4),
+                          "read_ceiling_GB/s": round(read_gbs, 1), "read_us_per_step": round(read_ms * 1e3, 2),
+                          "per_shape": per_shape}
+        log(f"tp{tp} share of the M={M} layer: {res[f'tp{tp}']}")
+        del shards
+        torch.cuda.empty_cache()
+    return res
+
+
 def view_load(ctx, weights):
     """tl_view_load of an 8192 x 8192 bf16 box of the down weight (K x N
     order: 8192 contiguous elements x 8192 columns), as a 2-D view and as an
@@ -721,6 +835,7 @@ def main():
         torch.cuda.empty_cache()
         extras["view_load"] = view_load(ctx, weights)
         extras["lgms_emulation"] = lgms_sweep(ctx, weights)
+        extras["tp_shard_decode_M8"] = tp_shard_layers(ctx, weights, args.steps, args.warmup)
 
     # ---------------- read amplification ----------------
     plan = tl.tl_gemm_plan(DECODE_M, 8192, 8192, desc, tl.TL_FETCH_BLOCK)

@@ -205,7 +205,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         if (tn != 32 && tn != 64) return TL_EUNSUPPORTED;
         if (tile && tn % p.L.br) return TL_EUNSUPPORTED;
         if (d->tile_k && (d->tile_k != p.k_unit)) return TL_EUNSUPPORTED;
-        const int64_t n_tiles = (N + tn - 1) / tn;
+        int64_t n_tiles = (N + tn - 1) / tn;
         const int64_t units = (K + p.k_unit - 1) / p.k_unit;
         // Balance: every CU should stream the same number of bytes.
         //  - at least two tiles per CU: one workgroup per tile, K not split
@@ -218,6 +218,13 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         //    CU, whose 8 or 16 waves split K among themselves (reduced in
         //    LDS), or four per CU when each K split still streams >= 4096 K
         //    (the reduce launch then costs a few per cent at most);
+        //  - fewer tiles than two rounds that do not divide the CUs: the
+        //    32- or 64-row tile and K split that fill one round of the CUs
+        //    to at least 7/8 (one workgroup per CU, its waves splitting K
+        //    too), as for tiles that divide the CUs -- measured on the
+        //    tensor-parallel shards of the Llama-70B shapes (40 - 448 tiles:
+        //    gate+up / 4 at M = 8 43.9 -> 37.9 us, QKV / 4 at M = 32
+        //    19.7 -> 14.7; equal fills take 64-row tiles above M = 16);
         //  - otherwise split K until there are about 1024 workgroups.
         // K splits write fp32 partials that a fixed-order reduce kernel sums;
         // every split covers >= 1024 K (>= 512 for a small weight).  (Chosen
@@ -236,7 +243,28 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                 if (K / (4 * S) >= 4096) S *= 4;
                 S = std::min(S, max_s);
             } else {
-                S = std::min((kTargetWorkgroups + n_tiles - 1) / n_tiles, max_s);
+                int best_tn = 0;
+                int64_t best_w = 0, best_s = 0;
+                const int prefer = p.m_tiles16 >= 2 ? 64 : 32;
+                for (int c : {32, 64}) {
+                    if (d->tile_n ? c != tn : (c == 64 && N % 64)) continue;
+                    if (tile && c % p.L.br) continue;
+                    const int64_t nt = (N + c - 1) / c;
+                    const int64_t sc = std::min<int64_t>(kCUs / nt, max_s);
+                    if (sc < 1) continue;
+                    if (nt * sc > best_w || (nt * sc == best_w && c == prefer)) {
+                        best_tn = c;
+                        best_w = nt * sc;
+                        best_s = sc;
+                    }
+                }
+                if (8 * best_w >= 7 * kCUs) {
+                    tn = best_tn;
+                    n_tiles = (N + tn - 1) / tn;
+                    S = best_s;
+                } else {
+                    S = std::min((kTargetWorkgroups + n_tiles - 1) / n_tiles, max_s);
+                }
             }
         }
         if (S < 1 || S > units || S > kMaxSplitK) return TL_EUNSUPPORTED;

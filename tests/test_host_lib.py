@@ -168,6 +168,18 @@ def test_gemm_plan_decode_and_prefill_shapes():
     for M in (17, 32):
         p = tl.tl_gemm_plan(M, 8192, 8192, d)
         assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (64, 2, 8, 256)
+    # tiles that neither fill two rounds of the CUs nor divide them (one
+    # GPU's share of the Llama shapes under tensor parallelism): the 32- or
+    # 64-row tile and K split that fill one round to >= 7/8, one workgroup per
+    # CU; full QKV (320 or 160 tiles, under 7/8) keeps about 1024 workgroups
+    for M, N, K, tn, S, wgs in [(8, 2560, 8192, 32, 3, 240), (32, 2560, 8192, 64, 6, 240),
+                                (1, 1280, 8192, 32, 6, 240), (32, 1280, 8192, 64, 12, 240),
+                                (8, 14336, 8192, 64, 1, 224), (32, 14336, 8192, 64, 1, 224),
+                                (8, 7168, 8192, 32, 1, 224), (32, 7168, 8192, 64, 2, 224),
+                                (8, 5120, 8192, 64, 3, 240), (64, 5120, 2048, 64, 3, 240)]:
+        p = tl.tl_gemm_plan(M, N, K, d)
+        assert (p["tile_n"], p["split_k"], p["workgroups"]) == (tn, S, wgs), (M, N, K, p)
+    assert tl.tl_gemm_plan(8, 10240, 8192, d)["workgroups"] == 1280
     # a fixed tile or split keeps the streaming kernel: 128 tiles of 64 rows,
     # K split in two, one 8-wave workgroup per CU
     p = tl.tl_gemm_plan(32, 8192, 8192, tl.layout(tile_n=64))
