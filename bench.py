@@ -26,6 +26,7 @@ repack GB/s; the decode kernel's roofline; the CPU oracle on a bounded sample.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
     python bench.py --sweep      # memory-tile granularity sweep, its own JSON line
+    python bench.py --tp         # tensor-parallel shares only, its own JSON line
 """
 import argparse
 import hashlib
@@ -715,6 +716,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip M=1/32, the layout comparison and the MoE layer")
     ap.add_argument("--sweep", action="store_true", help="run only the memory-tile granularity sweep")
+    ap.add_argument("--tp", action="store_true",
+                    help="run only one GPU's share of the M=8 layer under tensor parallelism (TP 2, 4, 8)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -751,6 +754,10 @@ def main():
         if not args.no_cpu_baseline:
             weights_host.append(bits)
         del bits
+
+    if args.tp:
+        print(json.dumps({"tp_shard_decode_M8": tp_shard_layers(ctx, weights, args.steps, args.warmup)}), flush=True)
+        return
 
     # ---------------- timed region: K eager steps of the M = 8 layer ---------
     log(f"warmup {args.warmup} steps, timing {args.steps} steps")
