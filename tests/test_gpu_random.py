@@ -5,6 +5,8 @@ tests do not name are exercised too.  Cases the planner rejects
 (TL_EUNSUPPORTED) are counted and skipped; everything it accepts must pass the
 parity gate (fp32 out) or match the bf16 rounding of the oracle.  The grouped
 launches: random group tables, ids, weights and memory tiles."""
+import os
+
 import numpy as np
 import pytest
 
@@ -14,6 +16,8 @@ from paper_2607_04031_amd import synth
 from tests._gpu import banner, dev_bf16, host_bits, host_f32, parity, parity_bf16_out
 
 pytestmark = pytest.mark.gpu
+# TL_RANDOM_SCALE=n runs n times as many tl_gemm draws (further seeds)
+SCALE = max(1, int(os.environ.get("TL_RANDOM_SCALE", "1")))
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -65,7 +69,7 @@ def run_case(M, N, K, d, fetch, seed):
 def test_random_gemm_cases(decode):
     rng = np.random.default_rng(2024 if decode else 2025)
     ran = skipped = 0
-    for case in range(60 if decode else 24):
+    for case in range((60 if decode else 24) * SCALE):
         M, N, K, d, fetch = draw(rng, decode)
         try:
             p = tl.tl_gemm_plan(M, N, K, d, fetch)
@@ -77,7 +81,7 @@ def test_random_gemm_cases(decode):
                f"br={d.block_rows} kind={d.kind} plan={p}")
         run_case(M, N, K, d, fetch, seed=7000 + case)
         ran += 1
-    assert ran >= (40 if decode else 12), (ran, skipped)
+    assert ran >= (40 if decode else 12) * SCALE, (ran, skipped)
 
 
 @pytest.mark.parametrize("case", range(6))
