@@ -16,7 +16,7 @@ from paper_2607_04031_amd import synth
 from tests._gpu import banner, dev_bf16, host_bits, host_f32, parity, parity_bf16_out
 
 pytestmark = pytest.mark.gpu
-# TL_RANDOM_SCALE=n runs n times as many tl_gemm draws (further seeds)
+# TL_RANDOM_SCALE=n runs n times as many draws of each sweep (further seeds)
 SCALE = max(1, int(os.environ.get("TL_RANDOM_SCALE", "1")))
 
 
@@ -84,7 +84,7 @@ def test_random_gemm_cases(decode):
     assert ran >= (40 if decode else 12) * SCALE, (ran, skipped)
 
 
-@pytest.mark.parametrize("case", range(6))
+@pytest.mark.parametrize("case", range(6 * SCALE))
 def test_random_lds_staged_cases(case):
     """17 <= M <= 32 on weights whose 32-row tiles fill the CUs in whole rounds
     (the LDS-staged kernel), random M, memory tile and output type."""
@@ -112,7 +112,7 @@ def test_random_grouped_cases(swiglu):
     tl_gemm_grouped_swiglu."""
     import torch
     rng = np.random.default_rng(4000 + swiglu)
-    for case in range(12):
+    for case in range(12 * SCALE):
         E = int(rng.integers(1, 10))
         counts = [int(rng.choice([0, 1, 3, 9, 17, 40])) for _ in range(E)]
         offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
