@@ -149,3 +149,49 @@ def test_random_grouped_cases(swiglu):
             parity_bf16_out(host_bits(C), ref, what)
         else:
             parity(host_f32(C), ref, what)
+
+
+def test_random_fp8_cases():
+    """Random weight-only FP8 (OCP E4M3) decode through tl_gemm_w8: ragged M,
+    N and K (K a multiple of 16; padded tile-major copies), memory tiles,
+    layouts, split counts, per-channel scales or none, both output types."""
+    import torch
+    rng = np.random.default_rng(5000)
+    ran = skipped = 0
+    for case in range(24 * SCALE):
+        G = int(rng.choice([1024, 4096, 16384]))
+        br = int(rng.choice([b for b in (16, 32, 64, 128) if G // b >= 16]))
+        M, N, K = int(rng.integers(1, 65)), int(rng.integers(1, 2000)), 16 * int(rng.integers(1, 400))
+        kind = tl.TL_LAYOUT_TILE if rng.random() < 0.85 else tl.TL_LAYOUT_NK_ROW
+        bf16 = rng.random() < 0.3
+        split_k = int(rng.choice([0, 0, 0, 1, 2, 3]))
+        scaled = rng.random() < 0.5
+        d = tl.layout(kind=kind, elem_bytes=1, G=G, block_rows=br, split_k=split_k,
+                      out_dtype=tl.TL_OUT_BF16 if bf16 else tl.TL_OUT_F32)
+        fetch = tl.TL_FETCH_BLOCK if kind == tl.TL_LAYOUT_TILE else tl.TL_FETCH_NATIVE
+        try:
+            p = tl.tl_gemm_plan(M, N, K, d, fetch)
+        except tl.TLError as e:
+            assert e.status == tl.TL_EUNSUPPORTED, (M, N, K, e)
+            skipped += 1
+            continue
+        banner(f"random fp8 case {case}: M={M} N={N} K={K} G={G} br={br} kind={kind} scaled={scaled} plan={p}")
+        W8, sc = synth.fp8_weights((N, K), seed=5100 + case)
+        A = synth.normal_bf16((M, K), seed=5200 + case)
+        W = torch.from_numpy(np.ascontiguousarray(W8)).cuda()
+        if kind == tl.TL_LAYOUT_TILE:
+            Wt = torch.zeros(tl.tl_tile_bytes(N, K, 1, G, br), dtype=torch.uint8, device="cuda")
+            tl.tl_repack(W, Wt, N, K, 1, G, br)
+            W = Wt
+        sc_dev = torch.from_numpy(np.ascontiguousarray(sc, dtype=np.float32)).cuda() if scaled else None
+        C = torch.full((M, N), float("nan"), dtype=torch.bfloat16 if bf16 else torch.float32, device="cuda")
+        tl.tl_gemm_w8(dev_bf16(A), W, sc_dev, C, M, N, K, d, fetch)
+        torch.cuda.synchronize()
+        ref = oracle.gemm_w8_f64(A, W8, sc if scaled else None)
+        what = f"fp8 case {case}: M={M} N={N} K={K} G={G} br={br} kind={kind} S={split_k} scaled={scaled} bf16={bf16}"
+        if bf16:
+            parity_bf16_out(host_bits(C), ref, what)
+        else:
+            parity(host_f32(C), ref, what)
+        ran += 1
+    assert ran >= 12 * SCALE, (ran, skipped)
