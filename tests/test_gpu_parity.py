@@ -230,9 +230,12 @@ def test_decode_bf16_output(M):
 @pytest.mark.parametrize("br", [8, 16, 32, 64])
 def test_decode_memory_tile_shapes(G, br):
     """One library binary for every memory-tile shape (runtime descriptor)."""
-    if G // (2 * br) < 8:
-        pytest.skip("block_cols < 8 is rejected by tl_gemm (TL_EUNSUPPORTED)")
     M, N, K = 8, 256, 4096
+    if G // (2 * br) < 8:   # memory-tile rows under 16 bytes: rejected before any device work
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_plan(M, N, K, tl.layout(G=G, block_rows=br))
+        assert e.value.status == tl.TL_EUNSUPPORTED
+        return
     banner(f"decode G={G} br={br}")
     A = synth.normal_bf16((M, K), seed=13)
     W = synth.normal_bf16((N, K), seed=14, sigma=synth.W_SIGMA)
