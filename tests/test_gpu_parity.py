@@ -157,8 +157,9 @@ def test_decode_split_k_parity_and_reproducible(split_k):
 
 def test_decode_split_k_interleaved_calls():
     """Split calls of different shapes and split counts, back to back on one
-    stream: each workgroup arrival counter must be back at zero after every
-    call, so every call equals the same call made alone."""
+    stream with no synchronisation: consecutive calls share the stream's
+    split-K workspace (partials, then the reduce kernel), so every call must
+    equal the same call made alone."""
     banner("decode split-K interleaved calls")
     cases = [(8, 512, 4096, 3), (1, 1024, 2048, 7), (8, 512, 4096, 2), (32, 256, 8192, 16), (8, 512, 4096, 3)]
     alone = {}
