@@ -10,8 +10,13 @@ every call streams its weight from HBM.  The timed region launches K steps
 eagerly on one stream; the same step captured as a HIP graph and replayed K
 times is timed too and reported beside it.
 
-value = algorithmic bytes (2NK + 2MK + 4MN summed over the four GEMMs) per
-second over the K timed steps, in GB/s.  Also reported: the same layer at
+Before each timed decode region the step runs back to back, untimed, for at
+least 250 ms (SETTLE_MS, whatever --warmup says): the GPU's clocks need tens of
+ms of sustained load to settle, and the weights are drawn on the CPU first,
+which leaves the GPU idle for seconds.  value = algorithmic bytes
+(2NK + 2MK + 4MN summed over the four GEMMs) per second of wall clock over the
+K timed steps, in GB/s; HIP events on the launch stream around the same steps
+give event_GB/s.  Also reported: the same layer at
 M = 1 and M = 32; the M = 8 layer over row-major weights read natively and
 read in whole 4 KB blocks (a large-granularity memory emulated), with the
 fetch amplification the kernel counts; prefill TFLOP/s at M = 2048 (the
@@ -109,8 +114,49 @@ def launch_bytes(M, N, K):
     return 2 * N * K + 2 * M * K + 4 * M * N
 
 
+SETTLE_MS = 250.0   # untimed back-to-back load before each timed decode region
+
+
+def settle(ctx, fn, min_ms=SETTLE_MS):
+    """Runs fn back to back, untimed, until at least min_ms of wall time has
+    passed (checked every 16 calls): the GPU's clocks take tens of ms of
+    sustained load to reach their steady state, so every timed region starts
+    from that state whatever ran before it (CPU-side input generation leaves
+    the GPU idle for seconds).  Returns (ms, calls)."""
+    ctx.torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    calls = 0
+    while True:
+        for _ in range(16):
+            fn()
+        calls += 16
+        ctx.torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3
+        if ms >= min_ms:
+            return ms, calls
+
+
+def timed_region(ctx, fn, reps):
+    """reps calls of fn between synchronisations: (wall s, GPU s).  The GPU
+    time comes from HIP events recorded on the launch stream around the same
+    calls (the stream every call in this file is enqueued on)."""
+    torch = ctx.torch
+    ev = ctx.event_pairs(1)[0]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(ctx.stream)
+    for _ in range(reps):
+        fn()
+    ev[1].record(ctx.stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, ev[0].elapsed_time(ev[1]) * 1e-3
+
+
 def decode_layer(ctx, weights, M, steps, warmup, desc, event_pass=False):
-    """Eager layer steps at batch M over tile-major weights [(name, N, K, W)]."""
+    """Eager layer steps at batch M over tile-major weights [(name, N, K, W)]:
+    an untimed settle phase (SETTLE_MS, independent of warmup), warmup
+    steps, then steps timed by wall clock and by HIP events on the stream."""
     tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
     acts = [ctx.to_dev(synth.normal_bf16((M, K), seed=synth.llama_decode_act_seed(i, M)))
             for i, (_, N, K, _) in enumerate(weights)]
@@ -125,10 +171,13 @@ def decode_layer(ctx, weights, M, steps, warmup, desc, event_pass=False):
             if ev is not None:
                 ev[j][1].record(ctx.stream)
 
+    settle_ms, settle_steps = settle(ctx, step)
     for _ in range(warmup):
         step()
-    wall = wall_time(ctx, step, steps)
+    wall, gpu = timed_region(ctx, step, steps)
     res = {"M": M, "GB/s": sum(lb) * steps / wall / 1e9, "ms_per_step": wall * 1e3 / steps,
+           "event_GB/s": sum(lb) * steps / gpu / 1e9, "event_ms_per_step": gpu * 1e3 / steps,
+           "settle_ms": round(settle_ms, 1), "settle_steps": settle_steps,
            "step_bytes": sum(lb), "launch_bytes": lb, "step": step}
     if event_pass:
         # per-launch durations from HIP events recorded on the launch stream
@@ -254,10 +303,11 @@ def prefill_layer(ctx, weights):
     # untimed: bring the clocks to their sustained MFMA-load state (about
     # 0.1 s of the layer), so that every configuration below is timed in it
     pd0 = tl.layout(G=G, block_rows=BR, out_dtype=tl.TL_OUT_BF16)
-    for _ in range(30):
+
+    def layer0():
         for (_, N, K, W), A, C in zip(weights, acts, outs):
             tl.tl_gemm(A, W, C, Mp, N, K, pd0, tl.TL_FETCH_BLOCK)
-    torch.cuda.synchronize()
+    settle_ms, _ = settle(ctx, layer0)
     # (0, 0) is the library's own plan (256 x 256 tiles; QKV's last 2048
     # columns as 128 x 128 tiles); the others pin one tile for every shape
     for tm, tn in ((0, 0), (256, 256), (256, 128), (128, 128)):
@@ -285,7 +335,15 @@ def prefill_layer(ctx, weights):
             "per_shape_TFLOP/s": {name: round(f / (t / reps * 1e-3) / 1e12, 1)
                                   for (name, _, _, _), f, t in zip(weights, flops, tot)}}
         log(f"prefill {'plan' if tm == 0 else f'tile {tm}x{tn}'}: {tf:.1f} TFLOP/s")
-    return res
+    # the library's plan at the first level (the headline prefill numbers),
+    # the pinned tiles below it
+    plan = res.pop("plan")
+    out = dict(plan)
+    out.update({"M": Mp, "settle_ms": round(settle_ms, 1),
+                "workload": "llama-3.1-70b-shaped prefill layer (qkv, o, gate_up, down), M=2048, bf16 out, "
+                            "tile-major G=4096 B 32x64 memory tiles; the library's tile plan",
+                "tiles": res})
+    return out
 
 
 def moe_layer(ctx, steps, warmup):
@@ -650,15 +708,17 @@ def view_load(ctx, weights):
     return res
 
 
-def granularity_sweep(ctx):
+def granularity_sweep(ctx, W=None):
     """Down projection [8192, 28672] for each memory tile (G, block_rows): the
     exact read amplification of 32 x tn x tk compute tiles over the tile-major
     and the row-major layout, the repack rate, and the GEMM at M = 32 (decode
     kernel) and M = 2048 (prefill kernel, bf16 out), whose own tiles cover
-    whole memory tiles."""
+    whole memory tiles.  W: the row-major down weight on the device (drawn
+    here when None)."""
     tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
     N, K = 8192, 28672
-    W = ctx.to_dev(synth.normal_bf16((N, K), seed=synth.llama_weight_seed(3), sigma=synth.W_SIGMA))
+    if W is None:
+        W = ctx.to_dev(synth.normal_bf16((N, K), seed=synth.llama_weight_seed(3), sigma=synth.W_SIGMA))
     Wt = torch.empty_like(W)
     A32 = ctx.to_dev(synth.normal_bf16((32, K), seed=synth.llama_decode_act_seed(3, 32)))
     A2k = ctx.to_dev(synth.normal_bf16((2048, K), seed=synth.llama_prefill_act_seed(3)))
@@ -667,6 +727,8 @@ def granularity_sweep(ctx):
     rm = tl.layout(kind=tl.TL_LAYOUT_NK_ROW)
     tiles = [(tn, tk) for tn in (64, 128, 256) for tk in (64, 128, 256)]
     rows = []
+    tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
+    settle(ctx, lambda: tl.tl_gemm(A32, Wt, C32, 32, N, K, tl.layout(G=4096, block_rows=32), tl.TL_FETCH_BLOCK))
     for Gs in (512, 1024, 4096, 16384):
         for br in (8, 16, 32, 64):
             d = tl.layout(G=Gs, block_rows=br)
@@ -707,6 +769,64 @@ def granularity_sweep(ctx):
             "rows": rows}
 
 
+def sweep_summary(sweep):
+    """One row per memory tile: the amplification of the 64x64, 128x128 and
+    256x256 compute tiles for both layouts, and the three measured rates."""
+    out = []
+    for r in sweep["rows"]:
+        out.append({"G": r["G"], "block_rows": r["block_rows"], "block_cols": r["block_cols"],
+                    "amp_tile_major_64_128_256": [r["read_amp_tile_major"][f"{t}x{t}"] for t in (64, 128, 256)],
+                    "amp_row_major_64_128_256": [r["read_amp_row_major"][f"{t}x{t}"] for t in (64, 128, 256)],
+                    "repack_GB/s": r["repack_GB/s"], "decode_M32_GB/s": r["decode_M32_GB/s"],
+                    "prefill_M2048_TFLOP/s": r["prefill_M2048_TFLOP/s"]})
+    return out
+
+
+def device_info():
+    """CU count and maximum engine clock of the first GPU agent, from rocminfo
+    (run before this process touches the GPU), and the dense bf16 MFMA rate
+    they imply at 4096 flop per CU per clock (gfx950: 2.5 PFLOP/s at 256 CUs
+    and 2.4 GHz)."""
+    import subprocess
+    info = {"source": "rocminfo"}
+    try:
+        text = subprocess.run(["rocminfo"], capture_output=True, text=True, timeout=120).stdout
+    except (OSError, subprocess.SubprocessError) as e:
+        return {"source": f"rocminfo unavailable: {e}"}
+    for block in text.split("*******")[1:]:
+        if "Device Type:             GPU" not in block and "Device Type: GPU" not in " ".join(block.split()):
+            continue
+        for line in block.splitlines():
+            key, _, val = line.strip().partition(":")
+            val = val.strip()
+            if key == "Marketing Name":
+                info["name"] = val
+            elif key == "Name" and val.startswith("gfx"):
+                info["arch"] = val
+            elif key == "Compute Unit":
+                info["compute_units"] = int(val)
+            elif key.startswith("Max Clock Freq"):
+                info["max_clock_mhz"] = int(val)
+        break
+    if not info.get("name"):
+        info.pop("name", None)
+    if "compute_units" in info and "max_clock_mhz" in info:
+        info["bf16_dense_TFLOP/s_at_max_clock"] = round(info["compute_units"] * info["max_clock_mhz"] * 4096 / 1e6, 1)
+    return info
+
+
+PAPER_CONTEXT = {
+    "what": "the paper's simulated results (cycle-level simulator of an H200-class GPU with a high-bandwidth-flash "
+            "tier of 4 KB access granularity and 5 us NAND read latency; Sections 1, 6.3 and 8); context only, "
+            "not a target and not comparable to rates measured on HBM",
+    "geomean_slowdown_vs_hbm_only_conventional_layouts": "1.61-6.49x",
+    "geomean_slowdown_row_major": 1.61,
+    "geomean_slowdown_tile_major_with_adaptive_prefetch": 1.01,
+    "geomean_slowdown_tile_major_prefetch_and_sram_buffer": 1.00,
+    "requests_per_128x256_bf16_tile_row_major_vs_tile_major": [128, 16],
+}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -724,6 +844,7 @@ def main():
               f"(the path is single-GPU; see the sharding notes in the design document)", file=sys.stderr)
         sys.exit(2)
 
+    dev_info = device_info()
     ctx = Ctx()
     if args.sweep:
         print(json.dumps(granularity_sweep(ctx)), flush=True)
@@ -769,18 +890,14 @@ def main():
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=ctx.stream):
         main_run["step"]()
+    settle(ctx, graph.replay)
     for _ in range(args.warmup):
         graph.replay()
-    graph_gbs = main_run["step_bytes"] * args.steps / wall_time(ctx, graph.replay, args.steps) / 1e9
     # roofline: HIP events on the launch stream around K graph-replayed steps,
     # whose kernels run back to back -- the decode kernels' time per step
-    ev = ctx.event_pairs(1)[0]
-    ev[0].record(ctx.stream)
-    for _ in range(args.steps):
-        graph.replay()
-    ev[1].record(ctx.stream)
-    torch.cuda.synchronize()
-    kernel_ms_per_step = ev[0].elapsed_time(ev[1]) / args.steps
+    graph_wall, graph_gpu = timed_region(ctx, graph.replay, args.steps)
+    graph_gbs = main_run["step_bytes"] * args.steps / graph_wall / 1e9
+    kernel_ms_per_step = graph_gpu * 1e3 / args.steps
     achieved = main_run["step_bytes"] / (kernel_ms_per_step * 1e-3) / 1e9
     del graph
 
@@ -798,15 +915,9 @@ def main():
     rgraph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(rgraph, stream=ctx.stream):
         read_step()
-    for _ in range(args.warmup):
-        rgraph.replay()
-    ev = ctx.event_pairs(1)[0]
-    ev[0].record(ctx.stream)
-    for _ in range(args.steps):
-        rgraph.replay()
-    ev[1].record(ctx.stream)
-    torch.cuda.synchronize()
-    read_ms_per_step = ev[0].elapsed_time(ev[1]) / args.steps
+    settle(ctx, rgraph.replay, SETTLE_MS / 2)
+    _, read_gpu = timed_region(ctx, rgraph.replay, args.steps)
+    read_ms_per_step = read_gpu * 1e3 / args.steps
     weight_bytes = sum(2 * N * K for (_, N, K, _) in weights)
     ceiling = weight_bytes / (read_ms_per_step * 1e-3) / 1e9
     del rgraph
@@ -821,12 +932,13 @@ def main():
         f"kernels {achieved:.1f} GB/s")
 
     # ---------------- other batch sizes, layouts, the MoE layer -------------
-    extras = None
+    extras, sweep = None, None
     if not args.no_extras:
         extras = {}
         for M in (1, 32):
-            r = decode_layer(ctx, weights, M, args.steps, 2, desc, event_pass=True)
+            r = decode_layer(ctx, weights, M, args.steps, args.warmup, desc, event_pass=True)
             extras[f"decode_layer_M{M}_GB/s"] = round(r["GB/s"], 1)
+            extras[f"decode_layer_M{M}_event_GB/s"] = round(r["event_GB/s"], 1)
             # per call, from HIP events around each tl_gemm (which add ~4 us)
             extras[f"decode_layer_M{M}_per_shape"] = {
                 name: {"us": round(ms * 1e3, 2), "split_k": tl.tl_gemm_plan(M, N, K, desc)["split_k"],
@@ -834,6 +946,7 @@ def main():
                 for (name, N, K, _), ms in zip(weights, r["per_launch_ms"])}
             log(f"decode layer M={M}: {r['GB/s']:.1f} GB/s {extras[f'decode_layer_M{M}_per_shape']}")
         extras["layouts_M8"] = layout_comparison(ctx, weights, weights_rm)
+        sweep = granularity_sweep(ctx, weights_rm[3][3])
         del weights_rm
         torch.cuda.empty_cache()
         extras["moe_qwen3_30b_a3b_64_tokens"] = moe_layer(ctx, args.steps, args.warmup)
@@ -924,12 +1037,20 @@ def main():
                    "M": DECODE_M, "G": G, "block_rows": BR,
                    "weight_bytes": sum(2 * N * K for (_, N, K, _) in weights)},
         "frac_hbm_peak": round(value_gbs / HBM_PEAK_GBS, 4),
+        "event_GB/s": round(main_run["event_GB/s"], 1),
+        "event_ms_per_step": round(main_run["event_ms_per_step"], 4),
+        "settle_ms": main_run["settle_ms"],
+        "settle_steps": main_run["settle_steps"],
         "graph_replay_GB/s": round(graph_gbs, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "prefill": prefill,
         "read_amp": read_amp,
         "repack_GB/s": round(repack_bytes / (repack_ms * 1e-3) / 1e9, 1),
+        "granularity_sweep": None if sweep is None else {
+            "workload": sweep["config"]["workload"], "tiles": "32 x tn x tk, tn = tk", "rows": sweep_summary(sweep)},
+        "paper_context": PAPER_CONTEXT,
+        "device": dev_info,
         "extras": extras,
     }
     print(json.dumps(out), flush=True)
