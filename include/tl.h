@@ -28,12 +28,18 @@
  *    inside a kernel surfaces at the caller's next synchronisation.
  *  - Calls are thread-safe.  The library owns, per (device, stream), a split-K
  *    workspace and a fetch counter; concurrent calls on the SAME stream from
- *    several host threads are serialised by the stream, as usual.
+ *    several host threads are serialised by the stream, as usual.  A
+ *    workspace that must grow is replaced by a larger one and the old one is
+ *    kept (not freed) until tl_release, so work already enqueued or captured
+ *    with it stays valid.
  *  - HIP graphs: the GEMM and repack calls enqueue kernels only (no memset or
  *    copy nodes) and may be captured, once the stream's library state exists:
  *    the first call on a stream, and a call that needs a larger split-K
  *    workspace than any before it on that stream, allocate device memory
- *    (hipMalloc) and must be made outside capture.  tl_fetch_counter_read
+ *    (hipMalloc) and must be made outside capture.  A captured graph binds
+ *    the capture stream's workspace as it was at capture time: replay it on
+ *    that stream (or serialised with it), never concurrently with split-K
+ *    calls on that stream, and not after tl_release.  tl_fetch_counter_read
  *    synchronises its stream and cannot be captured.
  */
 #ifndef TL_H_
@@ -429,9 +435,11 @@ int tl_stream_read(const void* src, int64_t bytes, uint32_t* checksum, void* str
  * bytes; TL_EHIP if a HIP call fails. */
 int tl_fetch_counter_read(void* stream, int64_t* bytes);
 
-/* tl_release -- frees every workspace and counter the library holds (all
- * devices, all streams).  The caller must ensure no library work is still in
- * flight.  Always TL_OK. */
+/* tl_release -- frees every workspace (current and retired) and counter the
+ * library holds (all devices, all streams); a call still running in another
+ * thread keeps its own buffers until it returns.  The caller must ensure no
+ * library work is still in flight on the GPU and replays no graph captured
+ * before it.  Always TL_OK. */
 int tl_release(void);
 
 /* tl_strerror -- static, NUL-terminated description of a tl_status. */

@@ -6,8 +6,10 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <utility>
+#include <vector>
 
 #include "tl_internal.h"
 
@@ -35,29 +37,57 @@ namespace {
 
 // ---------------------------------------------------------------------------
 // Library state: split-K workspace and the fetch tally, one set per
-// (device, stream).
+// (device, stream).  A workspace that has to grow is retired, not freed: a
+// HIP graph captured earlier on the stream, or a call of another thread that
+// took the old pointer, may still use it.  Retired workspaces are freed by
+// tl_release.  Each call holds a shared reference to its state, so the
+// buffers it enqueues on outlive a concurrent tl_release's host-side cleanup.
 // ---------------------------------------------------------------------------
 struct StreamState {
+    int dev = 0;
     float* ws = nullptr;
     size_t ws_bytes = 0;
+    unsigned long long* fetch = nullptr;
+    std::vector<float*> retired;
+    ~StreamState() {
+        int cur = 0;
+        const bool restore = hipGetDevice(&cur) == hipSuccess;
+        (void)hipSetDevice(dev);
+        for (float* p : retired) (void)hipFree(p);
+        if (ws) (void)hipFree(ws);
+        if (fetch) (void)hipFree(fetch);
+        if (restore) (void)hipSetDevice(cur);
+    }
+};
+
+// What one call uses: the buffers as they were when it looked them up.
+struct StateRef {
+    std::shared_ptr<StreamState> keep;
+    float* ws = nullptr;
     unsigned long long* fetch = nullptr;
 };
 
 std::mutex g_mu;
-std::map<std::pair<int, void*>, StreamState> g_state;
+std::map<std::pair<int, void*>, std::shared_ptr<StreamState>> g_state;
 
 int current_device(int* dev) {
     return hipGetDevice(dev) == hipSuccess ? TL_OK : TL_EHIP;
 }
 
-// Returns the state for (current device, stream), growing the workspace.  A
-// new tally is cleared on 'stream' so the clear is ordered before any kernel
-// that uses it.
-int get_state(hipStream_t stream, size_t ws_bytes, StreamState** out) {
+// Looks up (current device, stream), creating its tally (cleared on 'stream',
+// so the clear is ordered before any kernel that uses it) and growing its
+// workspace to at least ws_bytes.  The lock covers the map and the
+// allocations only; nothing here waits for the GPU.
+int get_state(hipStream_t stream, size_t ws_bytes, StateRef* out) {
     int dev = 0;
     if (current_device(&dev) != TL_OK) return TL_EHIP;
     std::lock_guard<std::mutex> lock(g_mu);
-    StreamState& st = g_state[{dev, (void*)stream}];
+    std::shared_ptr<StreamState>& sp = g_state[{dev, (void*)stream}];
+    if (!sp) {
+        sp = std::make_shared<StreamState>();
+        sp->dev = dev;
+    }
+    StreamState& st = *sp;
     if (!st.fetch) {
         if (hipMalloc(&st.fetch, sizeof(unsigned long long)) != hipSuccess) { st.fetch = nullptr; return TL_ENOMEM; }
         if (launch_zero_u64(st.fetch, stream) != hipSuccess) {   // the next call allocates and clears again
@@ -67,18 +97,18 @@ int get_state(hipStream_t stream, size_t ws_bytes, StreamState** out) {
         }
     }
     if (ws_bytes > st.ws_bytes) {
-        if (st.ws) {
-            // the old buffer may still be read by work in flight on this stream
-            if (hipStreamSynchronize(stream) != hipSuccess) return TL_EHIP;
-            (void)hipFree(st.ws);
-            st.ws = nullptr;
-            st.ws_bytes = 0;
-        }
-        size_t bytes = std::max<size_t>(ws_bytes, size_t(1) << 20);
-        if (hipMalloc(&st.ws, bytes) != hipSuccess) { st.ws = nullptr; return TL_ENOMEM; }
+        // at least double, so the retired buffers never add up to more than
+        // the current one
+        const size_t bytes = std::max({ws_bytes, 2 * st.ws_bytes, size_t(1) << 20});
+        float* p = nullptr;
+        if (hipMalloc(&p, bytes) != hipSuccess) return TL_ENOMEM;
+        if (st.ws) st.retired.push_back(st.ws);
+        st.ws = p;
         st.ws_bytes = bytes;
     }
-    *out = &st;
+    out->keep = sp;
+    out->ws = st.ws;
+    out->fetch = st.fetch;
     return TL_OK;
 }
 
@@ -440,7 +470,7 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
     if (scales && overlap(C, c_bytes, scales, N * 4)) return TL_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
-    StreamState* st = nullptr;
+    StateRef st;
     rc = get_state(s, size_t(p.pub.workspace_bytes), &st);
     if (rc != TL_OK) return rc;
 
@@ -450,8 +480,8 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
         d.A = static_cast<const uint16_t*>(A);
         d.W = static_cast<const uint8_t*>(W);
         d.C = C;
-        d.ws = st->ws;
-        d.fetch = p.count ? st->fetch : nullptr;
+        d.ws = st.ws;
+        d.fetch = p.count ? st.fetch : nullptr;
         d.M = M;
         d.N = N;
         d.K = K;
@@ -473,7 +503,7 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
         q.A = static_cast<const uint16_t*>(A);
         q.W = static_cast<const uint8_t*>(W);
         q.C = C;
-        q.fetch = p.count ? st->fetch : nullptr;
+        q.fetch = p.count ? st.fetch : nullptr;
         q.M = M;
         q.N = N;
         q.K = K;
@@ -525,7 +555,7 @@ static int grouped_impl(const void* A, int64_t a_rows, const int32_t* token_ids,
     if (overlap(C, c_bytes, A, a_rows * K * 2) || overlap(C, c_bytes, W, w_bytes)) return TL_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
-    StreamState* st = nullptr;
+    StateRef st;
     rc = get_state(s, 0, &st);
     if (rc != TL_OK) return rc;
     DecodeLaunch d;
@@ -533,7 +563,7 @@ static int grouped_impl(const void* A, int64_t a_rows, const int32_t* token_ids,
     d.W = static_cast<const uint8_t*>(W);
     d.C = C;
     d.ws = nullptr;
-    d.fetch = p.count ? st->fetch : nullptr;
+    d.fetch = p.count ? st.fetch : nullptr;
     d.M = std::min<int64_t>(max_group_rows, kDecodeMaxM);
     d.N = N;
     d.K = K;
@@ -634,14 +664,14 @@ int tl_gemm_lgms(const void* A, const void* W, void* C, int64_t M, int64_t N, in
     if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0) return TL_EHIP;
     const int64_t ticks = (latency_ns * int64_t(khz) + 999999) / 1000000;
     hipStream_t s = (hipStream_t)stream;
-    StreamState* st = nullptr;
+    StateRef st;
     rc = get_state(s, size_t(S > 1 ? S * ((M * N + 3) / 4 * 4) * 4 : 0), &st);
     if (rc != TL_OK) return rc;
     DecodeLaunch dl;
     dl.A = static_cast<const uint16_t*>(A);
     dl.W = static_cast<const uint8_t*>(W);
     dl.C = C;
-    dl.ws = st->ws;
+    dl.ws = st.ws;
     dl.fetch = nullptr;
     dl.M = M;
     dl.N = N;
@@ -694,29 +724,27 @@ int tl_stream_read(const void* src, int64_t bytes, uint32_t* checksum, void* str
 int tl_fetch_counter_read(void* stream, int64_t* bytes) {
     if (!bytes) return TL_EINVAL;
     hipStream_t s = (hipStream_t)stream;
-    StreamState* st = nullptr;
+    StateRef st;   // holds the tally's buffer for the rest of this call
     int rc = get_state(s, 0, &st);
     if (rc != TL_OK) return rc;
     unsigned long long v = 0;
     if (hipStreamSynchronize(s) != hipSuccess) return TL_EHIP;
-    if (hipMemcpy(&v, st->fetch, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return TL_EHIP;
-    if (launch_zero_u64(st->fetch, s) != hipSuccess) return TL_EHIP;
+    if (hipMemcpy(&v, st.fetch, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return TL_EHIP;
+    if (launch_zero_u64(st.fetch, s) != hipSuccess) return TL_EHIP;
     if (hipStreamSynchronize(s) != hipSuccess) return TL_EHIP;
     *bytes = int64_t(v);
     return TL_OK;
 }
 
 int tl_release(void) {
-    std::lock_guard<std::mutex> lock(g_mu);
-    int dev0 = 0;
-    (void)hipGetDevice(&dev0);
-    for (auto& kv : g_state) {
-        (void)hipSetDevice(kv.first.first);
-        if (kv.second.ws) (void)hipFree(kv.second.ws);
-        if (kv.second.fetch) (void)hipFree(kv.second.fetch);
+    // the states leave the map under the lock; their buffers are freed when
+    // the last call still holding one returns (here, when none does)
+    std::map<std::pair<int, void*>, std::shared_ptr<StreamState>> old;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        old.swap(g_state);
     }
-    g_state.clear();
-    (void)hipSetDevice(dev0);
+    old.clear();
     return TL_OK;
 }
 

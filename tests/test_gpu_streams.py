@@ -87,3 +87,49 @@ def test_release_then_reuse():
     torch.cuda.synchronize()
     assert np.array_equal(host_f32(C2), first)
     parity(first, oracle.gemm_f64(A, W), "after release")
+
+
+def test_graph_replay_after_workspace_growth():
+    """A graph captured while the stream's split-K workspace was small keeps
+    working after a later eager call grows the workspace: the old buffer is
+    retired, not freed, so the graph's kernels still write valid memory.
+    Every replay (with eager split-K work on the grown workspace between the
+    replays) equals the eager result of the captured call."""
+    import torch
+    banner("capture split-K on a small workspace, grow it eagerly, replay")
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        tl.tl_release()                                   # start from no state on any stream
+        small = _case(0)                                  # M=8, N=1024, K=4096: 128 KiB of partials
+        big = _case(1)                                    # M=32, N=8192, K=8192: 4 MiB at split_k 4
+        dev = []
+        for (M, N, K, A, W) in (small, big):
+            Wd = dev_bf16(W)
+            Wt = torch.empty_like(Wd)
+            tl.tl_repack(Wd, Wt, N, K, 2, 4096, 32)
+            dev.append((dev_bf16(A), Wt, torch.zeros((M, N), dtype=torch.float32, device="cuda")))
+        d = tl.layout(split_k=4)
+        (Ms, Ns, Ks, As, Ws), (Mb, Nb, Kb, Ab, Wb) = small, big
+        (A0, W0, C0), (A1, W1, C1) = dev
+        tl.tl_gemm(A0, W0, C0, Ms, Ns, Ks, d, tl.TL_FETCH_BLOCK)      # creates the small workspace
+        side.synchronize()
+        eager_small = C0.clone()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            tl.tl_gemm(A0, W0, C0, Ms, Ns, Ks, d, tl.TL_FETCH_BLOCK)
+        assert tl.tl_gemm_plan(Mb, Nb, Kb, d)["workspace_bytes"] > (1 << 20)
+        tl.tl_gemm(A1, W1, C1, Mb, Nb, Kb, d, tl.TL_FETCH_BLOCK)      # grows the workspace
+        side.synchronize()
+        eager_big = C1.clone()
+        for rep in range(4):
+            C0.fill_(float("nan"))
+            side.synchronize()
+            g.replay()
+            side.synchronize()
+            assert torch.equal(C0, eager_small), f"replay {rep}"
+            tl.tl_gemm(A1, W1, C1, Mb, Nb, Kb, d, tl.TL_FETCH_BLOCK)  # eager work on the new workspace
+            side.synchronize()
+            assert torch.equal(C1, eager_big), f"eager call after replay {rep}"
+        del g
+    parity(host_f32(eager_small), oracle.gemm_f64(As, Ws), "captured call")
+    parity(host_f32(eager_big), oracle.gemm_f64(Ab, Wb), "growing call")
