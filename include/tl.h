@@ -301,7 +301,7 @@ int tl_gemm_grouped_swiglu(const void* A, int64_t a_rows, const int32_t* token_i
 /*
  * tl_read_amp -- host only, exact integer count of the bytes a tiled GEMM
  * fetches at granularity G (Sections 1, 2.5; the per-tile request counts of
- * Section 6.4).  Model: the grid has ceil(M/tile_m) x ceil(N/tile_n) tiles,
+ * Section 6.5).  Model: the grid has ceil(M/tile_m) x ceil(N/tile_n) tiles,
  * each iterating ceil(K/tile_k) K-steps; at each step a tile fetches every
  * G-byte block (aligned relative to the weight's base) holding at least one
  * element of its weight sub-tile (clipped at the matrix edge); nothing is

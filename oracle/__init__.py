@@ -28,7 +28,7 @@ What each function follows (TileLens, arxiv 2607.04031):
                  holds (Section 3.1): OCP E4M3 decoded by its definition, and
                  the GEMM over them with per-output-channel scales, fp64
   round_bf16     round-to-nearest-even to 8 significant bits
-  read_amp       Sections 1, 2.5 and 6.4 (requests per compute tile at
+  read_amp       Sections 1, 2.5 and 6.5 (requests per compute tile at
                  granularity G; weights only, Section 5.1)
 """
 import ctypes

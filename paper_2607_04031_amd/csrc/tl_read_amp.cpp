@@ -1,6 +1,6 @@
 // tl_read_amp: exact count of the G-byte blocks a tiled GEMM fetches from a
 // large-granularity memory (TileLens Sections 1 and 2.5; the per-tile request
-// counts of Section 6.4).  Host-only integer arithmetic.
+// counts of Section 6.5).  Host-only integer arithmetic.
 //
 // Two routes, both exact:
 //  * closed forms for the aligned power-of-two cases every evaluated shape

@@ -387,24 +387,11 @@ def test_prefill_row_major_native():
 # Full-size workloads, sampled outputs
 # ---------------------------------------------------------------------------
 
-def _sampled_check(A_bits, W_bits, C, n_samples, seed, bf16_out=False):
-    M, N = C.shape
-    rng = np.random.default_rng(seed)
-    ms = rng.integers(0, M, n_samples)
-    ns = rng.integers(0, N, n_samples)
-    y_ref = oracle.gemm_f64_points(A_bits, W_bits, ms, ns)
-    import torch
-    got = C[torch.from_numpy(ms).cuda(), torch.from_numpy(ns).cuda()]
-    if bf16_out:
-        parity_bf16_out(host_bits(got), y_ref, "sampled bf16")
-    else:
-        parity(host_f32(got), y_ref, "sampled")
-
-
 @pytest.mark.parametrize("i,name,N,K", [(i, *s) for i, s in enumerate(synth.LLAMA70B)])
-def test_llama_decode_full_size_sampled(i, name, N, K):
+def test_llama_decode_full_size(i, name, N, K):
     """The bench workload (Llama-70B shapes, M = 1, 8, 32, tile-major G = 4 KB,
-    br = 32, block fetch), in the launch configuration the bench uses."""
+    br = 32, block fetch), in the launch configuration the bench uses: every
+    output element against the fp64 oracle."""
     banner(f"llama decode full {name}")
     import torch
     W_bits = synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA)
@@ -413,16 +400,34 @@ def test_llama_decode_full_size_sampled(i, name, N, K):
     tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
     del W
     for M in synth.LLAMA_DECODE_M:
+        banner(f"llama decode full {name} M={M} plan={tl.tl_gemm_plan(M, N, K, tl.layout())}")
         A_bits = synth.normal_bf16((M, K), seed=synth.llama_decode_act_seed(i, M))
         A = dev_bf16(A_bits)
         C = torch.empty((M, N), dtype=torch.float32, device="cuda")
         tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(), tl.TL_FETCH_BLOCK)
         _sync()
-        _sampled_check(A_bits, W_bits, C, 512, seed=M + i)
+        parity(host_f32(C), oracle.gemm_f64(A_bits, W_bits), f"{name} M={M}")
+
+
+def _prefill_bands(M, N):
+    """Rows and columns of the prefill band checks: 32 rows, one in each
+    64-row block at a varying offset, and 128 columns, one in each N/128-wide
+    block at a varying offset.  The row band (those rows x every column) then
+    holds rows of every 128- and 256-row tile, and the column band (every row
+    x those columns) columns of every 128- and 256-column tile."""
+    rows = np.array([64 * b + (13 * b + 5) % 64 for b in range(M // 64)], dtype=np.int64)
+    step = N // 128
+    cols = np.array([step * b + (37 * b + 11) % step for b in range(128)], dtype=np.int64)
+    return rows, cols
 
 
 @pytest.mark.parametrize("i,name,N,K", [(i, *s) for i, s in enumerate(synth.LLAMA70B)])
-def test_llama_prefill_full_size_sampled(i, name, N, K):
+def test_llama_prefill_full_size_bands(i, name, N, K):
+    """Prefill at M = 2048 for the four Llama shapes, every tile the library
+    offers and its own plan (the one bench.py times): a band of full rows and
+    a band of full columns against the fp64 oracle, bf16 output.  The bands
+    meet every workgroup's output tile of every plan (asserted), including
+    both launches of QKV's column split."""
     banner(f"llama prefill full {name}")
     import torch
     W_bits = synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA)
@@ -433,20 +438,51 @@ def test_llama_prefill_full_size_sampled(i, name, N, K):
     M = synth.LLAMA_PREFILL_M
     A_bits = synth.normal_bf16((M, K), seed=synth.llama_prefill_act_seed(i))
     A = dev_bf16(A_bits)
-    # (0, 0): the library's plan, the one bench.py times (QKV: 256 x 256 tiles
-    # on columns [0, 8192), 128 x 128 tiles on the rest)
+    rows, cols = _prefill_bands(M, N)
+    want_rows = oracle.gemm_f64(A_bits[rows], W_bits)            # [32, N]
+    want_cols = oracle.gemm_f64(A_bits, W_bits[cols])            # [M, 128]
+    d_rows, d_cols = torch.from_numpy(rows).cuda(), torch.from_numpy(cols).cuda()
+    # (0, 0): the library's plan (QKV: 256 x 256 tiles on columns [0, 8192),
+    # 128 x 128 tiles on the rest)
     for tm, tn in ((128, 128), (256, 128), (256, 256), (0, 0)):
+        d = tl.layout(tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16)
+        plan = tl.tl_gemm_plan(M, N, K, d)
+        ptm, ptn = plan["tile_m"], plan["tile_n"]
+        # every (m-tile, n-tile) of the plan holds a row-band element (and the
+        # 128 x 128 tiles of a column split are finer than any plan tile)
+        assert len(np.unique(rows // 128)) == M // 128 and len(np.unique(rows // ptm)) == -(-M // ptm)
+        assert len(np.unique(cols // 128)) == -(-N // 128)
+        banner(f"llama prefill full {name} tile {tm}x{tn} plan={plan}")
         C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-        tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16),
-                   tl.TL_FETCH_BLOCK)
+        tl.tl_gemm(A, Wt, C, M, N, K, d, tl.TL_FETCH_BLOCK)
         _sync()
-        _sampled_check(A_bits, W_bits, C, 512, seed=tm + tn + i, bf16_out=True)
-    if N == 10240:
-        # both sides of the column split, every row tile
-        ms = np.repeat(np.arange(0, M, 97), 4)
-        ns = np.tile(np.array([8190, 8191, 8192, 8193]), len(ms) // 4)
-        got = C[torch.from_numpy(ms).cuda(), torch.from_numpy(ns).cuda()]
-        parity_bf16_out(host_bits(got), oracle.gemm_f64_points(A_bits, W_bits, ms, ns), "split boundary")
+        parity_bf16_out(host_bits(C[d_rows]), want_rows, f"{name} {tm}x{tn} row band")
+        parity_bf16_out(host_bits(C[:, d_cols]), want_cols, f"{name} {tm}x{tn} column band")
+
+
+def test_llama_prefill_o_every_element():
+    """The O projection [8192, 8192] at M = 2048 with the library's plan: every
+    output element against the fp64 oracle (bf16 output), and the fp32-output
+    run of the same plan against the fp32 gate."""
+    i, name, N, K = 1, *synth.LLAMA70B[1]
+    banner(f"llama prefill {name} every element")
+    import torch
+    W_bits = synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA)
+    W = dev_bf16(W_bits)
+    Wt = torch.empty_like(W)
+    tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
+    del W
+    M = synth.LLAMA_PREFILL_M
+    A_bits = synth.normal_bf16((M, K), seed=synth.llama_prefill_act_seed(i))
+    A = dev_bf16(A_bits)
+    want = oracle.gemm_f64(A_bits, W_bits)
+    C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    tl.tl_gemm(A, Wt, C, M, N, K, tl.layout(out_dtype=tl.TL_OUT_BF16), tl.TL_FETCH_BLOCK)
+    C32 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    tl.tl_gemm(A, Wt, C32, M, N, K, tl.layout(), tl.TL_FETCH_BLOCK)
+    _sync()
+    parity_bf16_out(host_bits(C), want, f"{name} bf16 out")
+    parity(host_f32(C32), want, f"{name} fp32 out")
 
 
 # ---------------------------------------------------------------------------

@@ -80,7 +80,7 @@ def test_random_views_on_gpu(s, G, br):
 
 def test_llama_weight_box():
     """A 128 x 256 (K x N) box of the gate+up weight at a compute-tile
-    position, bf16, (64, 32) memory tiles: the compute tile of Section 6.4."""
+    position, bf16, (64, 32) memory tiles: the compute tile of Section 6.5."""
     import torch
     N, K, s, G, br = 57344, 8192, 2, 4096, 32
     banner("view load: gate_up 128 x 256 box")

@@ -203,6 +203,75 @@ def test_view_example_addresses_same_elements():
     assert len(logical) == 128 * 64
 
 
+def _numpy_tile_positions(K, N, a, b):
+    """Position of every element of a K x N column-major matrix (element
+    (i, j) has id j * K + i) in the tile-major order, built with numpy's
+    reshape and transpose alone: pos[j * K + i] = element index in the copy."""
+    ids = np.arange(N * K, dtype=np.int64).reshape(N, K)          # [j][i]
+    order = ids.reshape(N // b, b, K // a, a).transpose(0, 2, 1, 3).ravel()
+    pos = np.empty(N * K, dtype=np.int64)
+    pos[order] = np.arange(N * K, dtype=np.int64)
+    return pos
+
+
+def test_view_offsets_paper_example_order():
+    """orc_view_offsets on the Section 4.3 example (FP8 384 x 128 column-major
+    matrix, 128 x 64 box at (256, 64), 64 x 64 memory tiles): the 2-D, 3-D and
+    4-D descriptors give the same offsets in the same order -- the contiguous
+    index i = 256 + x0 fastest, then j = 64 + x1 -- and every offset is the
+    element's place in a tile-major copy built by numpy's reshape/transpose."""
+    g = load("paper_view_example.txt")
+    K, N, s = g["K"], g["N"], g["elem_bytes"]
+    G, b = 4096, 64
+    a = G // (s * b)
+    pos = _numpy_tile_positions(K, N, a, b)
+    want = np.array([pos[(64 + x1) * K + 256 + x0] * s for x1 in range(64) for x0 in range(128)])
+
+    def parse(v):
+        return [list(map(int, p.split(","))) for p in v.split(";")]
+
+    strides = {"view2d": [1, K], "view3d": [1, K, 128], "view4d": [1, K, 128, 64 * K]}
+    for name in ("view2d", "view3d", "view4d"):
+        _, coords, box = parse(g[name])
+        got = oracle.view_offsets(strides[name], coords, box, K, s, G, b)
+        assert np.array_equal(got, want), name
+
+
+def test_view_offsets_identity_extreme():
+    """block_rows = 1 with K * s = G: a memory tile is one whole column of
+    the column-major matrix, so the tile-major copy is the matrix itself and
+    every view's offsets are its linear element indices times s (dimension 0
+    fastest), for 2-D, 3-D and 4-D views of bf16 and FP8 matrices."""
+    for s, K, N in ((2, 2048, 48), (1, 4096, 24)):
+        G = K * s
+        cases = [([1, K], [5, 3], [40, 7]),
+                 ([1, K, 256], [16, 2, 1], [64, 5, 3]),
+                 ([1, 512, K, 4 * K], [8, 1, 1, 2], [32, 2, 3, 4])]
+        for strides, coords, box in cases:
+            got = oracle.view_offsets(strides, coords, box, K, s, G, 1)
+            want = []
+            for idx in itertools.product(*[range(n) for n in reversed(box)]):
+                x = idx[::-1]                                   # dimension 0 fastest
+                want.append(sum((c + xi) * st for c, xi, st in zip(coords, x, strides)) * s)
+            assert np.array_equal(got, np.array(want)), (s, strides)
+
+
+def test_view_offsets_case2_field_layout():
+    """Section 4.3 Case 2: an FP8 128 x 32 memory tile read by a 32-wide box
+    (u = 32 along the contiguous dimension, all b = 32 columns).  The box of
+    sub-tile t, element (row r along the contiguous dimension, column c), sits
+    at intra-tile offset c * a + t * u + r (fields col | sub | row); boxes in
+    the second memory tile of the strip add G."""
+    g = load("paper_case2_bitperm.txt")
+    a, b, u, s, G = g["memory_tile_a"], g["memory_tile_b"], g["tma_tile_u"], g["elem_bytes"], g["granularity"]
+    K = 2 * a
+    for tile in range(2):
+        for t in range(a // u):
+            got = oracle.view_offsets([1, K], [tile * a + t * u, 0], [u, b], K, s, G, b)
+            want = np.array([tile * G + (c * a + t * u + r) * s for c in range(b) for r in range(u)])
+            assert np.array_equal(got, want), (tile, t)
+
+
 def test_memory_tile_shapes_and_identity_extremes():
     """Section 3.1: shapes multiply to G; the (contiguous = G/s, other = 1)
     extreme is the plain row-major order, so the repack is the identity;
