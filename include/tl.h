@@ -56,7 +56,9 @@ typedef enum {
     TL_EINVAL = -1,        /* an argument violates the contract below */
     TL_EUNSUPPORTED = -2,  /* valid, but no kernel implements this combination */
     TL_EHIP = -3,          /* a HIP runtime call or a launch failed */
-    TL_ENOMEM = -4         /* the library could not allocate its workspace */
+    TL_ENOMEM = -4,        /* the library could not allocate its workspace */
+    TL_ESCRATCH = -5       /* tl_gemm_noalloc: the call needs more split-K
+                              scratch than TL_NOALLOC_SCRATCH_BYTES */
 } tl_status;
 
 /* Storage layout of a weight that is logically W[N][K]. */
@@ -428,6 +430,37 @@ int tl_view_load(const void* src_tm, const tl_view* view, int64_t K, int64_t N, 
  * fails.
  */
 int tl_stream_read(const void* src, int64_t bytes, uint32_t* checksum, void* stream);
+
+/* Bytes of the static device scratch behind tl_gemm_noalloc, per GPU. */
+#define TL_NOALLOC_SCRATCH_BYTES ((int64_t)32 << 20)
+
+/*
+ * tl_gemm_noalloc -- for callers that cannot allocate device memory: code
+ * under HIP graph capture, serving loops and harnesses that forbid hipMalloc.
+ * Same arguments, plan, kernels and results as tl_gemm, except that the
+ * split-K partials go to a static device array of TL_NOALLOC_SCRATCH_BYTES
+ * bytes (32 MiB) instead of the stream's library workspace.  The array
+ * belongs to the library's code object: every GPU the library runs on holds
+ * its own copy from the first use until the process ends.  This call
+ * allocates and frees nothing (no hipMalloc, no library state); its first
+ * call on a device looks up the array's device address
+ * (hipGetSymbolAddress), so make that first call outside graph capture if
+ * the capture mode forbids runtime queries.
+ * Every call on a GPU shares that GPU's array, and the array keeps the last
+ * call's contents (nothing in it needs to start at zero: every K split writes
+ * its whole partial before the reduce kernel reads it).  Calls that overlap
+ * on one GPU -- on two streams, or from two host threads -- race on the
+ * array and give unspecified results: serialise them (one stream, or events).
+ * A plan without K splits (split_k 1: e.g. prefill, or most M = 1..16 calls
+ * on large weights) does not touch the array.
+ * Errors: those of tl_gemm (except TL_ENOMEM); TL_ESCRATCH when the plan's
+ * split-K partials (tl_gemm_plan's workspace_bytes) exceed
+ * TL_NOALLOC_SCRATCH_BYTES -- layout->split_k can ask for fewer splits;
+ * TL_EUNSUPPORTED with TL_FETCH_COUNT (the tally is per-stream library
+ * state); TL_EHIP if the address lookup or a launch fails.
+ */
+int tl_gemm_noalloc(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
+                    const tl_layout_desc* layout, int32_t fetch_mode, void* stream);
 
 /* tl_fetch_counter_read -- synchronises 'stream', stores the weight bytes
  * tallied by tl_gemm calls made on it with TL_FETCH_COUNT since the last read

@@ -9,6 +9,7 @@ the C names and argument order of ``include/tl.h``:
     tl_repack(src, dst, rows, cols, elem_bytes, G, block_rows, stream=None)
     tl_unpack(src_tm, dst, rows, cols, elem_bytes, G, block_rows, stream=None)
     tl_gemm(A, W, C, M, N, K, layout, fetch_mode, stream=None)
+    tl_gemm_noalloc(A, W, C, M, N, K, layout, fetch_mode, stream=None)
     tl_gemm_plan(M, N, K, layout, fetch_mode) -> dict
     tl_gemm_grouped / tl_gemm_grouped_swiglu (..., layout, fetch_mode, stream=None)
     tl_read_amp(M, N, K, tile_m, tile_n, tile_k, layout, G) -> dict
@@ -32,12 +33,13 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtl.so")
 
-TL_OK, TL_EINVAL, TL_EUNSUPPORTED, TL_EHIP, TL_ENOMEM = 0, -1, -2, -3, -4
+TL_OK, TL_EINVAL, TL_EUNSUPPORTED, TL_EHIP, TL_ENOMEM, TL_ESCRATCH = 0, -1, -2, -3, -4, -5
+TL_NOALLOC_SCRATCH_BYTES = 32 << 20
 TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE = 0, 1, 2
 TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100
 
-EXPORTED = ("tl_tile_bytes", "tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_gemm_grouped_swiglu", "tl_read_amp",
+EXPORTED = ("tl_tile_bytes", "tl_repack", "tl_unpack", "tl_gemm", "tl_gemm_noalloc", "tl_gemm_w8", "tl_gemm_plan", "tl_gemm_grouped", "tl_gemm_grouped_swiglu", "tl_read_amp",
             "tl_view_offsets", "tl_view_load", "tl_prefetch_degree", "tl_gemm_lgms", "tl_lgms_occupancy",
             "tl_stream_read", "tl_fetch_counter_read", "tl_release", "tl_strerror")
 TL_VIEW_MAX_RANK = 5
@@ -125,6 +127,8 @@ def load_library():
     lib.tl_unpack.argtypes = [p, p, i64, i64, i32, i64, i32, p]
     lib.tl_gemm.restype = ctypes.c_int
     lib.tl_gemm.argtypes = [p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, p]
+    lib.tl_gemm_noalloc.restype = ctypes.c_int
+    lib.tl_gemm_noalloc.argtypes = [p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, p]
     lib.tl_gemm_w8.restype = ctypes.c_int
     lib.tl_gemm_w8.argtypes = [p, p, p, p, i64, i64, i64, ctypes.POINTER(LayoutDesc), i32, p]
     lib.tl_gemm_plan.restype = ctypes.c_int
@@ -223,6 +227,12 @@ def tl_gemm(A, W, C, M, N, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):
     d = _desc(layout)
     _check(load_library().tl_gemm(_ptr(A), _ptr(W), _ptr(C), M, N, K, ctypes.byref(d), fetch_mode,
                                   _stream(stream)), "tl_gemm")
+
+
+def tl_gemm_noalloc(A, W, C, M, N, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):
+    d = _desc(layout)
+    _check(load_library().tl_gemm_noalloc(_ptr(A), _ptr(W), _ptr(C), M, N, K, ctypes.byref(d), fetch_mode,
+                                          _stream(stream)), "tl_gemm_noalloc")
 
 
 def tl_gemm_w8(A, W_fp8, scales, C, M, N, K, layout, fetch_mode=TL_FETCH_BLOCK, stream=None):

@@ -457,11 +457,15 @@ int tl_gemm_plan(int64_t M, int64_t N, int64_t K, const tl_layout_desc* layout, 
     return TL_OK;
 }
 
+// noalloc: split-K partials in the static scratch (tl_scratch.hip), no
+// library state (no workspace, no tally), nothing allocated.
 static int gemm_impl(const void* A, const void* W, const float* scales, void* C, int64_t M, int64_t N, int64_t K,
-                     const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
+                     const tl_layout_desc* layout, int32_t fetch_mode, void* stream, bool noalloc = false) {
     Plan p;
     int rc = plan_gemm(M, N, K, layout, fetch_mode, &p);
     if (rc != TL_OK) return rc;
+    if (noalloc && p.count) return TL_EUNSUPPORTED;
+    if (noalloc && p.pub.workspace_bytes > kScratchBytes) return TL_ESCRATCH;
     if (!A || !W || !C || !aligned16(A) || !aligned16(W) || !aligned16(C)) return TL_EINVAL;
     if (scales && (reinterpret_cast<uintptr_t>(scales) & 3u)) return TL_EINVAL;
     const int64_t c_bytes = M * N * (p.out_bf16 ? 2 : 4);
@@ -471,8 +475,12 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
 
     hipStream_t s = (hipStream_t)stream;
     StateRef st;
-    rc = get_state(s, size_t(p.pub.workspace_bytes), &st);
-    if (rc != TL_OK) return rc;
+    if (noalloc) {
+        if (p.pub.workspace_bytes > 0 && scratch_address(&st.ws) != hipSuccess) return TL_EHIP;
+    } else {
+        rc = get_state(s, size_t(p.pub.workspace_bytes), &st);
+        if (rc != TL_OK) return rc;
+    }
 
     hipError_t e;
     if (p.pub.kernel == 1) {
@@ -605,6 +613,11 @@ int tl_gemm_grouped_swiglu(const void* A, int64_t a_rows, const int32_t* token_i
 int tl_gemm(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
             const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
     return gemm_impl(A, W, nullptr, C, M, N, K, layout, fetch_mode, stream);
+}
+
+int tl_gemm_noalloc(const void* A, const void* W, void* C, int64_t M, int64_t N, int64_t K,
+                    const tl_layout_desc* layout, int32_t fetch_mode, void* stream) {
+    return gemm_impl(A, W, nullptr, C, M, N, K, layout, fetch_mode, stream, true);
 }
 
 int tl_gemm_w8(const void* A, const void* W_fp8, const float* scales, void* C, int64_t M, int64_t N, int64_t K,
@@ -755,6 +768,7 @@ const char* tl_strerror(int status) {
         case TL_EUNSUPPORTED: return "TL_EUNSUPPORTED: no kernel implements this combination";
         case TL_EHIP: return "TL_EHIP: HIP runtime or launch failure";
         case TL_ENOMEM: return "TL_ENOMEM: workspace allocation failed";
+        case TL_ESCRATCH: return "TL_ESCRATCH: the split-K partials exceed the static scratch (TL_NOALLOC_SCRATCH_BYTES)";
         default: return "unknown tl_status";
     }
 }

@@ -114,6 +114,13 @@ struct PrefillLaunch {
 
 hipError_t launch_prefill(const PrefillLaunch& p, hipStream_t stream);
 
+// tl_gemm_noalloc's split-K scratch (tl_scratch.hip): a static device array
+// of kScratchBytes per GPU.  *out = its device address on the current device
+// (looked up with hipGetSymbolAddress on the first call per device; no
+// allocation).
+constexpr int64_t kScratchBytes = TL_NOALLOC_SCRATCH_BYTES;
+hipError_t scratch_address(float** out);
+
 // Counter program of a view load (TileLens-HW emulation, tl_view.cpp):
 // element e, decoded in mixed radix over count[] (counter 0 fastest), sits at
 //   off = tile_base + sum_c digit_c * stride[c]
