@@ -259,19 +259,27 @@ def cpu_oracle_timings(ctx, weights_host, threads):
 
 
 def layout_comparison(ctx, weights_tm, weights_rm):
-    """The M = 8 layer over tile-major weights (block fetch), row-major weights
-    read natively, and row-major weights read in whole 4 KB blocks.  Each case
-    reports the bytes the kernels fetched from weights (their own tally) over
-    the layer's weight bytes."""
+    """The M = 8 layer over the paper's three layouts (Section 2.4): tile-major
+    (block fetch), column-major -- W[N][K], K contiguous, the layout of a
+    linear layer's weight (TL_LAYOUT_NK_ROW) -- and row-major -- W stored
+    [K][N], N contiguous (TL_LAYOUT_KN_ROW) -- each linear layout read natively
+    and in whole 4 KB blocks (a large-granularity memory emulated on HBM).
+    Each case reports the weight bytes the kernels fetched (their own count
+    of the blocks or lines they load) over the layer's weight bytes."""
     tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    weights_kn = [(name, N, K, W.t().contiguous()) for (name, N, K, W) in weights_rm]
+    NK, KN = tl.TL_LAYOUT_NK_ROW, tl.TL_LAYOUT_KN_ROW
     cases = [("tile_major_block_4KB", weights_tm, tl.layout(G=G, block_rows=BR), tl.TL_FETCH_BLOCK),
-             ("row_major_native", weights_rm, tl.layout(kind=tl.TL_LAYOUT_NK_ROW), tl.TL_FETCH_NATIVE),
-             ("row_major_block_4KB", weights_rm, tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=G), tl.TL_FETCH_BLOCK)]
+             ("column_major_nk_row_native", weights_rm, tl.layout(kind=NK), tl.TL_FETCH_NATIVE),
+             ("column_major_nk_row_block_4KB", weights_rm, tl.layout(kind=NK, G=G), tl.TL_FETCH_BLOCK),
+             ("row_major_kn_row_native", weights_kn, tl.layout(kind=KN), tl.TL_FETCH_NATIVE),
+             ("row_major_kn_row_block_4KB", weights_kn, tl.layout(kind=KN, G=G), tl.TL_FETCH_BLOCK)]
     acts = [ctx.to_dev(synth.normal_bf16((DECODE_M, K), seed=synth.llama_decode_act_seed(i, DECODE_M)))
             for i, (_, N, K, _) in enumerate(weights_tm)]
     outs = [torch.empty((DECODE_M, N), dtype=torch.float32, device=ctx.dev) for (_, N, _, _) in weights_tm]
     wbytes = sum(2 * N * K for (_, N, K, _) in weights_tm)
-    res = {}
+    res = {"note": "paper orientation (Section 2.4): column-major = W[N][K] (K contiguous), "
+                   "row-major = W stored [K][N] (N contiguous)"}
     for name, ws, d, mode in cases:
         def step(extra=0):
             for (_, N, K, W), A, C in zip(ws, acts, outs):
@@ -282,13 +290,22 @@ def layout_comparison(ctx, weights_tm, weights_rm):
         step(tl.TL_FETCH_COUNT)
         torch.cuda.synchronize()
         fetched = tl.tl_fetch_counter_read()
-        reps = 3 if mode == tl.TL_FETCH_BLOCK and name.startswith("row") else 10
+        block = mode == tl.TL_FETCH_BLOCK and "block_4KB" in name and not name.startswith("tile")
+        reps = 3 if block else 10
         wall = wall_time(ctx, step, reps)
         res[name] = {"ms_per_layer": round(wall * 1e3 / reps, 3),
                      "weight_GB/s": round(wbytes * reps / wall / 1e9, 1),
                      "fetched_weight_bytes": fetched,
-                     "measured_amp": round(fetched / wbytes, 4) if fetched else None}
+                     "measured_amp": round(fetched / wbytes, 4) if fetched else None,
+                     # tl_read_amp of the kernels' tiles at the fetch granularity
+                     # (the 4 KB block, or a 128-byte line for native reads)
+                     "fetch_G": G if mode == tl.TL_FETCH_BLOCK else 128,
+                     "read_amp_exact": round(sum(tl.tl_read_amp(DECODE_M, N, K, p["tile_m"], p["tile_n"], p["tile_k"],
+                                                                d, G if mode == tl.TL_FETCH_BLOCK else 128)["fetched_bytes"]
+                                                 for (_, N, K, _) in ws
+                                                 for p in [tl.tl_gemm_plan(DECODE_M, N, K, d, mode)]) / wbytes, 4)}
         log(f"layout {name}: {res[name]}")
+    del weights_kn
     return res
 
 
@@ -769,6 +786,30 @@ def granularity_sweep(ctx, W=None):
             "rows": rows}
 
 
+def prefill_ab(ctx, reps=5):
+    """The gate+up prefill GEMM at M = 2048 (bf16 out) through the library's
+    plan on the tile-major weight and through torch's linear (the vendor
+    GEMM library) on the row-major weight, reps event-timed calls each after
+    an untimed settle: the pair a rocprofv3 counter comparison runs on."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    i, name, N, K = 2, *synth.LLAMA70B[2]
+    M = synth.LLAMA_PREFILL_M
+    W = ctx.to_dev(synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA))
+    Wt = torch.empty_like(W)
+    tl.tl_repack(W, Wt, N, K, 2, G, BR)
+    A = ctx.to_dev(synth.normal_bf16((M, K), seed=synth.llama_prefill_act_seed(i)))
+    C = torch.empty((M, N), dtype=torch.bfloat16, device=ctx.dev)
+    d = tl.layout(G=G, block_rows=BR, out_dtype=tl.TL_OUT_BF16)
+    calls = {"tile_major_plan": lambda: tl.tl_gemm(A, Wt, C, M, N, K, d, tl.TL_FETCH_BLOCK),
+             "torch_linear_row_major": lambda: torch.nn.functional.linear(A, W)}
+    res = {"shape": [M, N, K], "name": name}
+    for key, fn in calls.items():
+        settle(ctx, fn, 150.0)
+        _, gpu = timed_region(ctx, fn, reps)
+        res[key] = {"us": round(gpu / reps * 1e6, 1), "TFLOP/s": round(2.0 * M * N * K * reps / gpu / 1e12, 1)}
+    return res
+
+
 def sweep_summary(sweep):
     """One row per memory tile: the amplification of the 64x64, 128x128 and
     256x256 compute tiles for both layouts, and the three measured rates."""
@@ -836,6 +877,8 @@ def main():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip M=1/32, the layout comparison and the MoE layer")
     ap.add_argument("--sweep", action="store_true", help="run only the memory-tile granularity sweep")
+    ap.add_argument("--prefill-ab", action="store_true",
+                    help="run only gate+up prefill (M=2048) through the library and through torch's linear")
     ap.add_argument("--tp", action="store_true",
                     help="run only one GPU's share of the M=8 layer under tensor parallelism (TP 2, 4, 8)")
     args = ap.parse_args()
@@ -848,6 +891,9 @@ def main():
     ctx = Ctx()
     if args.sweep:
         print(json.dumps(granularity_sweep(ctx)), flush=True)
+        return
+    if args.prefill_ab:
+        print(json.dumps({"prefill_ab_gate_up_M2048": prefill_ab(ctx)}), flush=True)
         return
     torch, tl, synth = ctx.torch, ctx.tl, ctx.synth
 

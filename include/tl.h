@@ -184,10 +184,16 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  *      even) per layout->out_dtype.  C must not overlap A or W.
  * fetch_mode: TL_FETCH_NATIVE or TL_FETCH_BLOCK, optionally | TL_FETCH_COUNT.
  *      For TL_LAYOUT_TILE both modes load whole memory tiles (the compute tile
- *      is a whole number of memory tiles).  For TL_LAYOUT_NK_ROW, BLOCK loads
- *      every layout->G-byte block a K step touches, whole (decode kernel only;
- *      G a power of two, 128 <= G <= 2^30): the amplification of Section 2.5
- *      paid as real HBM traffic, and tallied by TL_FETCH_COUNT.
+ *      is a whole number of memory tiles).  For TL_LAYOUT_NK_ROW and
+ *      TL_LAYOUT_KN_ROW, BLOCK loads every layout->G-byte block a K step
+ *      touches, whole (decode kernel only; G a power of two,
+ *      128 <= G <= 2^30): the amplification of Section 2.5 paid as real HBM
+ *      traffic, and the blocks loaded are counted by TL_FETCH_COUNT.
+ * TL_LAYOUT_KN_ROW (W stored [K][N], N contiguous: the paper's row-major
+ * layout) runs a decode kernel (M <= 64) that loads each 64-row K step of a
+ * 64-column tile with whole 128-byte lines and transposes it through LDS
+ * into MFMA operands; it needs K % 64 == 0, N % 8 == 0 (N % 64 == 0 with
+ * BLOCK) and N < 2^27.
  * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound; at 17 <= M <= 32
  * on tile-major weights whose 32-row tiles and 512-column K chunks fill the
  * CUs in whole rounds, a variant that stages the activations in LDS and
@@ -202,7 +208,8 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * 16 / elem_bytes (one 16-byte load: keeps rows of A 16-byte aligned),
  * block_cols * elem_bytes < 16, a combination of layout, fetch mode and tile
  * that no kernel implements (NK_ROW with BLOCK above 64 rows, with FP8, or
- * with K % 64 or N % 32 != 0; FP8 above 64 rows), TL_LAYOUT_KN_ROW, or sizes
+ * with K % 64 or N % 32 != 0; FP8 above 64 rows; KN_ROW above 64 rows, with
+ * FP8, or outside the shape rules above), or sizes
  * past the kernels' 32-bit byte offsets: for M <= 64, 2 * M * K or the bytes
  * of tile_n weight rows (tile_n * K * elem_bytes, K padded for tile-major)
  * of 2^31 or more; above 64 rows, A or W of 2^32 bytes or more, or more

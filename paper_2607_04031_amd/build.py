@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtl.so")
 SOURCES = ["tl_api.cpp", "tl_read_amp.cpp", "tl_view.cpp", "tl_repack.hip", "tl_decode.hip", "tl_decode_fp8.hip",
            "tl_decode_lds.hip", "tl_lgms.hip", "tl_prefill.hip", "tl_view.hip", "tl_stream.hip",
-           "tl_scratch.hip"]
+           "tl_scratch.hip", "tl_decode_kn.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

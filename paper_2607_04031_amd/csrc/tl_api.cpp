@@ -161,6 +161,7 @@ struct Plan {
     int64_t n_main = 0;          // prefill: columns covered by the main tiles (rest: 128 x 128)
     bool fp8 = false;            // 1-byte (OCP E4M3) weight, decode kernel
     int lds_tiles = 0;           // > 0: decode with activations staged in LDS, tiles per workgroup
+    bool kn_row = false;         // weight stored [K][N] (N contiguous): the transposing decode kernel
 };
 
 constexpr int kDecodeMaxM = 64;
@@ -203,21 +204,63 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
             p.fetch_G = d->G;
         }
     } else {
-        return TL_EUNSUPPORTED;
+        // [K][N] row-major (the paper's row-major layout): the decode kernel
+        // that transposes each K step through LDS, bf16 only, M <= 64; whole
+        // 64-row K steps, rows of 16-byte multiples, and the rows one lane's
+        // eight loads span below 2^31 bytes
+        p.L.kind = TL_LAYOUT_KN_ROW;
+        p.kn_row = true;
+        if (block) {
+            if (!is_pow2(d->G) || d->G < 128 || d->G > (int64_t(1) << 30)) return TL_EINVAL;
+            p.block_row = true;
+            p.fetch_G = d->G;
+        }
+        if (p.fp8 || M > kDecodeMaxM || d->tile_m > 64) return TL_EUNSUPPORTED;
+        if (K % 64 || N % 8 || N >= (int64_t(1) << 27)) return TL_EUNSUPPORTED;
     }
     // Any N; K a multiple of one 16-byte lane load, so activation (and
     // row-major weight) rows stay 16-byte aligned and a load is either wholly
     // inside K or wholly past it.  Ragged N or K (padded tile-major weights,
     // Section 3.3) is not implemented for the row-major block emulation.
     if (K % (16 / s)) return TL_EUNSUPPORTED;
-    if (p.block_row && (K % 64 || N % 32)) return TL_EUNSUPPORTED;
+    // block emulation: whole 64-wide K steps, and tiles whose row segments
+    // start on 128-byte boundaries (so none straddles a block edge)
+    if (p.block_row && (K % 64 || N % (p.kn_row ? 64 : 32))) return TL_EUNSUPPORTED;
 
     const bool tile = d->kind == TL_LAYOUT_TILE;
     p.k_unit = tile ? std::max<int64_t>(64, p.L.bc) : 64;
 
     if (p.block_row && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;   // decode kernel only
     if (p.fp8 && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;        // FP8: decode kernel only
-    if (M <= kDecodeMaxM && d->tile_m <= 64) {
+    if (p.kn_row) {
+        // 64-column tiles (128-byte row segments), K split until there are
+        // about 1024 workgroups with >= 1024 K per split; 8 waves when the
+        // tiles need no more than two rounds of the CUs and their registers
+        // and LDS allow it
+        p.pub.kernel = 1;
+        p.m_tiles16 = int((M + 15) / 16);
+        if (p.m_tiles16 == 3) p.m_tiles16 = 4;
+        if (d->tile_n && d->tile_n != 64) return TL_EUNSUPPORTED;
+        if (d->tile_k && d->tile_k != 64) return TL_EUNSUPPORTED;
+        if (M * K * 2 >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;
+        p.k_unit = 64;
+        const int64_t n_tiles = (N + 63) / 64, units = K / 64;
+        int64_t S = d->split_k;
+        if (S == 0) {
+            const int64_t max_s = std::max<int64_t>(1, std::min<int64_t>(units / 16, kMaxSplitK));
+            S = n_tiles >= 2 * kCUs ? 1 : std::min((kTargetWorkgroups + n_tiles - 1) / n_tiles, max_s);
+        }
+        if (S < 1 || S > units || S > kMaxSplitK) return TL_EUNSUPPORTED;
+        const int64_t wgs = n_tiles * S;
+        p.waves = (wgs <= 2 * kCUs && p.m_tiles16 <= 2) ? 8 : 4;
+        p.pub.tile_m = 16 * p.m_tiles16;
+        p.pub.tile_n = 64;
+        p.pub.tile_k = 64;
+        p.pub.split_k = int(S);
+        p.pub.waves = p.waves;
+        p.pub.workgroups = wgs;
+        p.pub.workspace_bytes = S > 1 ? S * ((M * N + 3) / 4 * 4) * 4 : 0;
+    } else if (M <= kDecodeMaxM && d->tile_m <= 64) {
         p.pub.kernel = 1;
         p.m_tiles16 = int((M + 15) / 16);
         if (p.m_tiles16 == 3) p.m_tiles16 = 4;
@@ -406,7 +449,7 @@ int plan_grouped(int64_t max_group_rows, int64_t N, int64_t K, const tl_layout_d
     d1.split_k = 1;
     int rc = plan_gemm(std::min<int64_t>(max_group_rows, kDecodeMaxM), N, K, &d1, fetch_mode, P);
     if (rc != TL_OK) return rc;
-    if (P->pub.kernel != 1 || P->block_row || P->fp8) return TL_EUNSUPPORTED;
+    if (P->pub.kernel != 1 || P->block_row || P->fp8 || P->kn_row) return TL_EUNSUPPORTED;
     // A 32-row tile of a short weight (K < 1024: under 64 KB per tile, e.g. a
     // Qwen expert's down projection, K = 768) is little work per workgroup;
     // 64-row tiles halve the workgroups and their fixed costs (down: -3 %).

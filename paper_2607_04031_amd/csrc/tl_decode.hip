@@ -475,6 +475,8 @@ hipError_t launch_decode(const DecodeLaunch& d, hipStream_t stream) {
     const int grid = grouped ? d.num_groups * p.tiles_per_group : p.tiles_per_group * d.split_k;
     const int ns = d.tile_n / 16;
     hipError_t e;
+    if (d.L.kind == TL_LAYOUT_KN_ROW)
+        return launch_splitk_reduce(d, launch_kn_decode(p, grid, d.m_tiles16, d.waves, stream), stream);
     if (d.fp8) return launch_splitk_reduce(d, launch_fp8_decode(p, grid, d.m_tiles16, ns, d.waves, tile, stream), stream);
     switch (d.m_tiles16) {
         case 1: e = launch_m<1>(p, grid, ns, d.waves, tile, grouped, stream); break;

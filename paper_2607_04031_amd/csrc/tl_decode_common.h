@@ -83,6 +83,11 @@ __device__ inline bf16x8 load_stream(const uint8_t* p) {
 hipError_t launch_fp8_decode(const DecodeParams& p, int grid, int m_tiles16, int ns, int waves, bool tile,
                              hipStream_t stream);
 
+// Decode over a [K][N] row-major weight (tl_decode_kn.hip): 64-column tiles,
+// p.units 64-row K steps split p.split_k ways, 4 or 8 waves; block-granular
+// fetch when p.log2_fetch > 0.
+hipError_t launch_kn_decode(const DecodeParams& p, int grid, int m_tiles16, int waves, hipStream_t stream);
+
 // Decode with activations staged in LDS (tl_decode_lds.hip): M <= 32,
 // tile-major, tiles_per_wg (4..7) 32-row tiles per workgroup, p.units
 // chunks of 512 columns split p.split_k ways.

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_strerror_strings():
-    for st in (tl.TL_OK, tl.TL_EINVAL, tl.TL_EUNSUPPORTED, tl.TL_EHIP, tl.TL_ENOMEM):
+    for st in (tl.TL_OK, tl.TL_EINVAL, tl.TL_EUNSUPPORTED, tl.TL_EHIP, tl.TL_ENOMEM, tl.TL_ESCRATCH):
         assert tl.tl_strerror(st).startswith("TL_")
     assert "unknown" in tl.tl_strerror(12345)
 
@@ -250,7 +250,7 @@ def test_gemm_plan_error_codes():
         ((2048, 64, 100, d), tl.TL_EUNSUPPORTED),
         ((8, 64, 72, tl.layout(elem_bytes=1, block_rows=64)), tl.TL_EUNSUPPORTED),   # FP8: K % 16
         ((8, 64, 64, tl.layout(elem_bytes=4)), tl.TL_EUNSUPPORTED),    # only bf16 and FP8 weights
-        ((8, 64, 64, tl.layout(kind=tl.TL_LAYOUT_KN_ROW)), tl.TL_EUNSUPPORTED),
+        ((256, 64, 64, tl.layout(kind=tl.TL_LAYOUT_KN_ROW)), tl.TL_EUNSUPPORTED),   # [K][N]: decode only
         ((8, 64, 64, tl.layout(G=512, block_rows=64)), tl.TL_EUNSUPPORTED),   # bc = 4
         ((8, 64, 64, tl.layout(out_dtype=7)), tl.TL_EINVAL),
         ((8, 64, 64, tl.layout(tile_n=48)), tl.TL_EUNSUPPORTED),
@@ -277,6 +277,54 @@ def test_gemm_plan_error_codes():
         with pytest.raises(tl.TLError) as e:
             tl.tl_gemm_plan(8, N, K, rm, tl.TL_FETCH_BLOCK)
         assert e.value.status == tl.TL_EUNSUPPORTED
+
+
+def test_kn_row_plans():
+    """A weight stored [K][N] (the paper's row-major layout) runs the decode
+    kernel with 64-column tiles and 64-row K steps; its plan rules."""
+    kn = tl.layout(kind=tl.TL_LAYOUT_KN_ROW)
+    for M, N, K in ((1, 1024, 4096), (8, 57344, 8192), (32, 8192, 28672), (64, 8, 64)):
+        p = tl.tl_gemm_plan(M, N, K, kn, tl.TL_FETCH_NATIVE)
+        assert p["kernel"] == 1 and p["tile_n"] == 64 and p["tile_k"] == 64
+        assert p["tile_m"] == 16 * {1: 1, 2: 2, 3: 4, 4: 4}[-(-M // 16)]
+        assert p["workgroups"] == -(-N // 64) * p["split_k"]
+        assert K // 64 >= p["split_k"] >= 1 and p["waves"] in (4, 8)
+    assert tl.tl_gemm_plan(8, 57344, 8192, kn)["split_k"] == 1          # 896 tiles: no K split
+    assert tl.tl_gemm_plan(8, 4096, 8192, kn, tl.TL_FETCH_NATIVE)["split_k"] == 8
+    blk = tl.layout(kind=tl.TL_LAYOUT_KN_ROW, G=4096)
+    assert tl.tl_gemm_plan(8, 1024, 2048, blk, tl.TL_FETCH_BLOCK)["tile_n"] == 64
+    rejected = [
+        ((65, 1024, 1024, kn, 0), tl.TL_EUNSUPPORTED),       # decode kernel only
+        ((8, 1024, 1000, kn, 0), tl.TL_EUNSUPPORTED),        # whole 64-row K steps
+        ((8, 1020, 1024, kn, 0), tl.TL_EUNSUPPORTED),        # 16-byte row pieces
+        ((8, 1024, 1024, tl.layout(kind=tl.TL_LAYOUT_KN_ROW, tile_n=32), 0), tl.TL_EUNSUPPORTED),
+        ((8, 1024, 1024, tl.layout(kind=tl.TL_LAYOUT_KN_ROW, elem_bytes=1), 0), tl.TL_EUNSUPPORTED),
+        ((8, 1000, 1024, blk, tl.TL_FETCH_BLOCK), tl.TL_EUNSUPPORTED),   # block: 128-byte row segments
+        ((8, 1024, 1024, tl.layout(kind=tl.TL_LAYOUT_KN_ROW, G=100), tl.TL_FETCH_BLOCK), tl.TL_EINVAL),
+        ((8, 1 << 27, 64, kn, 0), tl.TL_EUNSUPPORTED),       # one lane's eight rows span < 2^31 bytes
+    ]
+    for (M, N, K, d, f), want in rejected:
+        with pytest.raises(tl.TLError) as e:
+            tl.tl_gemm_plan(M, N, K, d, f)
+        assert e.value.status == want, (M, N, K)
+
+
+def test_noalloc_rejects_before_device_work():
+    """tl_gemm_noalloc: partials beyond the static scratch -> TL_ESCRATCH and
+    the per-stream tally -> TL_EUNSUPPORTED, before any HIP call; its
+    arguments are otherwise checked as tl_gemm's."""
+    d = tl.layout(split_k=16)
+    assert tl.tl_gemm_plan(64, 16384, 65536, d)["workspace_bytes"] > tl.TL_NOALLOC_SCRATCH_BYTES
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm_noalloc(4096, 8192, 16384, 64, 16384, 65536, d, tl.TL_FETCH_BLOCK, stream=0)
+    assert e.value.status == tl.TL_ESCRATCH
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm_noalloc(4096, 8192, 16384, 8, 64, 64, tl.layout(), tl.TL_FETCH_BLOCK | tl.TL_FETCH_COUNT,
+                           stream=0)
+    assert e.value.status == tl.TL_EUNSUPPORTED
+    with pytest.raises(tl.TLError) as e:
+        tl.tl_gemm_noalloc(0, 0, 0, 8, 64, 64, tl.layout(), tl.TL_FETCH_BLOCK, stream=0)
+    assert e.value.status == tl.TL_EINVAL
 
 
 def test_gemm_plan_maximum_sizes():
