@@ -230,7 +230,6 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
     const bool tile = d->kind == TL_LAYOUT_TILE;
     p.k_unit = tile ? std::max<int64_t>(64, p.L.bc) : 64;
 
-    if (p.block_row && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;   // decode kernel only
     if (p.fp8 && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;        // FP8: decode kernel only
     if (p.kn_row) {
         // 64-column tiles (128-byte row segments), K split until there are
@@ -413,8 +412,9 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.n_main = N;
         const int64_t mt = (M + tm - 1) / tm;
         const int64_t tiles = mt * ((N + tn - 1) / tn);
+        // (not with the block emulation: its count follows one tile shape)
         if (!d->tile_m && !d->tile_n && tm == 256 && tn == 256 && N % 256 == 0 && tiles > kCUs &&
-            tiles % kCUs != 0 && (!tile || 128 % p.L.br == 0)) {
+            tiles % kCUs != 0 && (!tile || 128 % p.L.br == 0) && !p.block_row) {
             for (int64_t n1 = N - 256; n1 >= 256; n1 -= 256) {
                 if ((mt * (n1 / 256)) % kCUs) continue;
                 const int64_t rest = ((M + 127) / 128) * ((N - n1) / 128);
@@ -563,6 +563,8 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
         q.tile_n = p.pub.tile_n;
         q.out_bf16 = p.out_bf16;
         q.n_main = p.n_main;
+        q.block_fetch = p.block_row;
+        q.fetch_G = p.fetch_G;
         e = launch_prefill(q, s);
     }
     return e == hipSuccess ? TL_OK : TL_EHIP;

@@ -110,6 +110,8 @@ struct PrefillLaunch {
     // columns [0, n_main) use tile_m x tile_n tiles; columns [n_main, N), if
     // any, a second launch of 128 x 128 tiles (n_main is a multiple of tile_n)
     int64_t n_main;
+    bool block_fetch = false;   // row-major weight read in whole fetch_G-byte blocks
+    int64_t fetch_G = 0;
 };
 
 hipError_t launch_prefill(const PrefillLaunch& p, hipStream_t stream);

@@ -43,6 +43,8 @@ struct PrefillParams {
     int log2_br, log2_bc, log2_G;
     int br_mask, bc_mask;
     bool out_bf16;
+    int log2_fetch;          // block-granular emulation on a row-major weight: log2(G), else 0
+    int64_t w_bytes;         // bytes of the weight (the block loads stay below it)
 };
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
@@ -59,8 +61,17 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
 // touches 16 distinct 16-byte bank groups.
 __device__ inline int swz(int row, int chunk) { return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4); }
 
-template <int BM, int BN, int WGM, int WGN, bool TILE>
+typedef int i32x4p __attribute__((ext_vector_type(4)));
+
+// BLOCKROW (row-major weight, TL_FETCH_BLOCK): before the weight loads of a K
+// step, the workgroup loads whole every G-byte block (aligned to the weight's
+// base) that holds one of its BN row segments -- rows in address order, so a
+// block shared by consecutive rows is loaded once per step -- into a live
+// sink and counts it: a large-granularity memory's amplification (Section
+// 2.5) paid as real HBM traffic; the operand loads then hit in cache.
+template <int BM, int BN, int WGM, int WGN, bool TILE, bool BLOCKROW = false>
 __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p) {
+    static_assert(!(TILE && BLOCKROW), "block emulation is for row-major weights");
     constexpr int NT = 64 * WGM * WGN;   // threads; waves form a WGM x WGN grid
     constexpr int BK = 64;
     constexpr int A_BYTES = BM * BK * 2, W_BYTES = BN * BK * 2;
@@ -122,8 +133,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
         return uint32_t(k) << 1;
     };
     const int KT = (p.K + BK - 1) / BK;
+    i32x4p sink = {0, 0, 0, 0};
+    uint64_t fetched = 0;
+    auto fetch_blocks = [&](int k0) {
+        if constexpr (BLOCKROW) {
+            const int64_t Gb = int64_t(1) << p.log2_fetch;
+            int64_t prev = -1;
+            for (int r = 0; r < BN; ++r) {
+                const int64_t n = min(n0 + r, p.N - 1);
+                const int64_t blk = ((n * p.K + k0) * 2) >> p.log2_fetch;
+                if (blk == prev) continue;
+                prev = blk;
+                const uint8_t* base = p.W + (blk << p.log2_fetch);
+                for (int64_t c = int64_t(t) * 16; c < Gb; c += int64_t(NT) * 16)
+                    if ((blk << p.log2_fetch) + c < p.w_bytes)
+                        sink ^= __builtin_nontemporal_load(reinterpret_cast<const i32x4p*>(base + c));
+                fetched += uint64_t(Gb);
+            }
+        }
+    };
     auto gload = [&](int kstep) {
         const int k0 = kstep * BK;
+        fetch_blocks(k0);
         if (k0 + BK <= p.K) {   // uniform: every step but a partial last one
 #pragma unroll
             for (int i = 0; i < A_CH; ++i) ra[i] = *a_addr(i, k0);
@@ -216,7 +247,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
         __syncthreads();
     }
 
-    if (p.fetch && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)W_BYTES);
+    if (p.fetch && t == 0)
+        atomicAdd(p.fetch, BLOCKROW ? (unsigned long long)fetched : (unsigned long long)KT * (unsigned long long)W_BYTES);
+    if constexpr (BLOCKROW) {
+        // keeps the block loads live; M >= 1 always, so this never stores
+        if ((sink[0] ^ sink[1] ^ sink[2] ^ sink[3]) == 0x6c8e9cf5 && p.M < 0) static_cast<float*>(p.C)[0] = 0.f;
+    }
 
     // D layout of a 32x32 MFMA tile: lane l, register v holds
     // row 8*(v/4) + 4*(l/32) + v%4, column l%32.
@@ -254,6 +290,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
 template <int BM, int BN, int WGM, int WGN>
 hipError_t launch_t(const PrefillParams& p, int grid, bool tile, hipStream_t s) {
     if (tile) hipLaunchKernelGGL((prefill_kernel<BM, BN, WGM, WGN, true>), dim3(grid), dim3(64 * WGM * WGN), 0, s, p);
+    else if (p.log2_fetch > 0)
+        hipLaunchKernelGGL((prefill_kernel<BM, BN, WGM, WGN, false, true>), dim3(grid), dim3(64 * WGM * WGN), 0, s, p);
     else hipLaunchKernelGGL((prefill_kernel<BM, BN, WGM, WGN, false>), dim3(grid), dim3(64 * WGM * WGN), 0, s, p);
     return hipGetLastError();
 }
@@ -285,6 +323,8 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
     p.br_mask = tile ? int(q.L.br - 1) : 0;
     p.bc_mask = tile ? int(q.L.bc - 1) : 0;
     p.out_bf16 = q.out_bf16;
+    p.log2_fetch = (!tile && q.block_fetch) ? ilog2(q.fetch_G) : 0;
+    p.w_bytes = n_cols * kp * 2;
     const int64_t n_tiles = (n_cols + tile_n - 1) / tile_n;
     const int grid = int(p.m_tiles * n_tiles);
     // 256x256: 8 waves (2 per SIMD) of 128x64; smaller tiles: 4 waves in 2 x 2

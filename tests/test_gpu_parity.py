@@ -383,8 +383,32 @@ def test_prefill_row_major_native():
     parity(C, oracle.gemm_f64(A, W), "prefill NK_ROW")
 
 
+@pytest.mark.parametrize("M,N,K,G,tm,tn", [(256, 512, 1024, 4096, 0, 0), (300, 384, 2048, 1024, 128, 128),
+                                           (512, 1024, 512, 16384, 256, 256), (129, 96, 256, 128, 256, 128),
+                                           (1024, 2048, 1024, 4096, 0, 0)])
+def test_prefill_row_major_block_fetch_counted(M, N, K, G, tm, tn):
+    """Prefill over a row-major weight read in whole G-byte blocks: same
+    result, and the bytes the kernel counts while loading the blocks equal
+    tl_read_amp's fetched bytes for the plan's tile and the oracle's
+    brute-force enumeration (rows share a block when K * 2 < G; a ragged last
+    tile clips its rows)."""
+    banner(f"prefill NK_ROW block fetch M={M} N={N} K={K} G={G} tile {tm}x{tn}")
+    A = synth.normal_bf16((M, K), seed=31 + M)
+    W = synth.normal_bf16((N, K), seed=32 + N, sigma=synth.W_SIGMA)
+    d = tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=G, tile_m=tm, tile_n=tn)
+    p = tl.tl_gemm_plan(M, N, K, d, tl.TL_FETCH_BLOCK)
+    assert p["kernel"] == 2
+    tl.tl_fetch_counter_read()
+    C = run_gemm(A, W, d, fetch=tl.TL_FETCH_BLOCK | tl.TL_FETCH_COUNT, tile_major=False)
+    got = tl.tl_fetch_counter_read()
+    parity(host_f32(C), oracle.gemm_f64(A, W), f"prefill block G={G}")
+    amp = tl.tl_read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, G)
+    want = oracle.read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], oracle.NK_ROW, G)
+    assert got == amp["fetched_bytes"] == want["fetched_bytes"], (got, amp, want)
+
+
 # ---------------------------------------------------------------------------
-# Full-size workloads, sampled outputs
+# Full-size workloads
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("i,name,N,K", [(i, *s) for i, s in enumerate(synth.LLAMA70B)])

@@ -270,9 +270,10 @@ def test_gemm_plan_error_codes():
         with pytest.raises(tl.TLError) as e:
             tl.tl_gemm_plan(8, 64, 64, tl.layout(kind=tl.TL_LAYOUT_NK_ROW, G=bad_G), tl.TL_FETCH_BLOCK)
         assert e.value.status == tl.TL_EINVAL
-    with pytest.raises(tl.TLError) as e:
-        tl.tl_gemm_plan(256, 64, 64, rm, tl.TL_FETCH_BLOCK)
-    assert e.value.status == tl.TL_EUNSUPPORTED
+    # above 64 rows the prefill kernel emulates it too, with one tile shape
+    # (no column split) so tl_read_amp follows its count
+    pp = tl.tl_gemm_plan(2048, 10240, 8192, rm, tl.TL_FETCH_BLOCK)
+    assert pp["kernel"] == 2 and pp["workgroups"] == (2048 // pp["tile_m"]) * (10240 // pp["tile_n"])
     for N, K in ((64, 96), (40, 64)):          # the block emulation needs whole 64-wide steps and 32-row tiles
         with pytest.raises(tl.TLError) as e:
             tl.tl_gemm_plan(8, N, K, rm, tl.TL_FETCH_BLOCK)
