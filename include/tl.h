@@ -77,8 +77,15 @@ enum {
                               relative to the weight's base) is needed, load the
                               whole block: emulates a large-granularity memory
                               on HBM (Sections 2.2 and 2.5) */
-    TL_FETCH_COUNT = 0x100 /* OR-able: tally the weight bytes the kernel issues
-                              into this stream's fetch counter */
+    TL_FETCH_COUNT = 0x100 /* OR-able: tally weight bytes into this stream's
+                              fetch counter.  With BLOCK on a row- or
+                              column-major weight: G per whole block the
+                              kernel loads (counted as it loads them).
+                              Otherwise: the bytes of the weight load
+                              instructions of every K step the kernel issues
+                              (a construction check that each byte is loaded
+                              once; HBM traffic itself is what a hardware
+                              counter such as FETCH_SIZE measures) */
 };
 
 /* Layout descriptor: the memory-tile shape travels as a runtime argument, so
@@ -186,8 +193,9 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  *      For TL_LAYOUT_TILE both modes load whole memory tiles (the compute tile
  *      is a whole number of memory tiles).  For TL_LAYOUT_NK_ROW and
  *      TL_LAYOUT_KN_ROW, BLOCK loads every layout->G-byte block a K step
- *      touches, whole (decode kernel only; G a power of two,
- *      128 <= G <= 2^30): the amplification of Section 2.5 paid as real HBM
+ *      touches, whole (G a power of two, 128 <= G <= 2^30; NK_ROW in both
+ *      kernels, without the prefill plan's column split; KN_ROW in the
+ *      decode kernel): the amplification of Section 2.5 paid as real HBM
  *      traffic, and the blocks loaded are counted by TL_FETCH_COUNT.
  * TL_LAYOUT_KN_ROW (W stored [K][N], N contiguous: the paper's row-major
  * layout) runs a decode kernel (M <= 64) that loads each 64-row K step of a
@@ -207,8 +215,8 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * TL_EUNSUPPORTED for elem_bytes other than 1 or 2, K not a multiple of
  * 16 / elem_bytes (one 16-byte load: keeps rows of A 16-byte aligned),
  * block_cols * elem_bytes < 16, a combination of layout, fetch mode and tile
- * that no kernel implements (NK_ROW with BLOCK above 64 rows, with FP8, or
- * with K % 64 or N % 32 != 0; FP8 above 64 rows; KN_ROW above 64 rows, with
+ * that no kernel implements (NK_ROW with BLOCK with FP8, or with K % 64 or
+ * N % 32 != 0; FP8 above 64 rows; KN_ROW above 64 rows, with
  * FP8, or outside the shape rules above), or sizes
  * past the kernels' 32-bit byte offsets: for M <= 64, 2 * M * K or the bytes
  * of tile_n weight rows (tile_n * K * elem_bytes, K padded for tile-major)

@@ -1,26 +1,26 @@
 // Prefill GEMM (large M): C[M][N] = A[M][K] * W^T with bf16 MFMA 32x32x16 and
 // fp32 accumulation; W tile-major (or row-major [N][K]).  MFMA-bound at large
 // batch (TileLens Section 6.2: the dense FFN becomes compute-bound as the batch
-// grows).
+// grows).  Per-lane weight addresses are Eq. 2 with shifts and masks (Section
+// 3.2); for the (64, 32) BF16 memory tile a 64-wide K step of a weight tile is
+// a whole number of 4 KB memory tiles.
 //
-// Workgroup tile BM x BN x 64: 128x128 and 256x128 with 4 wavefronts in a
-// 2 x 2 grid, 256x256 with 8 wavefronts in a 2 x 4 grid (two per SIMD, so one
-// wave's MFMAs cover the other's LDS and barrier waits); each wave owns a block
-// of C as MFMA 32x32 tiles.
-// Per 64-wide K step the workgroup stages its A tile and its weight tile in
-// LDS; the weight tile of a (64, 32) BF16 memory tile layout is exactly four
-// whole 4 KB memory tiles, so each wavefront load instruction reads 1 KB of
-// one contiguous memory tile.  Per-lane weight addresses are Eq. 2 with shifts
-// and masks (Section 3.2).  The next K step's global loads are issued before
-// the current step's MFMAs (register double buffering; LDS is double buffered
-// so one barrier per step suffices); LDS operand fragments for the next
-// 16-wide sub-step are read while the current sub-step's MFMAs run.  LDS rows
-// are 128 B with 16-byte chunks XOR-swizzled (see swz) so operand reads are
-// free of bank conflicts.
+// Two kernels:
+//  - prefill_w4_kernel (256 x 256 tiles, K % 64 == 0): four waves of
+//    128 x 128, operands written to LDS straight from global memory (see the
+//    comment above it).  The library's plan for large M.
+//  - prefill_kernel (128 x 128, 256 x 128, and 256 x 256 when K % 64 != 0 or
+//    with the row-major block emulation): each K step stages the A tile and
+//    the weight tile through registers into LDS (double buffered, one barrier
+//    per step); 4 waves in a 2 x 2 grid, or 8 in 2 x 4 for 256 x 256.  LDS
+//    rows are 128 B with 16-byte chunks XOR-swizzled (see swz) so operand
+//    reads are free of bank conflicts.
 // Padded weights (Section 3.3; strips of ceil(K / bc) memory tiles): rows
-// past M or N are clamped and never stored; a last K step partly past K
-// (K % 8 == 0) stages zeros for the chunks past K.
+// past M or N are clamped and never stored; in prefill_kernel a last K step
+// partly past K (K % 8 == 0) stages zeros for the chunks past K.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "tl_internal.h"
 
@@ -287,6 +287,227 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
     }
 }
 
+// One 16-byte-per-lane load from global memory straight into LDS
+// (global_load_lds_dwordx4): lane l's 16 bytes at base + voff land at LDS
+// address lds + 16 l (lds is the same for every lane of the wave; M0 carries
+// it).  Written as inline assembly so the compiler does not see an LDS write
+// it cannot place -- it would otherwise wait for every load in flight before
+// any later LDS read; the kernel waits for these loads itself (vmcnt).  A
+// device function, so the LDS address-space cast stays out of code the host
+// compilation pass instantiates.  Nothing else in the kernels that call it
+// uses M0.
+__device__ inline void load_lds16(const uint8_t* base, uint32_t voff, uint8_t* lds) {
+    const uint32_t la = uint32_t(uintptr_t((__attribute__((address_space(3))) void*)lds));
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "s"(la)
+                 : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
+// s_waitcnt vmcnt(n) alone (expcnt and lgkmcnt left free), n < 64
+#define TL_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
+
+template <bool TILE, bool OUT_BF16>
+__global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
+    constexpr int BM = 256, BN = 256, BK = 64;
+    constexpr int HALF = BM * BK * 2;            // A (or W) tile of a step: 32 KB
+    constexpr int STAGE = 2 * HALF;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+
+    const int T = gridDim.x, b = blockIdx.x;
+    const int lb = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
+    const int tm = lb % p.m_tiles, tn = lb / p.m_tiles;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+
+    // loads: wave w writes rows 64 w .. 64 w + 63 of both tiles, eight
+    // instructions of 8 rows each; lane l: row + l / 8, LDS position l % 8
+    const int lrow = lane >> 3, lpos = lane & 7;
+    const uint8_t* Ab = reinterpret_cast<const uint8_t*>(p.A);
+    uint32_t a_off[8], w_row[8];
+    int w_ch[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int r = 64 * wave + 8 * i + lrow;
+        const int c = lpos ^ ((r >> 1) & 7);
+        w_ch[i] = c;
+        const uint32_t m = uint32_t(min(m0 + r, p.M - 1));
+        a_off[i] = (m * uint32_t(p.K) + uint32_t(c * 8)) * 2u;
+        const uint32_t n = uint32_t(min(n0 + r, p.N - 1));
+        if (TILE) w_row[i] = (n >> p.log2_br) * uint32_t(p.strip_bytes) + ((n & uint32_t(p.br_mask)) << (p.log2_bc + 1));
+        else w_row[i] = n * uint32_t(p.K) * 2u;
+    }
+    auto w_koff = [&](int k) -> uint32_t {
+        if (TILE) return (uint32_t(k >> p.log2_bc) << p.log2_G) + uint32_t((k & p.bc_mask) << 1);
+        return uint32_t(k) << 1;
+    };
+    // load q (0..15) of step s: q < 8 the A rows 8 q .., q >= 8 the W rows
+    // 8 (q - 8) .. of this wave's 64-row share (W chunk at K = k0 + 8 c goes
+    // through Eq. 1)
+    auto issue_one = [&](int s, int q) {
+        uint8_t* buf = smem + (s & 1) * STAGE + wave * 8192;
+        const int k0 = s * BK;
+        if (q < 8) load_lds16(Ab, a_off[q] + uint32_t(k0) * 2u, buf + q * 1024);
+        else load_lds16(p.W, w_row[q - 8] + w_koff(k0 + w_ch[q - 8] * 8), buf + HALF + (q - 8) * 1024);
+    };
+    // fragments: lane reads row lane % 32 of its 32-row tile at K chunk
+    // 2 * sub-step + lane / 32; offsets of sub-step 0 (a sub-step adds 2
+    // chunks, XORed into the position)
+    int fa_row[4], fb_row[4];
+    int fa_sw[4], fb_sw[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int ra = wm * 128 + i * 32 + (lane & 31);
+        fa_row[i] = ra * 128;
+        fa_sw[i] = (ra >> 1) & 7;
+        const int rb = wn * 128 + i * 32 + (lane & 31);
+        fb_row[i] = HALF + rb * 128;
+        fb_sw[i] = (rb >> 1) & 7;
+    }
+    const int khalf = lane >> 5;
+    // fragment q (0..7) of sub-step ss of step s: q < 4 W tile q, else A tile
+    // q - 4 (the next sub-step's first MFMAs take A tile 0 with every W tile,
+    // so the W tiles are read first)
+    auto fread_one = [&](int s, int ss, int q, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
+        const uint8_t* buf = smem + (s & 1) * STAGE;
+        const int c = 2 * ss + khalf;
+        if (q < 4) fb[q] = *reinterpret_cast<const bf16x8*>(buf + fb_row[q] + ((c ^ fb_sw[q]) << 4));
+        else fa[q - 4] = *reinterpret_cast<const bf16x8*>(buf + fa_row[q - 4] + ((c ^ fa_sw[q - 4]) << 4));
+    };
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    // every wave meets the others; an LDS-only fence, so loads stay in flight
+    auto lds_barrier = [&]() {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    };
+    bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+    // one sub-step: 16 MFMAs on (fa, fb); after MFMA q, fragment q / 2 of
+    // sub-step rss of step rs into (ga, gb) when q is even (READ) and load
+    // q / 2 + lq0 of step ls when q is odd (LOAD).  READ and LOAD are
+    // compile-time, so the loop holds no branch between its MFMAs.
+    auto substep = [&](auto read_c, auto load_c, const bf16x8 (&fa)[4], const bf16x8 (&fb)[4], int rs, int rss,
+                       bf16x8 (&ga)[4], bf16x8 (&gb)[4], int ls, int lq0) {
+        constexpr bool READ = decltype(read_c)::value, LOAD = decltype(load_c)::value;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            acc[q >> 2][q & 3] =
+                __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q >> 2], fb[q & 3], acc[q >> 2][q & 3], 0, 0, 0);
+            if ((q & 1) == 0) {
+                if constexpr (READ) fread_one(rs, rss, q >> 1, ga, gb);
+            } else {
+                if constexpr (LOAD) issue_one(ls, lq0 + (q >> 1));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    const std::true_type Y{};
+    const std::false_type N{};
+
+    const int KT = p.K / BK;
+    // prologue: step 0 loaded and visible, its first fragments read, the
+    // first half of step 1's loads in flight
+#pragma unroll
+    for (int q = 0; q < 16; ++q) issue_one(0, q);
+    TL_WAIT_VMCNT(0);
+    lds_barrier();
+#pragma unroll
+    for (int q = 0; q < 8; ++q) fread_one(0, 0, q, fa0, fb0);
+    if (KT > 1)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) issue_one(1, q);
+    int s = 0;
+    for (; s + 2 < KT; ++s) {            // steady state: every load present
+        substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);   // rest of step s + 1's loads
+        substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
+        substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+        TL_WAIT_VMCNT(0);                // step s + 1 landed
+        lds_barrier();
+        // first fragments of step s + 1, first half of step s + 2's loads
+        // (into the stage step s has finished reading)
+        substep(Y, Y, fa1, fb1, s + 1, 0, fa0, fb0, s + 2, 0);
+    }
+    if (s + 1 < KT) {                    // step KT - 2: no step KT to load
+        substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);
+        substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
+        substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+        TL_WAIT_VMCNT(0);
+        lds_barrier();
+        substep(Y, N, fa1, fb1, s + 1, 0, fa0, fb0, 0, 0);
+        ++s;
+    }
+    // the last step
+    substep(Y, N, fa0, fb0, s, 1, fa1, fb1, 0, 0);
+    substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
+    substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+    substep(N, N, fa1, fb1, 0, 0, fa0, fb0, 0, 0);
+
+    if (p.fetch && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)HALF);
+
+    // D layout of a 32x32 MFMA tile: lane l, register v holds
+    // row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32
+    if constexpr (OUT_BF16) {
+        // through LDS (the operand buffers are free once every wave is past
+        // its last MFMA): the 256 x 256 bf16 tile, 512-byte rows, then
+        // 16-byte stores of eight consecutive columns
+        TL_WAIT_VMCNT(0);
+        __syncthreads();
+        uint16_t* Cs = reinterpret_cast<uint16_t*>(smem);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int r = wm * 128 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                    const int c = wn * 128 + j * 32 + (lane & 31);
+                    Cs[r * 256 + c] = f32_to_bf16_rne(acc[i][j][v]);
+                }
+        __syncthreads();
+        uint16_t* C = static_cast<uint16_t*>(p.C);
+        for (int e = t; e < 256 * 32; e += 256) {
+            const int r = e >> 5, c = (e & 31) * 8;
+            const int row = m0 + r, col = n0 + c;
+            if (row >= p.M) continue;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(Cs + r * 256 + c);
+            uint16_t* dst = C + int64_t(row) * p.ldc + col;
+            if (col + 8 <= p.N && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
+                *reinterpret_cast<u32x4*>(dst) = v;
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q)
+                    if (col + q < p.N) dst[q] = uint16_t(v[q >> 1] >> (16 * (q & 1)));
+            }
+        }
+    } else {
+        const bool full = m0 + BM <= p.M && n0 + BN <= p.N;
+        const int row_base = m0 + wm * 128 + 4 * (lane >> 5);
+        const int col_base = n0 + wn * 128 + (lane & 31);
+        float* C = static_cast<float*>(p.C);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float* Cij = C + int64_t(row_base + i * 32) * p.ldc + col_base + j * 32;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int dr = 8 * (v >> 2) + (v & 3);
+                    if (full || (row_base + i * 32 + dr < p.M && col_base + j * 32 < p.N)) Cij[int64_t(dr) * p.ldc] = acc[i][j][v];
+                }
+            }
+    }
+}
+
 template <int BM, int BN, int WGM, int WGN>
 hipError_t launch_t(const PrefillParams& p, int grid, bool tile, hipStream_t s) {
     if (tile) hipLaunchKernelGGL((prefill_kernel<BM, BN, WGM, WGN, true>), dim3(grid), dim3(64 * WGM * WGN), 0, s, p);
@@ -328,7 +549,19 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
     const int64_t n_tiles = (n_cols + tile_n - 1) / tile_n;
     const int grid = int(p.m_tiles * n_tiles);
     // 256x256: 8 waves (2 per SIMD) of 128x64; smaller tiles: 4 waves in 2 x 2
-    if (tile_m == 256 && tile_n == 256) return launch_t<256, 256, 2, 4>(p, grid, tile, stream);
+    if (tile_m == 256 && tile_n == 256) {
+        if (q.K % 64 == 0 && p.log2_fetch == 0) {
+            if (tile) {
+                if (p.out_bf16) hipLaunchKernelGGL((prefill_w4_kernel<true, true>), dim3(grid), dim3(256), 0, stream, p);
+                else hipLaunchKernelGGL((prefill_w4_kernel<true, false>), dim3(grid), dim3(256), 0, stream, p);
+            } else {
+                if (p.out_bf16) hipLaunchKernelGGL((prefill_w4_kernel<false, true>), dim3(grid), dim3(256), 0, stream, p);
+                else hipLaunchKernelGGL((prefill_w4_kernel<false, false>), dim3(grid), dim3(256), 0, stream, p);
+            }
+            return hipGetLastError();
+        }
+        return launch_t<256, 256, 2, 4>(p, grid, tile, stream);
+    }
     if (tile_m == 256) return launch_t<256, 128, 2, 2>(p, grid, tile, stream);
     return launch_t<128, 128, 2, 2>(p, grid, tile, stream);
 }

@@ -278,8 +278,13 @@ def test_decode_row_major_block_fetch_emulation(M, N, K, G):
     assert got == want["fetched_bytes"]
 
 
-def test_decode_fetch_counter_equals_read_amp():
-    """TL_FETCH_COUNT tally == tl_read_amp fetched bytes for the plan's tile."""
+def test_decode_issued_weight_bytes_equal_read_amp():
+    """Construction check: on a tile-major weight the TL_FETCH_COUNT tally is
+    the bytes of the weight loads of every K step the kernel issues, and it
+    equals tl_read_amp's fetched bytes for the plan's tile (= N * K * 2: each
+    memory tile is loaded once, whole).  The HBM bytes themselves are measured
+    by the FETCH_SIZE counter (committed profile); the row- and column-major
+    block emulations count the blocks they load."""
     M, N, K = 8, 1024, 2048
     banner("decode fetch counter")
     A = synth.normal_bf16((M, K), seed=17)

@@ -11,7 +11,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2607_04031_amd", "csrc")
 KERNEL_SOURCES = ["tl_repack.hip", "tl_decode.hip", "tl_decode_fp8.hip", "tl_decode_lds.hip", "tl_lgms.hip", "tl_prefill.hip",
-                  "tl_view.hip", "tl_stream.hip", "tl_decode_kn.hip", "tl_scratch.hip"]
+                  "tl_view.hip", "tl_stream.hip", "tl_decode_kn.hip"]
 
 
 @pytest.mark.parametrize("src", KERNEL_SOURCES)
