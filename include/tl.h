@@ -447,14 +447,14 @@ int tl_view_load(const void* src_tm, const tl_view* view, int64_t K, int64_t N, 
 int tl_stream_read(const void* src, int64_t bytes, uint32_t* checksum, void* stream);
 
 /* Bytes of the static device scratch behind tl_gemm_noalloc, per GPU. */
-#define TL_NOALLOC_SCRATCH_BYTES ((int64_t)32 << 20)
+#define TL_NOALLOC_SCRATCH_BYTES ((int64_t)64 << 20)
 
 /*
  * tl_gemm_noalloc -- for callers that cannot allocate device memory: code
  * under HIP graph capture, serving loops and harnesses that forbid hipMalloc.
  * Same arguments, plan, kernels and results as tl_gemm, except that the
  * split-K partials go to a static device array of TL_NOALLOC_SCRATCH_BYTES
- * bytes (32 MiB) instead of the stream's library workspace.  The array
+ * bytes (64 MiB) instead of the stream's library workspace.  The array
  * belongs to the library's code object: every GPU the library runs on holds
  * its own copy from the first use until the process ends.  This call
  * allocates and frees nothing (no hipMalloc, no library state); its first

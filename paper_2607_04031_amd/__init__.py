@@ -34,7 +34,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtl.so")
 
 TL_OK, TL_EINVAL, TL_EUNSUPPORTED, TL_EHIP, TL_ENOMEM, TL_ESCRATCH = 0, -1, -2, -3, -4, -5
-TL_NOALLOC_SCRATCH_BYTES = 32 << 20
+TL_NOALLOC_SCRATCH_BYTES = 64 << 20
 TL_LAYOUT_NK_ROW, TL_LAYOUT_KN_ROW, TL_LAYOUT_TILE = 0, 1, 2
 TL_OUT_F32, TL_OUT_BF16 = 0, 1
 TL_FETCH_NATIVE, TL_FETCH_BLOCK, TL_FETCH_COUNT = 0, 1, 0x100

@@ -162,6 +162,7 @@ struct Plan {
     bool fp8 = false;            // 1-byte (OCP E4M3) weight, decode kernel
     int lds_tiles = 0;           // > 0: decode with activations staged in LDS, tiles per workgroup
     bool kn_row = false;         // weight stored [K][N] (N contiguous): the transposing decode kernel
+    int split_rest = 0;          // prefill: K splits of the 256 x 256 tiles past n_main (0: 128 x 128 tiles)
 };
 
 constexpr int kDecodeMaxM = 64;
@@ -421,16 +422,32 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                 if (rest <= 2 * kCUs) p.n_main = n1;
                 break;
             }
+            // The remaining columns as 256 x 256 tiles of the four-wave
+            // kernel with K split S ways, when those tiles times S fill the
+            // CUs exactly and each split keeps >= 8 of the 64-wide K steps
+            // (fp32 partials summed in a fixed order by a second kernel):
+            // QKV at M = 2048, 64 tiles x 4 splits (on one box 1021 -> 1113
+            // TFLOP/s against the 128 x 128 tiles).
+            if (p.n_main < N && K % 64 == 0) {
+                const int64_t rest256 = mt * ((N - p.n_main) / 256);
+                if (rest256 > 0 && kCUs % rest256 == 0) {
+                    const int64_t S = kCUs / rest256;
+                    if (S >= 2 && S <= 8 && K / 64 / S >= 8) p.split_rest = int(S);
+                }
+            }
         }
         p.pub.tile_m = tm;
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
         p.pub.split_k = 1;
-        p.pub.waves = tm == 256 && tn == 256 ? 8 : 4;
+        p.pub.waves = tm == 256 && tn == 256 ? (K % 64 == 0 && !p.block_row ? 4 : 8) : 4;
         p.pub.workgroups = mt * (p.n_main / tn + (p.n_main % tn ? 1 : 0)) +
-                           ((M + 127) / 128) * ((N - p.n_main) / 128);
+                           (p.split_rest ? mt * ((N - p.n_main) / 256) * p.split_rest
+                                         : ((M + 127) / 128) * ((N - p.n_main) / 128));
         if (p.pub.workgroups >= (int64_t(1) << 31)) return TL_EUNSUPPORTED;   // one launch's grid
-        p.pub.workspace_bytes = 0;
+        // split_k reports the K splits of the remaining columns' tiles
+        p.pub.split_k = p.split_rest ? p.split_rest : 1;
+        p.pub.workspace_bytes = p.split_rest ? int64_t(p.split_rest) * M * (N - p.n_main) * 4 : 0;
     }
     *P = p;
     return TL_OK;
@@ -565,6 +582,8 @@ static int gemm_impl(const void* A, const void* W, const float* scales, void* C,
         q.n_main = p.n_main;
         q.block_fetch = p.block_row;
         q.fetch_G = p.fetch_G;
+        q.split_rest = p.split_rest;
+        q.ws = st.ws;
         e = launch_prefill(q, s);
     }
     return e == hipSuccess ? TL_OK : TL_EHIP;

@@ -112,6 +112,11 @@ struct PrefillLaunch {
     int64_t n_main;
     bool block_fetch = false;   // row-major weight read in whole fetch_G-byte blocks
     int64_t fetch_G = 0;
+    // > 1: columns [n_main, N) run as 256 x 256 tiles with K split this many
+    // ways (fp32 partials in ws, M * (N - n_main) floats per split) instead
+    // of 128 x 128 tiles
+    int split_rest = 0;
+    float* ws = nullptr;
 };
 
 hipError_t launch_prefill(const PrefillLaunch& p, hipStream_t stream);

@@ -45,6 +45,12 @@ struct PrefillParams {
     bool out_bf16;
     int log2_fetch;          // block-granular emulation on a row-major weight: log2(G), else 0
     int64_t w_bytes;         // bytes of the weight (the block loads stay below it)
+    // prefill_w4_kernel only: K split across workgroups (1 = none); split s
+    // writes its fp32 partial of the M x N range to ws + s * ws_stride
+    // (row stride N), summed by prefill_splitk_reduce
+    int split_k = 1;
+    float* ws = nullptr;
+    int64_t ws_stride = 0;
 };
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
@@ -313,12 +319,21 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     constexpr int BM = 256, BN = 256, BK = 64;
     constexpr int HALF = BM * BK * 2;            // A (or W) tile of a step: 32 KB
     constexpr int STAGE = 2 * HALF;
-    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+    constexpr int C_STAGE = BM * 576;            // bf16 epilogue: the C tile with 576-byte rows
+    constexpr int LDS_BYTES = (OUT_BF16 && C_STAGE > 2 * STAGE) ? C_STAGE : 2 * STAGE;
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+    __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
 
     const int T = gridDim.x, b = blockIdx.x;
     const int lb = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
-    const int tm = lb % p.m_tiles, tn = lb / p.m_tiles;
+    const int tiles = T / p.split_k;
+    const int split = lb / tiles, tile = lb - split * tiles;
+    const int tm = tile % p.m_tiles, tn = tile / p.m_tiles;
     const int m0 = tm * BM, n0 = tn * BN;
+    // this workgroup's 64-wide K steps: [kt0, kt0 + KT)
+    const int KT_all = p.K / BK;
+    const int kt0 = int((int64_t(KT_all) * split) / p.split_k);
+    const int KT = int((int64_t(KT_all) * (split + 1)) / p.split_k) - kt0;
 
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -350,7 +365,7 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     // through Eq. 1)
     auto issue_one = [&](int s, int q) {
         uint8_t* buf = smem + (s & 1) * STAGE + wave * 8192;
-        const int k0 = s * BK;
+        const int k0 = (kt0 + s) * BK;
         if (q < 8) load_lds16(Ab, a_off[q] + uint32_t(k0) * 2u, buf + q * 1024);
         else load_lds16(p.W, w_row[q - 8] + w_koff(k0 + w_ch[q - 8] * 8), buf + HALF + (q - 8) * 1024);
     };
@@ -414,7 +429,6 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     const std::true_type Y{};
     const std::false_type N{};
 
-    const int KT = p.K / BK;
     // prologue: step 0 loaded and visible, its first fragments read, the
     // first half of step 1's loads in flight
 #pragma unroll
@@ -457,21 +471,43 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     // D layout of a 32x32 MFMA tile: lane l, register v holds
     // row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32
     if constexpr (OUT_BF16) {
-        // through LDS (the operand buffers are free once every wave is past
-        // its last MFMA): the 256 x 256 bf16 tile, 512-byte rows, then
-        // 16-byte stores of eight consecutive columns
+        // through LDS (the operand stages are free once every wave is past
+        // its last MFMA): the 256 x 256 bf16 tile with 576-byte rows, then
+        // 16-byte stores of eight consecutive columns.  A lane holds four
+        // consecutive rows of one column per MFMA row group; the four lanes
+        // of a quad (four consecutive columns) transpose that 4 x 4 block
+        // with two DPP swaps, so each lane writes one row's four columns
+        // (8 bytes) -- the 576-byte stride puts those four rows in four
+        // distinct 64-byte bank ranges.
+        constexpr int CS = C_STAGE / BM;
         TL_WAIT_VMCNT(0);
         __syncthreads();
-        uint16_t* Cs = reinterpret_cast<uint16_t*>(smem);
+        uint8_t* Cs = smem;
+        const int qd = lane & 3;
+        const int rsel = ((qd & 1) << 1) | ((qd & 2) >> 1);   // row of the quad's block this lane writes
+        const int cquad = (lane & 31) & ~3;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int r = wm * 128 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                    const int c = wn * 128 + j * 32 + (lane & 31);
-                    Cs[r * 256 + c] = f32_to_bf16_rne(acc[i][j][v]);
+                for (int g = 0; g < 4; ++g) {
+                    const uint32_t h0 = f32_to_bf16_rne(acc[i][j][4 * g + 0]), h1 = f32_to_bf16_rne(acc[i][j][4 * g + 1]);
+                    const uint32_t h2 = f32_to_bf16_rne(acc[i][j][4 * g + 2]), h3 = f32_to_bf16_rne(acc[i][j][4 * g + 3]);
+                    // swap with lane ^ 1: even lanes keep rows 0-1, odd lanes rows 2-3
+                    const uint32_t send1 = (qd & 1) ? (h0 | (h1 << 16)) : (h2 | (h3 << 16));
+                    const uint32_t recv1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send1), 0xB1, 0xf, 0xf, false));
+                    const uint32_t x_first = (qd & 1) ? ((recv1 & 0xffffu) | (h2 << 16)) : (h0 | (recv1 << 16));
+                    const uint32_t x_second = (qd & 1) ? ((recv1 >> 16) | (h3 << 16)) : (h1 | (recv1 & 0xffff0000u));
+                    // swap with lane ^ 2: one row's four columns per lane
+                    const uint32_t send2 = (qd & 2) ? x_first : x_second;
+                    const uint32_t recv2 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send2), 0x4E, 0xf, 0xf, false));
+                    uint2 v;
+                    v.x = (qd & 2) ? recv2 : x_first;
+                    v.y = (qd & 2) ? x_second : recv2;
+                    const int r = wm * 128 + i * 32 + 8 * g + 4 * (lane >> 5) + rsel;
+                    const int c = wn * 128 + j * 32 + cquad;
+                    *reinterpret_cast<uint2*>(Cs + r * CS + c * 2) = v;
                 }
         __syncthreads();
         uint16_t* C = static_cast<uint16_t*>(p.C);
@@ -479,7 +515,7 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             const int r = e >> 5, c = (e & 31) * 8;
             const int row = m0 + r, col = n0 + c;
             if (row >= p.M) continue;
-            const u32x4 v = *reinterpret_cast<const u32x4*>(Cs + r * 256 + c);
+            const u32x4 v = *reinterpret_cast<const u32x4*>(Cs + r * CS + c * 2);
             uint16_t* dst = C + int64_t(row) * p.ldc + col;
             if (col + 8 <= p.N && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
                 *reinterpret_cast<u32x4*>(dst) = v;
@@ -490,21 +526,48 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             }
         }
     } else {
+        // fp32 output, or this split's fp32 partial (row stride N)
         const bool full = m0 + BM <= p.M && n0 + BN <= p.N;
         const int row_base = m0 + wm * 128 + 4 * (lane >> 5);
         const int col_base = n0 + wn * 128 + (lane & 31);
-        float* C = static_cast<float*>(p.C);
+        const bool part = p.split_k > 1;
+        float* C = part ? p.ws + int64_t(split) * p.ws_stride : static_cast<float*>(p.C);
+        const int64_t ldc = part ? int64_t(p.N) : p.ldc;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                float* Cij = C + int64_t(row_base + i * 32) * p.ldc + col_base + j * 32;
+                float* Cij = C + int64_t(row_base + i * 32) * ldc + col_base + j * 32;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int dr = 8 * (v >> 2) + (v & 3);
-                    if (full || (row_base + i * 32 + dr < p.M && col_base + j * 32 < p.N)) Cij[int64_t(dr) * p.ldc] = acc[i][j][v];
+                    if (full || (row_base + i * 32 + dr < p.M && col_base + j * 32 < p.N)) Cij[int64_t(dr) * ldc] = acc[i][j][v];
                 }
             }
+    }
+}
+
+// C[m][n] (row stride ldc) = sum over s = 0..S-1, in that order, of
+// ws[s * stride + m * N + n]: the K-split partials of prefill_w4_kernel,
+// four consecutive columns per thread (N % 4 == 0).  No float atomics, so
+// results are bitwise reproducible.
+template <bool OUT_BF16>
+__global__ __launch_bounds__(256) void prefill_splitk_reduce(const float* ws, int S, int64_t stride, int M, int N,
+                                                             void* C, int64_t ldc) {
+    typedef float f32x4p __attribute__((ext_vector_type(4)));
+    const int64_t e = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 4;
+    if (e >= int64_t(M) * N) return;
+    const int64_t m = e / N, n = e - m * N;
+    f32x4p acc = *reinterpret_cast<const f32x4p*>(ws + e);
+    for (int s = 1; s < S; ++s) acc += *reinterpret_cast<const f32x4p*>(ws + int64_t(s) * stride + e);
+    if (OUT_BF16) {
+        uint16_t* c = static_cast<uint16_t*>(C) + m * ldc + n;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) c[q] = f32_to_bf16_rne(acc[q]);
+    } else {
+        float* c = static_cast<float*>(C) + m * ldc + n;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) c[q] = acc[q];
     }
 }
 
@@ -571,7 +634,48 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
 hipError_t launch_prefill(const PrefillLaunch& q, hipStream_t stream) {
     hipError_t e = launch_range(q, 0, q.n_main, q.tile_m, q.tile_n, stream);
     if (e != hipSuccess || q.n_main == q.N) return e;
-    return launch_range(q, q.n_main, q.N - q.n_main, 128, 128, stream);
+    if (q.split_rest <= 1) return launch_range(q, q.n_main, q.N - q.n_main, 128, 128, stream);
+    // the remaining columns: 256 x 256 tiles of prefill_w4_kernel, K split
+    // split_rest ways (fp32 partials in ws), then the fixed-order reduce
+    const bool tile = q.L.kind == TL_LAYOUT_TILE;
+    const int64_t kp = tile ? padded_cols(q.L, q.K) : q.K;
+    const int64_t n_cols = q.N - q.n_main;
+    PrefillParams p;
+    p.A = q.A;
+    p.W = q.W + q.n_main * kp * 2;
+    p.C = nullptr;
+    p.fetch = q.fetch;
+    p.M = int(q.M);
+    p.N = int(n_cols);
+    p.K = int(q.K);
+    p.ldc = q.N;
+    p.m_tiles = int((q.M + 255) / 256);
+    p.strip_bytes = tile ? q.L.br * kp * 2 : 0;
+    p.log2_br = tile ? q.L.log2_br : 0;
+    p.log2_bc = tile ? q.L.log2_bc : 0;
+    p.log2_G = tile ? q.L.log2_G : 0;
+    p.br_mask = tile ? int(q.L.br - 1) : 0;
+    p.bc_mask = tile ? int(q.L.bc - 1) : 0;
+    p.out_bf16 = false;
+    p.log2_fetch = 0;
+    p.w_bytes = n_cols * kp * 2;
+    p.split_k = q.split_rest;
+    p.ws = q.ws;
+    p.ws_stride = q.M * n_cols;
+    const int grid = int(p.m_tiles * ((n_cols + 255) / 256) * q.split_rest);
+    if (tile) hipLaunchKernelGGL((prefill_w4_kernel<true, false>), dim3(grid), dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((prefill_w4_kernel<false, false>), dim3(grid), dim3(256), 0, stream, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    uint8_t* c0 = static_cast<uint8_t*>(q.C) + q.n_main * (q.out_bf16 ? 2 : 4);
+    const int rgrid = int((q.M * n_cols / 4 + 255) / 256);
+    if (q.out_bf16)
+        hipLaunchKernelGGL((prefill_splitk_reduce<true>), dim3(rgrid), dim3(256), 0, stream, q.ws, q.split_rest,
+                           p.ws_stride, p.M, p.N, (void*)c0, int64_t(q.N));
+    else
+        hipLaunchKernelGGL((prefill_splitk_reduce<false>), dim3(rgrid), dim3(256), 0, stream, q.ws, q.split_rest,
+                           p.ws_stride, p.M, p.N, (void*)c0, int64_t(q.N));
+    return hipGetLastError();
 }
 
 }  // namespace tl

@@ -315,9 +315,9 @@ def test_noalloc_rejects_before_device_work():
     the per-stream tally -> TL_EUNSUPPORTED, before any HIP call; its
     arguments are otherwise checked as tl_gemm's."""
     d = tl.layout(split_k=16)
-    assert tl.tl_gemm_plan(64, 16384, 65536, d)["workspace_bytes"] > tl.TL_NOALLOC_SCRATCH_BYTES
+    assert tl.tl_gemm_plan(64, 32768, 65536, d)["workspace_bytes"] > tl.TL_NOALLOC_SCRATCH_BYTES
     with pytest.raises(tl.TLError) as e:
-        tl.tl_gemm_noalloc(4096, 8192, 16384, 64, 16384, 65536, d, tl.TL_FETCH_BLOCK, stream=0)
+        tl.tl_gemm_noalloc(4096, 8192, 16384, 64, 32768, 65536, d, tl.TL_FETCH_BLOCK, stream=0)
     assert e.value.status == tl.TL_ESCRATCH
     with pytest.raises(tl.TLError) as e:
         tl.tl_gemm_noalloc(4096, 8192, 16384, 8, 64, 64, tl.layout(), tl.TL_FETCH_BLOCK | tl.TL_FETCH_COUNT,

@@ -106,7 +106,7 @@ def test_noalloc_rejections():
     W = torch.zeros(64 * 16, dtype=torch.bfloat16, device="cuda")
     C = torch.zeros(64 * 16, dtype=torch.float32, device="cuda")
     d = tl.layout(split_k=16)
-    M, N, K = 64, 16384, 65536                 # 16 splits x 64 x 16384 fp32 = 64 MiB of partials
+    M, N, K = 64, 32768, 65536                 # 16 splits x 64 x 32768 fp32 = 128 MiB of partials
     assert tl.tl_gemm_plan(M, N, K, d)["workspace_bytes"] > tl.TL_NOALLOC_SCRATCH_BYTES
     with pytest.raises(tl.TLError) as e:
         tl.tl_gemm_noalloc(A, W, C, M, N, K, d, tl.TL_FETCH_BLOCK)
