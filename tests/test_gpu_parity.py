@@ -354,6 +354,39 @@ def test_prefill_column_split_exact():
     assert np.array_equal(host_f32(C).astype(np.float64), oracle.gemm_f64(A, W))
 
 
+# Columns past the whole rounds of 256 x 256 tiles, run as 256 x 256 tiles
+# with K split S ways (fp32 partials, fixed-order reduce): M, N, K, S.
+# M = 2000 = 7 * 256 + 208 leaves a ragged last row of tiles.
+KSPLIT_REST = [(2000, 12288, 1024, 2), (2000, 10240, 2048, 4)]
+
+
+@pytest.mark.parametrize("M,N,K,S", KSPLIT_REST)
+def test_prefill_ksplit_rest(M, N, K, S):
+    plan = tl.tl_gemm_plan(M, N, K, tl.layout())
+    banner(f"prefill K-split rest M={M} N={N} K={K} plan={plan}")
+    assert plan["split_k"] == S and plan["workgroups"] == 512
+    assert plan["workspace_bytes"] == S * M * (N - 8192) * 4
+    A = synth.normal_bf16((M, K), seed=95 + S)
+    W = synth.normal_bf16((N, K), seed=96 + S, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    parity(host_f32(run_gemm(A, W, tl.layout())), y_ref, f"K-split rest S={S} f32")
+    Cb = run_gemm(A, W, tl.layout(out_dtype=tl.TL_OUT_BF16))
+    parity_bf16_out(host_bits(Cb), y_ref, f"K-split rest S={S} bf16")
+
+
+def test_prefill_ksplit_rest_exact():
+    """Small-integer inputs: exact in fp32 whatever the split, so the split
+    path equals the oracle bit for bit, and two calls are identical."""
+    M, N, K = 2000, 10240, 2048
+    banner("prefill K-split rest exact")
+    A = synth.small_int_bf16((M, K), seed=97)
+    W = synth.small_int_bf16((N, K), seed=98)
+    C1 = host_f32(run_gemm(A, W, tl.layout()))
+    C2 = host_f32(run_gemm(A, W, tl.layout()))
+    assert np.array_equal(C1.astype(np.float64), oracle.gemm_f64(A, W))
+    assert np.array_equal(C1, C2)
+
+
 def test_prefill_exact_inputs():
     M, N, K = 256, 256, 1024
     banner("prefill one-hot / small-int")

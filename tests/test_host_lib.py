@@ -227,12 +227,21 @@ def test_fp8_plans():
 def test_prefill_plan_column_split():
     """256 x 256 tiles whose count leaves the last round part-empty are kept on
     the widest column range with a whole number of rounds; the rest of the
-    columns take 128 x 128 tiles when those fit in one round."""
+    columns take 256 x 256 tiles with K split S ways when those tiles times S
+    fill the CUs (fp32 partials: split_k and workspace_bytes report them),
+    else 128 x 128 tiles when those fit in one round."""
     bf = tl.layout(out_dtype=tl.TL_OUT_BF16)
-    assert tl.tl_gemm_plan(2048, 10240, 8192, bf)["workgroups"] == 256 + 256      # QKV
-    assert tl.tl_gemm_plan(2048, 8192, 8192, bf)["workgroups"] == 256              # O: no split
+    qkv = tl.tl_gemm_plan(2048, 10240, 8192, bf)                                   # QKV
+    assert qkv["workgroups"] == 256 + 64 * 4
+    assert qkv["split_k"] == 4 and qkv["workspace_bytes"] == 4 * 2048 * 2048 * 4
+    o = tl.tl_gemm_plan(2048, 8192, 8192, bf)                                      # O: no split
+    assert o["workgroups"] == 256 and o["split_k"] == 1 and o["workspace_bytes"] == 0
     assert tl.tl_gemm_plan(2048, 57344, 8192, bf)["workgroups"] == 1792            # gate+up: 7 rounds
-    assert tl.tl_gemm_plan(4096, 10240, 8192, bf)["workgroups"] == 512 + 512
+    q4 = tl.tl_gemm_plan(4096, 10240, 8192, bf)
+    assert q4["workgroups"] == 512 + 128 * 2 and q4["split_k"] == 2
+    # K too short for the split (8 K steps per split at least): 128 x 128 rest
+    short = tl.tl_gemm_plan(2048, 10240, 1024, bf)
+    assert short["workgroups"] == 256 + 256 and short["split_k"] == 1
     # pinned tiles are never split
     pinned = tl.layout(tile_m=256, tile_n=256, out_dtype=tl.TL_OUT_BF16)
     assert tl.tl_gemm_plan(2048, 10240, 8192, pinned)["workgroups"] == 320
