@@ -127,7 +127,10 @@ typedef struct tl_plan {
     int32_t tile_m;      /* compute tile used by the kernel; with tile_k it is  */
     int32_t tile_n;      /* the tile to pass to tl_read_amp to account for the  */
     int32_t tile_k;      /* kernel's fetches                                     */
-    int32_t split_k;     /* workgroups per output tile along K */
+    int32_t split_k;     /* workgroups per output tile along K (prefill: > 1
+                            when the columns past the whole rounds of
+                            256 x 256 tiles run with their K split, fp32
+                            partials summed in a fixed order) */
     int32_t waves;       /* wavefronts per workgroup (decode: 4, 8 or 16; the
                             waves of a workgroup also split K, reduced in LDS) */
     int64_t workgroups;  /* grid size */
@@ -205,8 +208,11 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound; at 17 <= M <= 32
  * on tile-major weights whose 32-row tiles and 512-column K chunks fill the
  * CUs in whole rounds, a variant that stages the activations in LDS and
- * shares them across several tiles); larger M runs the prefill kernel (bf16
- * MFMA tiles 256x256x64, 256x128x64 or 128x128x64, MFMA-bound).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
+ * shares them across several tiles); larger M runs the prefill kernels (bf16
+ * MFMA tiles 256x256x64, 256x128x64 or 128x128x64, MFMA-bound; when
+ * 256x256 tiles would leave the last round of workgroups part-empty, the
+ * columns past the whole rounds take 256x256 tiles with K split across
+ * workgroups, or 128x128 tiles; see tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
  * byte per element, e.g. 64 x 64 memory tiles of 4 KB, Section 3.1): decode
  * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
  * per-channel scales).
@@ -466,8 +472,8 @@ int tl_stream_read(const void* src, int64_t bytes, uint32_t* checksum, void* str
  * its whole partial before the reduce kernel reads it).  Calls that overlap
  * on one GPU -- on two streams, or from two host threads -- race on the
  * array and give unspecified results: serialise them (one stream, or events).
- * A plan without K splits (split_k 1: e.g. prefill, or most M = 1..16 calls
- * on large weights) does not touch the array.
+ * A plan without K splits (split_k 1: most prefill plans, and most
+ * M = 1..16 calls on large weights) does not touch the array.
  * Errors: those of tl_gemm (except TL_ENOMEM); TL_ESCRATCH when the plan's
  * split-K partials (tl_gemm_plan's workspace_bytes) exceed
  * TL_NOALLOC_SCRATCH_BYTES -- layout->split_k can ask for fewer splits;

@@ -20,6 +20,7 @@ hipError_t launch_prefill(const PrefillLaunch&, hipStream_t) { std::abort(); }
 hipError_t launch_view_load(const uint8_t*, int64_t, const ViewProgram&, uint8_t*, hipStream_t) { std::abort(); }
 hipError_t launch_zero_u64(unsigned long long*, hipStream_t) { std::abort(); }
 hipError_t launch_stream_read(const uint8_t*, int64_t, unsigned*, hipStream_t) { std::abort(); }
+hipError_t scratch_address(float**) { std::abort(); }
 }  // namespace tl
 
 int main() {
@@ -76,6 +77,29 @@ int main() {
     rm.kind = TL_LAYOUT_NK_ROW;
     if (tl_gemm_plan(int64_t(1) << 26, int64_t(1) << 26, 16, &rm, TL_FETCH_NATIVE, &p) != TL_EUNSUPPORTED) ++bad;
     if (tl_gemm_plan(int64_t(1) << 16, int64_t(1) << 16, 16, &rm, TL_FETCH_NATIVE, &p) != TL_OK) ++bad;
+    // row-major [K][N] decode plans (native and block fetch), the prefill
+    // plan's K-split remaining columns, and the allocation-free entry
+    // point's rejections (before anything reaches the device)
+    tl_layout_desc kn = d;
+    kn.kind = TL_LAYOUT_KN_ROW;
+    for (int64_t M : {1, 8, 32, 64})
+        for (int64_t N : {64, 520, 8192})
+            if (tl_gemm_plan(M, N, 4096, &kn, TL_FETCH_NATIVE, &p) != TL_OK) ++bad;
+    if (tl_gemm_plan(8, 8192, 4096, &kn, TL_FETCH_BLOCK, &p) != TL_OK) ++bad;
+    if (tl_gemm_plan(8, 520, 4096, &kn, TL_FETCH_BLOCK, &p) != TL_EUNSUPPORTED) ++bad;
+    tl_layout_desc bf = d;
+    bf.out_dtype = TL_OUT_BF16;
+    if (tl_gemm_plan(2048, 10240, 8192, &bf, TL_FETCH_BLOCK, &p) != TL_OK || p.split_k != 4 ||
+        p.workspace_bytes != int64_t(4) * 2048 * 2048 * 4)
+        ++bad;
+    tl_layout_desc big = d;
+    big.split_k = 16;
+    const void* dp = reinterpret_cast<const void*>(uintptr_t(1) << 42);
+    if (tl_gemm_noalloc(dp, dp, const_cast<void*>(dp), 64, 32768, 65536, &big, TL_FETCH_BLOCK, nullptr) != TL_ESCRATCH)
+        ++bad;
+    if (tl_gemm_noalloc(dp, dp, const_cast<void*>(dp), 8, 64, 64, &d, TL_FETCH_BLOCK | TL_FETCH_COUNT, nullptr) !=
+        TL_EUNSUPPORTED)
+        ++bad;
     // tl_stream_read argument checks (no device work)
     uint32_t* ck = reinterpret_cast<uint32_t*>(uintptr_t(1) << 40);
     const void* src = reinterpret_cast<const void*>(uintptr_t(1) << 41);

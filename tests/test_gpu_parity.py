@@ -506,14 +506,14 @@ def test_llama_prefill_full_size_bands(i, name, N, K):
     want_cols = oracle.gemm_f64(A_bits, W_bits[cols])            # [M, 128]
     d_rows, d_cols = torch.from_numpy(rows).cuda(), torch.from_numpy(cols).cuda()
     # (0, 0): the library's plan (QKV: 256 x 256 tiles on columns [0, 8192),
-    # 128 x 128 tiles on the rest)
+    # 256 x 256 tiles with K split 4 ways on the rest)
     for tm, tn in ((128, 128), (256, 128), (256, 256), (0, 0)):
         d = tl.layout(tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16)
         plan = tl.tl_gemm_plan(M, N, K, d)
         ptm, ptn = plan["tile_m"], plan["tile_n"]
-        # every (m-tile, n-tile) of the plan -- and of the 128 x 128 tiles of
-        # a column split -- holds row-band elements: the band has rows in
-        # every 128-row block and all N columns
+        # every (m-tile, n-tile) of the plan -- and of either kind of tile
+        # past a column split -- holds row-band elements: the band has rows
+        # in every 128-row block and all N columns
         assert len(np.unique(rows // 128)) == M // 128 and len(np.unique(rows // ptm)) == -(-M // ptm)
         assert ptn % 128 == 0
         banner(f"llama prefill full {name} tile {tm}x{tn} plan={plan}")
