@@ -117,6 +117,10 @@ struct PrefillLaunch {
     // of 128 x 128 tiles
     int split_rest = 0;
     float* ws = nullptr;
+    // columns [0, n_main) with 256 x 256 tiles, bf16 out, M and n_main
+    // multiples of 256, K of 128, and more tiles than CUs: a persistent grid
+    // of one workgroup per CU walks the tiles
+    bool persist = false;
 };
 
 hipError_t launch_prefill(const PrefillLaunch& p, hipStream_t stream);

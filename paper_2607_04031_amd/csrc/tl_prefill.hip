@@ -51,13 +51,17 @@ struct PrefillParams {
     int split_k = 1;
     float* ws = nullptr;
     int64_t ws_stride = 0;
+    // prefill_w4_kernel with PERSIST: the number of tiles the grid deals out
+    int units = 0;
 };
 
+// fp32 -> bf16, round to nearest even; a NaN stays a (quiet) NaN.  One
+// comparison and a select, so unrolled epilogues stay branch-free.
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return uint16_t((u >> 16) | 0x0040u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return uint16_t(u >> 16);
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+    const uint32_t quiet = (u >> 16) | 0x0040u;
+    return uint16_t((u & 0x7fffffffu) > 0x7f800000u ? quiet : rounded);
 }
 
 // LDS byte offset of 16-byte chunk 'chunk' (0..7) of 128-byte row 'row'.
@@ -314,23 +318,42 @@ __device__ inline void load_lds16(const uint8_t* base, uint32_t voff, uint8_t* l
 // s_waitcnt vmcnt(n) alone (expcnt and lgkmcnt left free), n < 64
 #define TL_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
 
-template <bool TILE, bool OUT_BF16>
+// PERSIST (bf16 output, no K split, whole 256 x 256 tiles, an even number of
+// K steps): a grid of one workgroup per CU walks p.units tiles.  The next
+// tile's first K step is loaded during this tile's last two steps, and this
+// tile's C is stored straight from registers (bf16, quad-transposed: 8 bytes
+// of one row per lane), so no workgroup ends and starts between tiles and
+// the next tile's first loads are not waited for.
+template <bool TILE, bool OUT_BF16, bool PERSIST = false>
 __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
+    static_assert(!PERSIST || OUT_BF16, "the persistent grid writes bf16");
     constexpr int BM = 256, BN = 256, BK = 64;
     constexpr int HALF = BM * BK * 2;            // A (or W) tile of a step: 32 KB
     constexpr int STAGE = 2 * HALF;
     constexpr int C_STAGE = BM * 576;            // bf16 epilogue: the C tile with 576-byte rows
-    constexpr int LDS_BYTES = (OUT_BF16 && C_STAGE > 2 * STAGE) ? C_STAGE : 2 * STAGE;
+    constexpr int LDS_BYTES = (OUT_BF16 && !PERSIST && C_STAGE > 2 * STAGE) ? C_STAGE : 2 * STAGE;
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
 
-    const int T = gridDim.x, b = blockIdx.x;
-    const int lb = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
+    // work units (tile x K split) in XCD-aware order: unit u runs on XCD
+    // u mod 8 and each XCD takes a contiguous range of units.  A persistent
+    // grid takes units blockIdx.x + i * gridDim.x (gridDim.x a multiple of
+    // 8, so they stay on the workgroup's XCD).
+    const int T = PERSIST ? p.units : int(gridDim.x);
     const int tiles = T / p.split_k;
-    const int split = lb / tiles, tile = lb - split * tiles;
-    const int tm = tile % p.m_tiles, tn = tile / p.m_tiles;
-    const int m0 = tm * BM, n0 = tn * BN;
-    // this workgroup's 64-wide K steps: [kt0, kt0 + KT)
+    int v = blockIdx.x;
+    auto unit_of = [&](int u, int& um0, int& un0, int& us) {
+        const int lb = (T % 8 == 0) ? (u % 8) * (T / 8) + u / 8 : u;
+        us = lb / tiles;
+        const int tile = lb - us * tiles;
+        um0 = (tile % p.m_tiles) * BM;
+        un0 = (tile / p.m_tiles) * BN;
+    };
+    if (v >= T) return;
+    int m0, n0, split;
+    unit_of(v, m0, n0, split);
+    // this workgroup's 64-wide K steps: [kt0, kt0 + KT) (every unit of a
+    // persistent grid: split 0, all of K)
     const int KT_all = p.K / BK;
     const int kt0 = int((int64_t(KT_all) * split) / p.split_k);
     const int KT = int((int64_t(KT_all) * (split + 1)) / p.split_k) - kt0;
@@ -345,17 +368,20 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     const uint8_t* Ab = reinterpret_cast<const uint8_t*>(p.A);
     uint32_t a_off[8], w_row[8];
     int w_ch[8];
+    auto set_rows = [&](int um0, int un0) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int r = 64 * wave + 8 * i + lrow;
-        const int c = lpos ^ ((r >> 1) & 7);
-        w_ch[i] = c;
-        const uint32_t m = uint32_t(min(m0 + r, p.M - 1));
-        a_off[i] = (m * uint32_t(p.K) + uint32_t(c * 8)) * 2u;
-        const uint32_t n = uint32_t(min(n0 + r, p.N - 1));
-        if (TILE) w_row[i] = (n >> p.log2_br) * uint32_t(p.strip_bytes) + ((n & uint32_t(p.br_mask)) << (p.log2_bc + 1));
-        else w_row[i] = n * uint32_t(p.K) * 2u;
-    }
+        for (int i = 0; i < 8; ++i) {
+            const int r = 64 * wave + 8 * i + lrow;
+            const int c = lpos ^ ((r >> 1) & 7);
+            w_ch[i] = c;
+            const uint32_t m = uint32_t(min(um0 + r, p.M - 1));
+            a_off[i] = (m * uint32_t(p.K) + uint32_t(c * 8)) * 2u;
+            const uint32_t n = uint32_t(min(un0 + r, p.N - 1));
+            if (TILE) w_row[i] = (n >> p.log2_br) * uint32_t(p.strip_bytes) + ((n & uint32_t(p.br_mask)) << (p.log2_bc + 1));
+            else w_row[i] = n * uint32_t(p.K) * 2u;
+        }
+    };
+    set_rows(m0, n0);
     auto w_koff = [&](int k) -> uint32_t {
         if (TILE) return (uint32_t(k >> p.log2_bc) << p.log2_G) + uint32_t((k & p.bc_mask) << 1);
         return uint32_t(k) << 1;
@@ -394,12 +420,15 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
         else fa[q - 4] = *reinterpret_cast<const bf16x8*>(buf + fa_row[q - 4] + ((c ^ fa_sw[q - 4]) << 4));
     };
     f32x16 acc[4][4];
+    auto zero_acc = [&]() {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    };
+    zero_acc();
     // every wave meets the others; an LDS-only fence, so loads stay in flight
     auto lds_barrier = [&]() {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
@@ -429,121 +458,198 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     const std::true_type Y{};
     const std::false_type N{};
 
-    // prologue: step 0 loaded and visible, its first fragments read, the
-    // first half of step 1's loads in flight
+    // quad transpose of the bf16 C: a lane holds four consecutive rows of one
+    // column per MFMA row group; the four lanes of a quad (four consecutive
+    // columns) swap 2 x 2 blocks with lane ^ 1 and then with lane ^ 2, so each
+    // lane ends with one row's four columns (8 bytes) -- row
+    // 8 g + 4 (l / 32) + qrow of MFMA tile (i, j), columns 4 (l % 32 / 4) ..
+    const int qd = lane & 3;
+    const int qrow = ((qd & 1) << 1) | ((qd & 2) >> 1);
+    const int cquad = (lane & 31) & ~3;
+    // lane-select masks (all ones on odd lanes / on lanes 2 and 3 of a quad):
+    // the swaps below pick with masks, so the unrolled code has no branches
+    const uint32_t odd = 0u - uint32_t(qd & 1), hi2 = 0u - uint32_t((qd >> 1) & 1);
+    auto pick = [](uint32_t mask, uint32_t a, uint32_t b) { return b ^ ((a ^ b) & mask); };   // mask ? a : b
+    // before the first quad_pack after the MFMAs: 24 wait states, more than
+    // any MFMA-result read hazard needs (the reads below are inline assembly,
+    // which the compiler's hazard check does not see into; the other tiles'
+    // reads come hundreds of instructions after their MFMAs)
+    auto mfma_settle = []() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); };
+    auto quad_pack = [&](int i, int j, int g) -> uint2 {
+        // the four sums, read out of their AGPRs here (an asm the compiler
+        // cannot move, so the reads of one MFMA tile happen where it is used)
+        float f0, f1, f2, f3;
+        asm volatile("v_accvgpr_read_b32 %0, %4\n\tv_accvgpr_read_b32 %1, %5\n\t"
+                     "v_accvgpr_read_b32 %2, %6\n\tv_accvgpr_read_b32 %3, %7"
+                     : "=v"(f0), "=v"(f1), "=v"(f2), "=v"(f3)
+                     : "a"(acc[i][j][4 * g + 0]), "a"(acc[i][j][4 * g + 1]), "a"(acc[i][j][4 * g + 2]),
+                       "a"(acc[i][j][4 * g + 3]));
+        const uint32_t h0 = f32_to_bf16_rne(f0), h1 = f32_to_bf16_rne(f1);
+        const uint32_t h2 = f32_to_bf16_rne(f2), h3 = f32_to_bf16_rne(f3);
+        // swap with lane ^ 1: even lanes keep rows 0-1, odd lanes rows 2-3
+        const uint32_t send1 = pick(odd, h0 | (h1 << 16), h2 | (h3 << 16));
+        const uint32_t recv1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send1), 0xB1, 0xf, 0xf, false));
+        const uint32_t x_first = pick(odd, (recv1 & 0xffffu) | (h2 << 16), h0 | (recv1 << 16));
+        const uint32_t x_second = pick(odd, (recv1 >> 16) | (h3 << 16), h1 | (recv1 & 0xffff0000u));
+        // swap with lane ^ 2: one row's four columns per lane
+        const uint32_t send2 = pick(hi2, x_first, x_second);
+        const uint32_t recv2 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send2), 0x4E, 0xf, 0xf, false));
+        uint2 r;
+        r.x = pick(hi2, recv2, x_first);
+        r.y = pick(hi2, x_second, recv2);
+        return r;
+    };
+
+    // first step of the first unit in flight
 #pragma unroll
     for (int q = 0; q < 16; ++q) issue_one(0, q);
-    TL_WAIT_VMCNT(0);
-    lds_barrier();
-#pragma unroll
-    for (int q = 0; q < 8; ++q) fread_one(0, 0, q, fa0, fb0);
-    if (KT > 1)
-#pragma unroll
-        for (int q = 0; q < 8; ++q) issue_one(1, q);
-    int s = 0;
-    for (; s + 2 < KT; ++s) {            // steady state: every load present
-        substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);   // rest of step s + 1's loads
-        substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
-        substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
-        TL_WAIT_VMCNT(0);                // step s + 1 landed
-        lds_barrier();
-        // first fragments of step s + 1, first half of step s + 2's loads
-        // (into the stage step s has finished reading)
-        substep(Y, Y, fa1, fb1, s + 1, 0, fa0, fb0, s + 2, 0);
-    }
-    if (s + 1 < KT) {                    // step KT - 2: no step KT to load
-        substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);
-        substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
-        substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+    for (;;) {
+        // step 0 loaded and visible, its first fragments read, the first
+        // half of step 1's loads in flight
         TL_WAIT_VMCNT(0);
         lds_barrier();
-        substep(Y, N, fa1, fb1, s + 1, 0, fa0, fb0, 0, 0);
-        ++s;
-    }
-    // the last step
-    substep(Y, N, fa0, fb0, s, 1, fa1, fb1, 0, 0);
-    substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
-    substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
-    substep(N, N, fa1, fb1, 0, 0, fa0, fb0, 0, 0);
-
-    if (p.fetch && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)HALF);
-
-    // D layout of a 32x32 MFMA tile: lane l, register v holds
-    // row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32
-    if constexpr (OUT_BF16) {
-        // through LDS (the operand stages are free once every wave is past
-        // its last MFMA): the 256 x 256 bf16 tile with 576-byte rows, then
-        // 16-byte stores of eight consecutive columns.  A lane holds four
-        // consecutive rows of one column per MFMA row group; the four lanes
-        // of a quad (four consecutive columns) transpose that 4 x 4 block
-        // with two DPP swaps, so each lane writes one row's four columns
-        // (8 bytes) -- the 576-byte stride puts those four rows in four
-        // distinct 64-byte bank ranges.
-        constexpr int CS = C_STAGE / BM;
-        TL_WAIT_VMCNT(0);
-        __syncthreads();
-        uint8_t* Cs = smem;
-        const int qd = lane & 3;
-        const int rsel = ((qd & 1) << 1) | ((qd & 2) >> 1);   // row of the quad's block this lane writes
-        const int cquad = (lane & 31) & ~3;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int q = 0; q < 8; ++q) fread_one(0, 0, q, fa0, fb0);
+        if (KT > 1)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const uint32_t h0 = f32_to_bf16_rne(acc[i][j][4 * g + 0]), h1 = f32_to_bf16_rne(acc[i][j][4 * g + 1]);
-                    const uint32_t h2 = f32_to_bf16_rne(acc[i][j][4 * g + 2]), h3 = f32_to_bf16_rne(acc[i][j][4 * g + 3]);
-                    // swap with lane ^ 1: even lanes keep rows 0-1, odd lanes rows 2-3
-                    const uint32_t send1 = (qd & 1) ? (h0 | (h1 << 16)) : (h2 | (h3 << 16));
-                    const uint32_t recv1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send1), 0xB1, 0xf, 0xf, false));
-                    const uint32_t x_first = (qd & 1) ? ((recv1 & 0xffffu) | (h2 << 16)) : (h0 | (recv1 << 16));
-                    const uint32_t x_second = (qd & 1) ? ((recv1 >> 16) | (h3 << 16)) : (h1 | (recv1 & 0xffff0000u));
-                    // swap with lane ^ 2: one row's four columns per lane
-                    const uint32_t send2 = (qd & 2) ? x_first : x_second;
-                    const uint32_t recv2 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send2), 0x4E, 0xf, 0xf, false));
-                    uint2 v;
-                    v.x = (qd & 2) ? recv2 : x_first;
-                    v.y = (qd & 2) ? x_second : recv2;
-                    const int r = wm * 128 + i * 32 + 8 * g + 4 * (lane >> 5) + rsel;
-                    const int c = wn * 128 + j * 32 + cquad;
-                    *reinterpret_cast<uint2*>(Cs + r * CS + c * 2) = v;
-                }
-        __syncthreads();
-        uint16_t* C = static_cast<uint16_t*>(p.C);
-        for (int e = t; e < 256 * 32; e += 256) {
-            const int r = e >> 5, c = (e & 31) * 8;
-            const int row = m0 + r, col = n0 + c;
-            if (row >= p.M) continue;
-            const u32x4 v = *reinterpret_cast<const u32x4*>(Cs + r * CS + c * 2);
-            uint16_t* dst = C + int64_t(row) * p.ldc + col;
-            if (col + 8 <= p.N && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
-                *reinterpret_cast<u32x4*>(dst) = v;
-            } else {
-#pragma unroll
-                for (int q = 0; q < 8; ++q)
-                    if (col + q < p.N) dst[q] = uint16_t(v[q >> 1] >> (16 * (q & 1)));
-            }
+            for (int q = 0; q < 8; ++q) issue_one(1, q);
+        int s = 0;
+        for (; s + 2 < KT; ++s) {            // steady state: every load present
+            substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);   // rest of step s + 1's loads
+            substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
+            substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+            TL_WAIT_VMCNT(0);                // step s + 1 landed
+            lds_barrier();
+            // first fragments of step s + 1, first half of step s + 2's loads
+            // (into the stage step s has finished reading)
+            substep(Y, Y, fa1, fb1, s + 1, 0, fa0, fb0, s + 2, 0);
         }
-    } else {
-        // fp32 output, or this split's fp32 partial (row stride N)
-        const bool full = m0 + BM <= p.M && n0 + BN <= p.N;
-        const int row_base = m0 + wm * 128 + 4 * (lane >> 5);
-        const int col_base = n0 + wn * 128 + (lane & 31);
-        const bool part = p.split_k > 1;
-        float* C = part ? p.ws + int64_t(split) * p.ws_stride : static_cast<float*>(p.C);
-        const int64_t ldc = part ? int64_t(p.N) : p.ldc;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                float* Cij = C + int64_t(row_base + i * 32) * ldc + col_base + j * 32;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int dr = 8 * (v >> 2) + (v & 3);
-                    if (full || (row_base + i * 32 + dr < p.M && col_base + j * 32 < p.N)) Cij[int64_t(dr) * ldc] = acc[i][j][v];
-                }
+        // PERSIST: the next unit (or, after the last one, this unit again:
+        // loads nothing reads) and its tile origin
+        int nv = v, nm0 = m0, nn0 = n0;
+        if (s + 1 < KT) {                    // step KT - 2: no step KT to load
+            substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);
+            substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
+            substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+            TL_WAIT_VMCNT(0);
+            lds_barrier();
+            if constexpr (PERSIST) {
+                // the next unit's first step goes into the stage step KT - 2
+                // has just finished reading (stage 0: KT is even) -- its A
+                // half now, its W half during the last step -- so it lands
+                // under this tile's last MFMAs
+                nv = v + int(gridDim.x);
+                int ns;
+                if (nv < T) unit_of(nv, nm0, nn0, ns);
+                set_rows(nm0, nn0);
+                substep(Y, Y, fa1, fb1, s + 1, 0, fa0, fb0, 0, 0);
+            } else {
+                substep(Y, N, fa1, fb1, s + 1, 0, fa0, fb0, 0, 0);
             }
+            ++s;
+        }
+        // the last step
+        if constexpr (PERSIST) substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, 0, 8);
+        else substep(Y, N, fa0, fb0, s, 1, fa1, fb1, 0, 0);
+        substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
+        substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+        substep(N, N, fa1, fb1, 0, 0, fa0, fb0, 0, 0);
+
+        if (p.fetch && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)HALF);
+
+        if constexpr (PERSIST) {
+            // whole tiles only (the launcher's condition; a uniform test, so
+            // the stores need no per-lane bounds)
+            mfma_settle();
+            if (m0 + BM <= p.M && n0 + BN <= p.N) {
+                uint16_t* Cw = static_cast<uint16_t*>(p.C) + int64_t(m0 + wm * 128 + 4 * (lane >> 5) + qrow) * p.ldc +
+                               (n0 + wn * 128 + cquad);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+                        for (int g = 0; g < 4; ++g)
+                            *reinterpret_cast<uint2*>(Cw + int64_t(i * 32 + 8 * g) * p.ldc + j * 32) = quad_pack(i, j, g);
+                        // one MFMA tile at a time: keeps the accumulator reads
+                        // from being hoisted into 256 VGPRs at once
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+            }
+            // every accumulator is read before it is cleared (else the two
+            // sets of 256 overlap and spill)
+            __builtin_amdgcn_sched_barrier(0);
+            zero_acc();
+            if (nv >= T) {
+                TL_WAIT_VMCNT(0);        // the reloads land before the workgroup's LDS is released
+                break;
+            }
+            v = nv;
+            m0 = nm0;
+            n0 = nn0;
+        } else {
+            // D layout of a 32x32 MFMA tile: lane l, register v holds
+            // row 8 (v / 4) + 4 (l / 32) + v % 4, column l % 32
+            if constexpr (OUT_BF16) {
+                // through LDS (the operand stages are free once every wave is
+                // past its last MFMA): the 256 x 256 bf16 tile with 576-byte
+                // rows, each lane writing its quad-transposed 8 bytes (the
+                // stride puts a quad's four rows in four distinct 64-byte bank
+                // ranges), then 16-byte stores of eight consecutive columns
+                constexpr int CS = C_STAGE / BM;
+                TL_WAIT_VMCNT(0);
+                __syncthreads();
+                mfma_settle();
+                uint8_t* Cs = smem;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int r = wm * 128 + i * 32 + 8 * g + 4 * (lane >> 5) + qrow;
+                            const int c = wn * 128 + j * 32 + cquad;
+                            *reinterpret_cast<uint2*>(Cs + r * CS + c * 2) = quad_pack(i, j, g);
+                            __builtin_amdgcn_sched_barrier(0);
+                        }
+                __syncthreads();
+                uint16_t* C = static_cast<uint16_t*>(p.C);
+                for (int e = t; e < 256 * 32; e += 256) {
+                    const int r = e >> 5, c = (e & 31) * 8;
+                    const int row = m0 + r, col = n0 + c;
+                    if (row >= p.M) continue;
+                    const u32x4 cv = *reinterpret_cast<const u32x4*>(Cs + r * CS + c * 2);
+                    uint16_t* dst = C + int64_t(row) * p.ldc + col;
+                    if (col + 8 <= p.N && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
+                        *reinterpret_cast<u32x4*>(dst) = cv;
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 8; ++q)
+                            if (col + q < p.N) dst[q] = uint16_t(cv[q >> 1] >> (16 * (q & 1)));
+                    }
+                }
+            } else {
+                // fp32 output, or this split's fp32 partial (row stride N)
+                const bool full = m0 + BM <= p.M && n0 + BN <= p.N;
+                const int row_base = m0 + wm * 128 + 4 * (lane >> 5);
+                const int col_base = n0 + wn * 128 + (lane & 31);
+                const bool part = p.split_k > 1;
+                float* C = part ? p.ws + int64_t(split) * p.ws_stride : static_cast<float*>(p.C);
+                const int64_t ldc = part ? int64_t(p.N) : p.ldc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        float* Cij = C + int64_t(row_base + i * 32) * ldc + col_base + j * 32;
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) {
+                            const int dr = 8 * (e >> 2) + (e & 3);
+                            if (full || (row_base + i * 32 + dr < p.M && col_base + j * 32 < p.N)) Cij[int64_t(dr) * ldc] = acc[i][j][e];
+                        }
+                    }
+            }
+            break;
+        }
     }
 }
 
@@ -570,6 +676,10 @@ __global__ __launch_bounds__(256) void prefill_splitk_reduce(const float* ws, in
         for (int q = 0; q < 4; ++q) c[q] = acc[q];
     }
 }
+
+// workgroups of a persistent prefill grid: one per CU (a multiple of 8, so
+// each keeps to its XCD's range of tiles)
+constexpr int kPersistGrid = 256;
 
 template <int BM, int BN, int WGM, int WGN>
 hipError_t launch_t(const PrefillParams& p, int grid, bool tile, hipStream_t s) {
@@ -614,6 +724,17 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
     // 256x256: 8 waves (2 per SIMD) of 128x64; smaller tiles: 4 waves in 2 x 2
     if (tile_m == 256 && tile_n == 256) {
         if (q.K % 64 == 0 && p.log2_fetch == 0) {
+            // more than one round of whole tiles, bf16 out: one workgroup per
+            // CU walks them
+            if (q.persist && p.out_bf16 && grid > kPersistGrid && q.M % 256 == 0 && n_cols % 256 == 0 &&
+                q.K % 128 == 0) {
+                p.units = grid;
+                if (tile)
+                    hipLaunchKernelGGL((prefill_w4_kernel<true, true, true>), dim3(kPersistGrid), dim3(256), 0, stream, p);
+                else
+                    hipLaunchKernelGGL((prefill_w4_kernel<false, true, true>), dim3(kPersistGrid), dim3(256), 0, stream, p);
+                return hipGetLastError();
+            }
             if (tile) {
                 if (p.out_bf16) hipLaunchKernelGGL((prefill_w4_kernel<true, true>), dim3(grid), dim3(256), 0, stream, p);
                 else hipLaunchKernelGGL((prefill_w4_kernel<true, false>), dim3(grid), dim3(256), 0, stream, p);

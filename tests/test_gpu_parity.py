@@ -387,6 +387,43 @@ def test_prefill_ksplit_rest_exact():
     assert np.array_equal(C1, C2)
 
 
+# A persistent grid (one workgroup per CU) over more than one round of whole
+# 256 x 256 tiles with bf16 output: M, N, K, tile_m/tile_n pinned or not.
+#  - 512 tiles, two per workgroup;
+#  - 1024 tiles (four per workgroup) next to a second launch of 128 x 128
+#    tiles on the last 4096 columns (K too short for the K-split remainder);
+#  - 300 pinned tiles, not a multiple of 8 (units in plain order), 1 or 2 per
+#    workgroup.
+PERSIST_CASES = [(1024, 32768, 512, 0), (2048, 36864, 256, 0), (256, 76800, 256, 256)]
+
+
+@pytest.mark.parametrize("M,N,K,pin", PERSIST_CASES)
+def test_prefill_persistent_grid(M, N, K, pin):
+    d = tl.layout(tile_m=pin, tile_n=pin, out_dtype=tl.TL_OUT_BF16)
+    plan = tl.tl_gemm_plan(M, N, K, d)
+    banner(f"prefill persistent M={M} N={N} K={K} pin={pin} plan={plan}")
+    assert plan["workgroups"] >= 256 and plan["tile_m"] == 256
+    A = synth.normal_bf16((M, K), seed=130 + M // 256)
+    W = synth.normal_bf16((N, K), seed=131, sigma=synth.W_SIGMA)
+    parity_bf16_out(host_bits(run_gemm(A, W, d)), oracle.gemm_f64(A, W), f"persistent M={M} N={N}")
+
+
+def test_prefill_persistent_exact():
+    """Small-integer inputs through the persistent grid: every fp32 sum is
+    exact, so the bf16 output equals the oracle's exact result rounded to
+    bf16 (nearest even) bit for bit, and two calls are identical."""
+    M, N, K = 1024, 32768, 512
+    banner("prefill persistent exact")
+    A = synth.small_int_bf16((M, K), seed=132)
+    W = synth.small_int_bf16((N, K), seed=133)
+    d = tl.layout(out_dtype=tl.TL_OUT_BF16)
+    assert tl.tl_gemm_plan(M, N, K, d)["workgroups"] == 256
+    C1 = host_bits(run_gemm(A, W, d))
+    C2 = host_bits(run_gemm(A, W, d))
+    assert np.array_equal(C1, C2)
+    assert np.array_equal(C1, oracle.round_bf16(oracle.gemm_f64(A, W)))
+
+
 def test_prefill_exact_inputs():
     M, N, K = 256, 256, 1024
     banner("prefill one-hot / small-int")

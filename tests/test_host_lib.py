@@ -236,18 +236,24 @@ def test_prefill_plan_column_split():
     assert qkv["split_k"] == 4 and qkv["workspace_bytes"] == 4 * 2048 * 2048 * 4
     o = tl.tl_gemm_plan(2048, 8192, 8192, bf)                                      # O: no split
     assert o["workgroups"] == 256 and o["split_k"] == 1 and o["workspace_bytes"] == 0
-    assert tl.tl_gemm_plan(2048, 57344, 8192, bf)["workgroups"] == 1792            # gate+up: 7 rounds
+    # gate+up: 1792 tiles, 7 rounds -> a persistent grid of one workgroup per CU
+    assert tl.tl_gemm_plan(2048, 57344, 8192, bf)["workgroups"] == 256
+    # fp32 output, or a ragged M: one workgroup per tile
+    assert tl.tl_gemm_plan(2048, 57344, 8192, tl.layout())["workgroups"] == 1792
+    assert tl.tl_gemm_plan(2000, 57344, 8192, bf)["workgroups"] == 1792
     q4 = tl.tl_gemm_plan(4096, 10240, 8192, bf)
-    assert q4["workgroups"] == 512 + 128 * 2 and q4["split_k"] == 2
+    assert q4["workgroups"] == 256 + 128 * 2 and q4["split_k"] == 2          # 512 main tiles: persistent
     # K too short for the split (8 K steps per split at least): 128 x 128 rest
     short = tl.tl_gemm_plan(2048, 10240, 1024, bf)
     assert short["workgroups"] == 256 + 256 and short["split_k"] == 1
-    # pinned tiles are never split
+    # pinned tiles are never split: the 320 tiles go to a persistent grid
+    # (fp32 output: one workgroup per tile)
     pinned = tl.layout(tile_m=256, tile_n=256, out_dtype=tl.TL_OUT_BF16)
-    assert tl.tl_gemm_plan(2048, 10240, 8192, pinned)["workgroups"] == 320
+    assert tl.tl_gemm_plan(2048, 10240, 8192, pinned)["workgroups"] == 256
+    assert tl.tl_gemm_plan(2048, 10240, 8192, tl.layout(tile_m=256, tile_n=256))["workgroups"] == 320
     # a memory tile taller than the 128-row remainder tiles keeps one launch
     tall = tl.layout(G=65536, block_rows=256, out_dtype=tl.TL_OUT_BF16)
-    assert tl.tl_gemm_plan(2048, 10240, 8192, tall)["workgroups"] == 320
+    assert tl.tl_gemm_plan(2048, 10240, 8192, tall)["workgroups"] == 256
 
 
 def test_gemm_plan_error_codes():
