@@ -437,20 +437,21 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                 }
             }
         }
-        // More than one round of whole 256 x 256 tiles with bf16 output and
-        // an even number of 64-wide K steps: a persistent grid of one
-        // workgroup per CU walks them, loading a tile's first step under the
-        // previous tile's last MFMAs (gate+up at M = 2048, 7 tiles per CU:
-        // 1476 -> 1441 us on one box).
+        // Whole 256 x 256 tiles with bf16 output and an even number of
+        // 64-wide K steps: a persistent grid of at most one workgroup per CU
+        // walks them, loading a tile's first step under the previous tile's
+        // last MFMAs and storing C straight from registers (gate+up at
+        // M = 2048, 7 tiles per CU: 1476 -> 1441 us on one box; down, one
+        // tile per CU: 720 -> 706 us on another).
         const int64_t main_tiles = mt * (p.n_main / tn + (p.n_main % tn ? 1 : 0));
         p.persist = tm == 256 && tn == 256 && K % 128 == 0 && !p.block_row && p.out_bf16 && M % 256 == 0 &&
-                    p.n_main % 256 == 0 && main_tiles > kCUs;
+                    p.n_main % 256 == 0;
         p.pub.tile_m = tm;
         p.pub.tile_n = tn;
         p.pub.tile_k = int(p.k_unit);
         p.pub.split_k = 1;
         p.pub.waves = tm == 256 && tn == 256 ? (K % 64 == 0 && !p.block_row ? 4 : 8) : 4;
-        p.pub.workgroups = (p.persist ? kCUs : main_tiles) +
+        p.pub.workgroups = (p.persist ? std::min<int64_t>(main_tiles, kCUs) : main_tiles) +
                            (p.split_rest ? mt * ((N - p.n_main) / 256) * p.split_rest
                                          : ((M + 127) / 128) * ((N - p.n_main) / 128));
         // one launch's grid, and the persistent grid's tile count (an int

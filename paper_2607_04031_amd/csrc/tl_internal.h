@@ -118,8 +118,8 @@ struct PrefillLaunch {
     int split_rest = 0;
     float* ws = nullptr;
     // columns [0, n_main) with 256 x 256 tiles, bf16 out, M and n_main
-    // multiples of 256, K of 128, and more tiles than CUs: a persistent grid
-    // of one workgroup per CU walks the tiles
+    // multiples of 256, K of 128: a persistent grid of at most one
+    // workgroup per CU walks the tiles
     bool persist = false;
 };
 

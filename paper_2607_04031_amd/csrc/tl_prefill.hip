@@ -319,11 +319,12 @@ __device__ inline void load_lds16(const uint8_t* base, uint32_t voff, uint8_t* l
 #define TL_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
 
 // PERSIST (bf16 output, no K split, whole 256 x 256 tiles, an even number of
-// K steps): a grid of one workgroup per CU walks p.units tiles.  The next
-// tile's first K step is loaded during this tile's last two steps, and this
-// tile's C is stored straight from registers (bf16, quad-transposed: 8 bytes
-// of one row per lane), so no workgroup ends and starts between tiles and
-// the next tile's first loads are not waited for.
+// K steps): a grid of at most one workgroup per CU walks p.units tiles.  The
+// next tile's first K step is loaded during this tile's last two steps, and
+// this tile's C is stored straight from registers (bf16, quad-transposed: 8
+// bytes of one row per lane), so no workgroup ends and starts between tiles
+// and the next tile's first loads are not waited for.  (With one tile per
+// workgroup only the direct stores remain: no LDS round trip and barrier.)
 template <bool TILE, bool OUT_BF16, bool PERSIST = false>
 __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     static_assert(!PERSIST || OUT_BF16, "the persistent grid writes bf16");
@@ -677,8 +678,8 @@ __global__ __launch_bounds__(256) void prefill_splitk_reduce(const float* ws, in
     }
 }
 
-// workgroups of a persistent prefill grid: one per CU (a multiple of 8, so
-// each keeps to its XCD's range of tiles)
+// workgroups of a persistent prefill grid with more tiles than CUs: one per
+// CU (a multiple of 8, so each keeps to its XCD's range of tiles)
 constexpr int kPersistGrid = 256;
 
 template <int BM, int BN, int WGM, int WGN>
@@ -724,15 +725,14 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
     // 256x256: 8 waves (2 per SIMD) of 128x64; smaller tiles: 4 waves in 2 x 2
     if (tile_m == 256 && tile_n == 256) {
         if (q.K % 64 == 0 && p.log2_fetch == 0) {
-            // more than one round of whole tiles, bf16 out: one workgroup per
-            // CU walks them
-            if (q.persist && p.out_bf16 && grid > kPersistGrid && q.M % 256 == 0 && n_cols % 256 == 0 &&
-                q.K % 128 == 0) {
+            // whole tiles, bf16 out: at most one workgroup per CU walks them
+            if (q.persist && p.out_bf16 && q.M % 256 == 0 && n_cols % 256 == 0 && q.K % 128 == 0) {
                 p.units = grid;
+                const int pgrid = grid < kPersistGrid ? grid : kPersistGrid;
                 if (tile)
-                    hipLaunchKernelGGL((prefill_w4_kernel<true, true, true>), dim3(kPersistGrid), dim3(256), 0, stream, p);
+                    hipLaunchKernelGGL((prefill_w4_kernel<true, true, true>), dim3(pgrid), dim3(256), 0, stream, p);
                 else
-                    hipLaunchKernelGGL((prefill_w4_kernel<false, true, true>), dim3(kPersistGrid), dim3(256), 0, stream, p);
+                    hipLaunchKernelGGL((prefill_w4_kernel<false, true, true>), dim3(pgrid), dim3(256), 0, stream, p);
                 return hipGetLastError();
             }
             if (tile) {

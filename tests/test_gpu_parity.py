@@ -393,8 +393,9 @@ def test_prefill_ksplit_rest_exact():
 #  - 1024 tiles (four per workgroup) next to a second launch of 128 x 128
 #    tiles on the last 4096 columns (K too short for the K-split remainder);
 #  - 300 pinned tiles, not a multiple of 8 (units in plain order), 1 or 2 per
-#    workgroup.
-PERSIST_CASES = [(1024, 32768, 512, 0), (2048, 36864, 256, 0), (256, 76800, 256, 256)]
+#    workgroup;
+#  - 2 tiles with K = 128, the fewest K steps the kernel takes (two).
+PERSIST_CASES = [(1024, 32768, 512, 0), (2048, 36864, 256, 0), (256, 76800, 256, 256), (256, 512, 128, 256)]
 
 
 @pytest.mark.parametrize("M,N,K,pin", PERSIST_CASES)
@@ -402,7 +403,8 @@ def test_prefill_persistent_grid(M, N, K, pin):
     d = tl.layout(tile_m=pin, tile_n=pin, out_dtype=tl.TL_OUT_BF16)
     plan = tl.tl_gemm_plan(M, N, K, d)
     banner(f"prefill persistent M={M} N={N} K={K} pin={pin} plan={plan}")
-    assert plan["workgroups"] >= 256 and plan["tile_m"] == 256
+    assert plan["workgroups"] == min(256, (M // 256) * (N // 256)) + (512 if N == 36864 else 0)
+    assert plan["tile_m"] == 256
     A = synth.normal_bf16((M, K), seed=130 + M // 256)
     W = synth.normal_bf16((N, K), seed=131, sigma=synth.W_SIGMA)
     parity_bf16_out(host_bits(run_gemm(A, W, d)), oracle.gemm_f64(A, W), f"persistent M={M} N={N}")
