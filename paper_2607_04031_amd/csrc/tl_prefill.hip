@@ -368,33 +368,39 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     const int lrow = lane >> 3, lpos = lane & 7;
     const uint8_t* Ab = reinterpret_cast<const uint8_t*>(p.A);
     uint32_t a_off[8], w_row[8];
-    int w_ch[8];
+    // Eq. 1's byte offset of column k inside a strip (row-major: 2 k).  For a
+    // step start k0 (a multiple of 64) and a chunk start 8 c < 64 it splits,
+    // w_koff(k0 + 8 c) = w_koff(k0) + w_koff(8 c): a memory tile at least 64
+    // columns wide holds the whole step (the chunk only moves inside it), and
+    // a narrower one divides 64 (the step starts on a memory-tile boundary).
+    auto w_koff = [&](int k) -> uint32_t {
+        if (TILE) return (uint32_t(k >> p.log2_bc) << p.log2_G) + uint32_t((k & p.bc_mask) << 1);
+        return uint32_t(k) << 1;
+    };
+    // per-lane load offsets, fixed over the K loop: the A row and chunk; the
+    // weight row and Eq. 1's offset of the chunk (the step's share is a
+    // uniform base, so a load needs no vector arithmetic)
     auto set_rows = [&](int um0, int un0) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int r = 64 * wave + 8 * i + lrow;
             const int c = lpos ^ ((r >> 1) & 7);
-            w_ch[i] = c;
             const uint32_t m = uint32_t(min(um0 + r, p.M - 1));
             a_off[i] = (m * uint32_t(p.K) + uint32_t(c * 8)) * 2u;
             const uint32_t n = uint32_t(min(un0 + r, p.N - 1));
             if (TILE) w_row[i] = (n >> p.log2_br) * uint32_t(p.strip_bytes) + ((n & uint32_t(p.br_mask)) << (p.log2_bc + 1));
             else w_row[i] = n * uint32_t(p.K) * 2u;
+            w_row[i] += w_koff(c * 8);
         }
     };
     set_rows(m0, n0);
-    auto w_koff = [&](int k) -> uint32_t {
-        if (TILE) return (uint32_t(k >> p.log2_bc) << p.log2_G) + uint32_t((k & p.bc_mask) << 1);
-        return uint32_t(k) << 1;
-    };
     // load q (0..15) of step s: q < 8 the A rows 8 q .., q >= 8 the W rows
-    // 8 (q - 8) .. of this wave's 64-row share (W chunk at K = k0 + 8 c goes
-    // through Eq. 1)
+    // 8 (q - 8) .. of this wave's 64-row share
     auto issue_one = [&](int s, int q) {
         uint8_t* buf = smem + (s & 1) * STAGE + wave * 8192;
         const int k0 = (kt0 + s) * BK;
-        if (q < 8) load_lds16(Ab, a_off[q] + uint32_t(k0) * 2u, buf + q * 1024);
-        else load_lds16(p.W, w_row[q - 8] + w_koff(k0 + w_ch[q - 8] * 8), buf + HALF + (q - 8) * 1024);
+        if (q < 8) load_lds16(Ab + size_t(k0) * 2, a_off[q], buf + q * 1024);
+        else load_lds16(p.W + w_koff(k0), w_row[q - 8], buf + HALF + (q - 8) * 1024);
     };
     // fragments: lane reads row lane % 32 of its 32-row tile at K chunk
     // 2 * sub-step + lane / 32; offsets of sub-step 0 (a sub-step adds 2
