@@ -133,7 +133,8 @@ typedef struct tl_plan {
                             partials summed in a fixed order) */
     int32_t waves;       /* wavefronts per workgroup (decode: 4, 8 or 16; the
                             waves of a workgroup also split K, reduced in LDS) */
-    int64_t workgroups;  /* grid size */
+    int64_t workgroups;  /* grid size, summed over the call's launches (a
+                            persistent prefill grid: at most 256) */
     int64_t workspace_bytes;  /* split-K partials the call needs from the library */
 } tl_plan;
 
@@ -209,10 +210,12 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * on tile-major weights whose 32-row tiles and 512-column K chunks fill the
  * CUs in whole rounds, a variant that stages the activations in LDS and
  * shares them across several tiles); larger M runs the prefill kernels (bf16
- * MFMA tiles 256x256x64, 256x128x64 or 128x128x64, MFMA-bound; when
- * 256x256 tiles would leave the last round of workgroups part-empty, the
- * columns past the whole rounds take 256x256 tiles with K split across
- * workgroups, or 128x128 tiles; see tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
+ * MFMA tiles 256x256x64, 256x128x64 or 128x128x64, MFMA-bound; with bf16
+ * output, whole 256x256 tiles and K % 128 == 0 a persistent grid of at most
+ * 256 workgroups walks the tiles; when 256x256 tiles would leave the last
+ * round of workgroups part-empty, the columns past the whole rounds take
+ * 256x256 tiles with K split across workgroups, or 128x128 tiles; see
+ * tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
  * byte per element, e.g. 64 x 64 memory tiles of 4 KB, Section 3.1): decode
  * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
  * per-channel scales).
