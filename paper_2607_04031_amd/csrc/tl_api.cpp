@@ -406,6 +406,28 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         // the kernel addresses A and W with 32-bit byte offsets
         const int64_t wb = tile ? packed_bytes(p.L, N, K) : N * K * 2;
         if (M * K * 2 >= (int64_t(1) << 32) || wb >= (int64_t(1) << 32)) return TL_EUNSUPPORTED;
+        // 256 x 320 tiles (each wave 128 x 160 of C) where they fill the CUs
+        // in whole rounds and 256 x 256 tiles do not: QKV at M = 2048, 256
+        // tiles instead of 320 -- one round, no second launch, no partials
+        // (persistent bf16 only; no tile requested)
+        if (!d->tile_m && !d->tile_n && tm == 256 && p.out_bf16 && !p.block_row && K % 128 == 0 && M % 256 == 0 &&
+            N % 320 == 0 && (!tile || 320 % p.L.br == 0)) {
+            const int64_t t320 = (M / 256) * (N / 320);
+            const int64_t t256 = N % 256 == 0 ? (M / 256) * (N / 256) : 1;
+            if (t320 % kCUs == 0 && t256 % kCUs != 0 && t320 < (int64_t(1) << 31) - kCUs) {
+                p.n_main = N;
+                p.persist = true;
+                p.pub.tile_m = 256;
+                p.pub.tile_n = 320;
+                p.pub.tile_k = int(p.k_unit);
+                p.pub.split_k = 1;
+                p.pub.waves = 4;
+                p.pub.workgroups = kCUs;
+                p.pub.workspace_bytes = 0;
+                *P = p;
+                return TL_OK;
+            }
+        }
         // Quantisation: 256 x 256 tiles that leave the last round of
         // workgroups part-empty (QKV at M = 2048: 320 tiles on 256 CUs) cover
         // the widest column range whose tile count is a multiple of the CU

@@ -105,7 +105,7 @@ struct PrefillLaunch {
     int64_t M, N, K;
     Layout L;
     int tile_m;                 // 128 or 256
-    int tile_n;                 // 128 or 256 (256 only with tile_m 256)
+    int tile_n;                 // 128, 256 or 320 (256 and 320 only with tile_m 256; 320 persistent)
     bool out_bf16;
     // columns [0, n_main) use tile_m x tile_n tiles; columns [n_main, N), if
     // any, a second launch of 128 x 128 tiles (n_main is a multiple of tile_n)

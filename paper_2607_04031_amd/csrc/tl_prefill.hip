@@ -325,12 +325,24 @@ __device__ inline void load_lds16(const uint8_t* base, uint32_t voff, uint8_t* l
 // bytes of one row per lane), so no workgroup ends and starts between tiles
 // and the next tile's first loads are not waited for.  (With one tile per
 // workgroup only the direct stores remain: no LDS round trip and barrier.)
-template <bool TILE, bool OUT_BF16, bool PERSIST = false>
+//
+// NJ: 32-column MFMA tiles per wave along N -- 4 (256 x 256 tiles) or 5
+// (256 x 320 tiles, each wave 128 x 160 of C: 320 sums per lane, AGPRs and
+// VGPRs; persistent bf16 only, whose epilogue needs no LDS).  A 256 x 320
+// tile fills the CUs in whole rounds where 256 x 256 does not (QKV at
+// M = 2048: 256 tiles instead of 320).
+template <bool TILE, bool OUT_BF16, bool PERSIST = false, int NJ = 4>
 __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     static_assert(!PERSIST || OUT_BF16, "the persistent grid writes bf16");
-    constexpr int BM = 256, BN = 256, BK = 64;
-    constexpr int HALF = BM * BK * 2;            // A (or W) tile of a step: 32 KB
-    constexpr int STAGE = 2 * HALF;
+    static_assert(NJ == 4 || (NJ == 5 && PERSIST), "256 x 320 tiles: persistent bf16 only");
+    constexpr int BM = 256, BN = 64 * NJ, BK = 64;
+    constexpr int HALF = BM * BK * 2;            // A tile of a step: 32 KB
+    constexpr int WHALF = BN * BK * 2;           // W tile of a step: 32 or 40 KB
+    constexpr int STAGE = HALF + WHALF;
+    constexpr int WROWS = BN / 4;                // W rows each wave loads per step
+    constexpr int NWL = WROWS / 8;               // ... in loads of 8 rows: 8 or 10
+    constexpr int NLOAD = 8 + NWL;               // loads per step and wave
+    constexpr int NREAD = 4 + NJ;                // fragment reads per sub-step
     constexpr int C_STAGE = BM * 576;            // bf16 epilogue: the C tile with 576-byte rows
     constexpr int LDS_BYTES = (OUT_BF16 && !PERSIST && C_STAGE > 2 * STAGE) ? C_STAGE : 2 * STAGE;
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
@@ -363,11 +375,12 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
     const int wm = wave >> 1, wn = wave & 1;
 
-    // loads: wave w writes rows 64 w .. 64 w + 63 of both tiles, eight
-    // instructions of 8 rows each; lane l: row + l / 8, LDS position l % 8
+    // loads: wave w writes rows 64 w .. 64 w + 63 of the A tile and rows
+    // WROWS w .. WROWS (w + 1) - 1 of the W tile, in instructions of 8 rows;
+    // lane l: row + l / 8, LDS position l % 8
     const int lrow = lane >> 3, lpos = lane & 7;
     const uint8_t* Ab = reinterpret_cast<const uint8_t*>(p.A);
-    uint32_t a_off[8], w_row[8];
+    uint32_t a_off[8], w_row[NWL];
     // Eq. 1's byte offset of column k inside a strip (row-major: 2 k).  For a
     // step start k0 (a multiple of 64) and a chunk start 8 c < 64 it splits,
     // w_koff(k0 + 8 c) = w_koff(k0) + w_koff(8 c): a memory tile at least 64
@@ -387,6 +400,11 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             const int c = lpos ^ ((r >> 1) & 7);
             const uint32_t m = uint32_t(min(um0 + r, p.M - 1));
             a_off[i] = (m * uint32_t(p.K) + uint32_t(c * 8)) * 2u;
+        }
+#pragma unroll
+        for (int i = 0; i < NWL; ++i) {
+            const int r = WROWS * wave + 8 * i + lrow;
+            const int c = lpos ^ ((r >> 1) & 7);
             const uint32_t n = uint32_t(min(un0 + r, p.N - 1));
             if (TILE) w_row[i] = (n >> p.log2_br) * uint32_t(p.strip_bytes) + ((n & uint32_t(p.br_mask)) << (p.log2_bc + 1));
             else w_row[i] = n * uint32_t(p.K) * 2u;
@@ -394,44 +412,47 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
         }
     };
     set_rows(m0, n0);
-    // load q (0..15) of step s: q < 8 the A rows 8 q .., q >= 8 the W rows
-    // 8 (q - 8) .. of this wave's 64-row share
+    // load q (0 .. NLOAD - 1) of step s: q < 8 the A rows 8 q .. of this
+    // wave's 64-row share, q >= 8 the W rows 8 (q - 8) .. of its WROWS-row share
     auto issue_one = [&](int s, int q) {
-        uint8_t* buf = smem + (s & 1) * STAGE + wave * 8192;
+        uint8_t* buf = smem + (s & 1) * STAGE;
         const int k0 = (kt0 + s) * BK;
-        if (q < 8) load_lds16(Ab + size_t(k0) * 2, a_off[q], buf + q * 1024);
-        else load_lds16(p.W + w_koff(k0), w_row[q - 8], buf + HALF + (q - 8) * 1024);
+        if (q < 8) load_lds16(Ab + size_t(k0) * 2, a_off[q], buf + wave * 8192 + q * 1024);
+        else load_lds16(p.W + w_koff(k0), w_row[q - 8], buf + HALF + wave * (WROWS * 128) + (q - 8) * 1024);
     };
     // fragments: lane reads row lane % 32 of its 32-row tile at K chunk
     // 2 * sub-step + lane / 32; offsets of sub-step 0 (a sub-step adds 2
     // chunks, XORed into the position)
-    int fa_row[4], fb_row[4];
-    int fa_sw[4], fb_sw[4];
+    int fa_row[4], fb_row[NJ];
+    int fa_sw[4], fb_sw[NJ];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int ra = wm * 128 + i * 32 + (lane & 31);
         fa_row[i] = ra * 128;
         fa_sw[i] = (ra >> 1) & 7;
-        const int rb = wn * 128 + i * 32 + (lane & 31);
-        fb_row[i] = HALF + rb * 128;
-        fb_sw[i] = (rb >> 1) & 7;
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int rb = wn * (32 * NJ) + j * 32 + (lane & 31);
+        fb_row[j] = HALF + rb * 128;
+        fb_sw[j] = (rb >> 1) & 7;
     }
     const int khalf = lane >> 5;
-    // fragment q (0..7) of sub-step ss of step s: q < 4 W tile q, else A tile
-    // q - 4 (the next sub-step's first MFMAs take A tile 0 with every W tile,
-    // so the W tiles are read first)
-    auto fread_one = [&](int s, int ss, int q, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
+    // fragment q (0 .. NREAD - 1) of sub-step ss of step s: q < NJ W tile q,
+    // else A tile q - NJ (the next sub-step's first MFMAs take A tile 0 with
+    // every W tile, so the W tiles are read first)
+    auto fread_one = [&](int s, int ss, int q, bf16x8 (&fa)[4], bf16x8 (&fb)[NJ]) {
         const uint8_t* buf = smem + (s & 1) * STAGE;
         const int c = 2 * ss + khalf;
-        if (q < 4) fb[q] = *reinterpret_cast<const bf16x8*>(buf + fb_row[q] + ((c ^ fb_sw[q]) << 4));
-        else fa[q - 4] = *reinterpret_cast<const bf16x8*>(buf + fa_row[q - 4] + ((c ^ fa_sw[q - 4]) << 4));
+        if (q < NJ) fb[q] = *reinterpret_cast<const bf16x8*>(buf + fb_row[q] + ((c ^ fb_sw[q]) << 4));
+        else fa[q - NJ] = *reinterpret_cast<const bf16x8*>(buf + fa_row[q - NJ] + ((c ^ fa_sw[q - NJ]) << 4));
     };
-    f32x16 acc[4][4];
+    f32x16 acc[4][NJ];
     auto zero_acc = [&]() {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
     };
@@ -442,22 +463,39 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
     };
-    bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
-    // one sub-step: 16 MFMAs on (fa, fb); after MFMA q, fragment q / 2 of
-    // sub-step rss of step rs into (ga, gb) when q is even (READ) and load
-    // q / 2 + lq0 of step ls when q is odd (LOAD).  READ and LOAD are
-    // compile-time, so the loop holds no branch between its MFMAs.
-    auto substep = [&](auto read_c, auto load_c, const bf16x8 (&fa)[4], const bf16x8 (&fb)[4], int rs, int rss,
-                       bf16x8 (&ga)[4], bf16x8 (&gb)[4], int ls, int lq0) {
+    bf16x8 fa0[4], fb0[NJ], fa1[4], fb1[NJ];
+    // one sub-step: 4 NJ MFMAs on (fa, fb); after MFMA q, fragment q / 2 of
+    // sub-step rss of step rs into (ga, gb) when q is even (READ, the first
+    // NREAD) and load q / 2 + lq0 of step ls when q is odd (LOAD: the eight
+    // A loads from lq0 = 0 or the NWL W loads from lq0 = 8).  READ, LOAD and
+    // lq0 are compile-time at every call, so the loop holds no branch
+    // between its MFMAs.
+    auto substep = [&](auto read_c, auto load_c, const bf16x8 (&fa)[4], const bf16x8 (&fb)[NJ], int rs, int rss,
+                       bf16x8 (&ga)[4], bf16x8 (&gb)[NJ], int ls, int lq0) {
         constexpr bool READ = decltype(read_c)::value, LOAD = decltype(load_c)::value;
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            acc[q >> 2][q & 3] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q >> 2], fb[q & 3], acc[q >> 2][q & 3], 0, 0, 0);
-            if ((q & 1) == 0) {
-                if constexpr (READ) fread_one(rs, rss, q >> 1, ga, gb);
+        for (int q = 0; q < 4 * NJ; ++q) {
+            if (q % NJ < 4) {
+                acc[q / NJ][q % NJ] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[q / NJ], fb[q % NJ], acc[q / NJ][q % NJ], 0, 0, 0);
             } else {
-                if constexpr (LOAD) issue_one(ls, lq0 + (q >> 1));
+                // the fifth column of tiles keeps its sums in VGPRs (the
+                // first four fill the 256 AGPRs; the compiler does not split
+                // the accumulators between the two files by itself).  Its
+                // previous MFMA on the same sums is 4 NJ - 1 MFMAs back, far
+                // beyond any dependency wait.
+                asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0"
+                             : "+v"(acc[q / NJ][4])
+                             : "v"(fa[q / NJ]), "v"(fb[4]));
+            }
+            if ((q & 1) == 0) {
+                if constexpr (READ) {
+                    if ((q >> 1) < NREAD) fread_one(rs, rss, q >> 1, ga, gb);
+                }
+            } else {
+                if constexpr (LOAD) {
+                    if ((q >> 1) < (lq0 == 0 ? 8 : NWL)) issue_one(ls, lq0 + (q >> 1));
+                }
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -484,13 +522,21 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     auto mfma_settle = []() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); };
     auto quad_pack = [&](int i, int j, int g) -> uint2 {
         // the four sums, read out of their AGPRs here (an asm the compiler
-        // cannot move, so the reads of one MFMA tile happen where it is used)
+        // cannot move, so the reads of one MFMA tile happen where it is used);
+        // the fifth column's sums are VGPRs already
         float f0, f1, f2, f3;
-        asm volatile("v_accvgpr_read_b32 %0, %4\n\tv_accvgpr_read_b32 %1, %5\n\t"
-                     "v_accvgpr_read_b32 %2, %6\n\tv_accvgpr_read_b32 %3, %7"
-                     : "=v"(f0), "=v"(f1), "=v"(f2), "=v"(f3)
-                     : "a"(acc[i][j][4 * g + 0]), "a"(acc[i][j][4 * g + 1]), "a"(acc[i][j][4 * g + 2]),
-                       "a"(acc[i][j][4 * g + 3]));
+        if (j < 4) {
+            asm volatile("v_accvgpr_read_b32 %0, %4\n\tv_accvgpr_read_b32 %1, %5\n\t"
+                         "v_accvgpr_read_b32 %2, %6\n\tv_accvgpr_read_b32 %3, %7"
+                         : "=v"(f0), "=v"(f1), "=v"(f2), "=v"(f3)
+                         : "a"(acc[i][j][4 * g + 0]), "a"(acc[i][j][4 * g + 1]), "a"(acc[i][j][4 * g + 2]),
+                           "a"(acc[i][j][4 * g + 3]));
+        } else {
+            f0 = acc[i][j][4 * g + 0];
+            f1 = acc[i][j][4 * g + 1];
+            f2 = acc[i][j][4 * g + 2];
+            f3 = acc[i][j][4 * g + 3];
+        }
         const uint32_t h0 = f32_to_bf16_rne(f0), h1 = f32_to_bf16_rne(f1);
         const uint32_t h2 = f32_to_bf16_rne(f2), h3 = f32_to_bf16_rne(f3);
         // swap with lane ^ 1: even lanes keep rows 0-1, odd lanes rows 2-3
@@ -509,14 +555,14 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
 
     // first step of the first unit in flight
 #pragma unroll
-    for (int q = 0; q < 16; ++q) issue_one(0, q);
+    for (int q = 0; q < NLOAD; ++q) issue_one(0, q);
     for (;;) {
         // step 0 loaded and visible, its first fragments read, the first
         // half of step 1's loads in flight
         TL_WAIT_VMCNT(0);
         lds_barrier();
 #pragma unroll
-        for (int q = 0; q < 8; ++q) fread_one(0, 0, q, fa0, fb0);
+        for (int q = 0; q < NREAD; ++q) fread_one(0, 0, q, fa0, fb0);
         if (KT > 1)
 #pragma unroll
             for (int q = 0; q < 8; ++q) issue_one(1, q);
@@ -562,7 +608,7 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
         substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
         substep(N, N, fa1, fb1, 0, 0, fa0, fb0, 0, 0);
 
-        if (p.fetch && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)HALF);
+        if (p.fetch && t == 0) atomicAdd(p.fetch, (unsigned long long)KT * (unsigned long long)WHALF);
 
         if constexpr (PERSIST) {
             // whole tiles only (the launcher's condition; a uniform test, so
@@ -570,11 +616,11 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             mfma_settle();
             if (m0 + BM <= p.M && n0 + BN <= p.N) {
                 uint16_t* Cw = static_cast<uint16_t*>(p.C) + int64_t(m0 + wm * 128 + 4 * (lane >> 5) + qrow) * p.ldc +
-                               (n0 + wn * 128 + cquad);
+                               (n0 + wn * (32 * NJ) + cquad);
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
+                    for (int j = 0; j < NJ; ++j) {
 #pragma unroll
                         for (int g = 0; g < 4; ++g)
                             *reinterpret_cast<uint2*>(Cw + int64_t(i * 32 + 8 * g) * p.ldc + j * 32) = quad_pack(i, j, g);
@@ -584,7 +630,7 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
                     }
             }
             // every accumulator is read before it is cleared (else the two
-            // sets of 256 overlap and spill)
+            // sets of sums overlap and spill)
             __builtin_amdgcn_sched_barrier(0);
             zero_acc();
             if (nv >= T) {
@@ -728,6 +774,19 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
     p.w_bytes = n_cols * kp * 2;
     const int64_t n_tiles = (n_cols + tile_n - 1) / tile_n;
     const int grid = int(p.m_tiles * n_tiles);
+    // 256x320: the four-wave kernel with five MFMA tiles per wave along N
+    // (persistent, bf16 out, whole tiles -- the planner's conditions)
+    if (tile_m == 256 && tile_n == 320) {
+        if (!(q.persist && p.out_bf16 && q.M % 256 == 0 && n_cols % 320 == 0 && q.K % 128 == 0))
+            return hipErrorInvalidValue;
+        p.units = grid;
+        const int pgrid = grid < kPersistGrid ? grid : kPersistGrid;
+        if (tile)
+            hipLaunchKernelGGL((prefill_w4_kernel<true, true, true, 5>), dim3(pgrid), dim3(256), 0, stream, p);
+        else
+            hipLaunchKernelGGL((prefill_w4_kernel<false, true, true, 5>), dim3(pgrid), dim3(256), 0, stream, p);
+        return hipGetLastError();
+    }
     // 256x256: 8 waves (2 per SIMD) of 128x64; smaller tiles: 4 waves in 2 x 2
     if (tile_m == 256 && tile_n == 256) {
         if (q.K % 64 == 0 && p.log2_fetch == 0) {

@@ -426,6 +426,45 @@ def test_prefill_persistent_exact():
     assert np.array_equal(C1, oracle.round_bf16(oracle.gemm_f64(A, W)))
 
 
+# 256 x 320 tiles (each wave 128 x 160 of C, the fifth 32-column tile's sums
+# in VGPRs): M, N, K, memory tile (G, block_rows) or None for a row-major
+# weight.  512 tiles (two per workgroup), 256 tiles (one each, 16 K steps),
+# 64- and 16-row memory tiles, and [N][K] row-major.
+TILES_320 = [(1024, 40960, 512, (4096, 32)), (2048, 10240, 1024, (4096, 32)), (1024, 40960, 256, (8192, 64)),
+             (1024, 40960, 256, (2048, 16)), (1024, 40960, 512, None)]
+
+
+@pytest.mark.parametrize("M,N,K,mt", TILES_320)
+def test_prefill_tiles_256x320(M, N, K, mt):
+    G, br = mt if mt else (4096, 32)
+    kind = tl.TL_LAYOUT_TILE if mt else tl.TL_LAYOUT_NK_ROW
+    d = tl.layout(kind=kind, G=G, block_rows=br, out_dtype=tl.TL_OUT_BF16)
+    fetch = tl.TL_FETCH_BLOCK if mt else tl.TL_FETCH_NATIVE     # (block fetch on [N][K]: the emulation)
+    plan = tl.tl_gemm_plan(M, N, K, d, fetch)
+    banner(f"prefill 256x320 M={M} N={N} K={K} mt={mt} plan={plan}")
+    assert plan["tile_n"] == 320 and plan["workgroups"] == 256 and plan["split_k"] == 1
+    A = synth.normal_bf16((M, K), seed=140 + K // 256)
+    W = synth.normal_bf16((N, K), seed=141 + br, sigma=synth.W_SIGMA)
+    C = run_gemm(A, W, d, fetch=fetch, tile_major=mt is not None)
+    parity_bf16_out(host_bits(C), oracle.gemm_f64(A, W), f"256x320 M={M} N={N} K={K} mt={mt}")
+
+
+def test_prefill_tiles_256x320_exact():
+    """Small integers: the bf16 output equals the oracle's exact result
+    rounded to bf16 bit for bit (all five column tiles of every wave), and two
+    calls are identical."""
+    M, N, K = 1024, 40960, 512
+    banner("prefill 256x320 exact")
+    A = synth.small_int_bf16((M, K), seed=142)
+    W = synth.small_int_bf16((N, K), seed=143)
+    d = tl.layout(out_dtype=tl.TL_OUT_BF16)
+    assert tl.tl_gemm_plan(M, N, K, d)["tile_n"] == 320
+    C1 = host_bits(run_gemm(A, W, d))
+    C2 = host_bits(run_gemm(A, W, d))
+    assert np.array_equal(C1, C2)
+    assert np.array_equal(C1, oracle.round_bf16(oracle.gemm_f64(A, W)))
+
+
 def test_prefill_exact_inputs():
     M, N, K = 256, 256, 1024
     banner("prefill one-hot / small-int")
@@ -529,7 +568,7 @@ def test_llama_prefill_full_size_bands(i, name, N, K):
     offers and its own plan (the one bench.py times): a band of full rows and
     a band of full columns against the fp64 oracle, bf16 output.  The bands
     meet every workgroup's output tile of every plan (asserted), including
-    both launches of QKV's column split."""
+    the 256 x 320 tiles of QKV's plan."""
     banner(f"llama prefill full {name}")
     import torch
     W_bits = synth.normal_bf16((N, K), seed=synth.llama_weight_seed(i), sigma=synth.W_SIGMA)
@@ -544,8 +583,7 @@ def test_llama_prefill_full_size_bands(i, name, N, K):
     want_rows = oracle.gemm_f64(A_bits[rows], W_bits)            # [32, N]
     want_cols = oracle.gemm_f64(A_bits, W_bits[cols])            # [M, 128]
     d_rows, d_cols = torch.from_numpy(rows).cuda(), torch.from_numpy(cols).cuda()
-    # (0, 0): the library's plan (QKV: 256 x 256 tiles on columns [0, 8192),
-    # 256 x 256 tiles with K split 4 ways on the rest)
+    # (0, 0): the library's plan (QKV: 256 x 320 tiles, one round)
     for tm, tn in ((128, 128), (256, 128), (256, 256), (0, 0)):
         d = tl.layout(tile_m=tm, tile_n=tn, out_dtype=tl.TL_OUT_BF16)
         plan = tl.tl_gemm_plan(M, N, K, d)
@@ -554,7 +592,7 @@ def test_llama_prefill_full_size_bands(i, name, N, K):
         # past a column split -- holds row-band elements: the band has rows
         # in every 128-row block and all N columns
         assert len(np.unique(rows // 128)) == M // 128 and len(np.unique(rows // ptm)) == -(-M // ptm)
-        assert ptn % 128 == 0
+        assert ptn % 64 == 0
         banner(f"llama prefill full {name} tile {tm}x{tn} plan={plan}")
         C = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
         tl.tl_gemm(A, Wt, C, M, N, K, d, tl.TL_FETCH_BLOCK)

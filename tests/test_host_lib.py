@@ -231,8 +231,13 @@ def test_prefill_plan_column_split():
     fill the CUs (fp32 partials: split_k and workspace_bytes report them),
     else 128 x 128 tiles when those fit in one round."""
     bf = tl.layout(out_dtype=tl.TL_OUT_BF16)
-    qkv = tl.tl_gemm_plan(2048, 10240, 8192, bf)                                   # QKV
-    assert qkv["workgroups"] == 256 + 64 * 4
+    # QKV, bf16 out: 256 x 320 tiles fill one round exactly (256 tiles)
+    qkv = tl.tl_gemm_plan(2048, 10240, 8192, bf)
+    assert (qkv["tile_n"], qkv["workgroups"], qkv["split_k"], qkv["workspace_bytes"]) == (320, 256, 1, 0)
+    # QKV, fp32 out (no 256 x 320 tiles): 256 x 256 on 8192 columns, the
+    # rest with K split 4 ways
+    qkv = tl.tl_gemm_plan(2048, 10240, 8192, tl.layout())
+    assert qkv["tile_n"] == 256 and qkv["workgroups"] == 256 + 64 * 4
     assert qkv["split_k"] == 4 and qkv["workspace_bytes"] == 4 * 2048 * 2048 * 4
     o = tl.tl_gemm_plan(2048, 8192, 8192, bf)                                      # O: no split
     assert o["workgroups"] == 256 and o["split_k"] == 1 and o["workspace_bytes"] == 0
@@ -241,11 +246,16 @@ def test_prefill_plan_column_split():
     # fp32 output, or a ragged M: one workgroup per tile
     assert tl.tl_gemm_plan(2048, 57344, 8192, tl.layout())["workgroups"] == 1792
     assert tl.tl_gemm_plan(2000, 57344, 8192, bf)["workgroups"] == 1792
-    q4 = tl.tl_gemm_plan(4096, 10240, 8192, bf)
-    assert q4["workgroups"] == 256 + 128 * 2 and q4["split_k"] == 2          # 512 main tiles: persistent
+    q4 = tl.tl_gemm_plan(4096, 10240, 8192, bf)                                    # 512 tiles of 256 x 320
+    assert q4["tile_n"] == 320 and q4["workgroups"] == 256 and q4["split_k"] == 1
+    q4 = tl.tl_gemm_plan(4096, 10240, 8192, tl.layout())
+    assert q4["workgroups"] == 512 + 128 * 2 and q4["split_k"] == 2
     # K too short for the split (8 K steps per split at least): 128 x 128 rest
-    short = tl.tl_gemm_plan(2048, 10240, 1024, bf)
+    short = tl.tl_gemm_plan(2048, 10240, 1024, tl.layout())
     assert short["workgroups"] == 256 + 256 and short["split_k"] == 1
+    # a memory tile of 128 rows does not divide 320: 256 x 256 and the split
+    tall128 = tl.tl_gemm_plan(2048, 10240, 8192, tl.layout(G=16384, block_rows=128, out_dtype=tl.TL_OUT_BF16))
+    assert tall128["tile_n"] == 256 and tall128["split_k"] == 4
     # pinned tiles are never split: the 320 tiles go to a persistent grid
     # (fp32 output: one workgroup per tile)
     pinned = tl.layout(tile_m=256, tile_n=256, out_dtype=tl.TL_OUT_BF16)
