@@ -87,10 +87,12 @@ int main() {
             if (tl_gemm_plan(M, N, 4096, &kn, TL_FETCH_NATIVE, &p) != TL_OK) ++bad;
     if (tl_gemm_plan(8, 8192, 4096, &kn, TL_FETCH_BLOCK, &p) != TL_OK) ++bad;
     if (tl_gemm_plan(8, 520, 4096, &kn, TL_FETCH_BLOCK, &p) != TL_EUNSUPPORTED) ++bad;
+    if (tl_gemm_plan(2048, 10240, 8192, &d, TL_FETCH_BLOCK, &p) != TL_OK || p.split_k != 4 ||
+        p.workspace_bytes != int64_t(4) * 2048 * 2048 * 4)
+        ++bad;
     tl_layout_desc bf = d;
     bf.out_dtype = TL_OUT_BF16;
-    if (tl_gemm_plan(2048, 10240, 8192, &bf, TL_FETCH_BLOCK, &p) != TL_OK || p.split_k != 4 ||
-        p.workspace_bytes != int64_t(4) * 2048 * 2048 * 4)
+    if (tl_gemm_plan(2048, 10240, 8192, &bf, TL_FETCH_BLOCK, &p) != TL_OK || p.tile_n != 320 || p.workgroups != 256)
         ++bad;
     tl_layout_desc big = d;
     big.split_k = 16;
