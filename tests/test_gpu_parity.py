@@ -465,6 +465,27 @@ def test_prefill_tiles_256x320_exact():
     assert np.array_equal(C1, oracle.round_bf16(oracle.gemm_f64(A, W)))
 
 
+@pytest.mark.parametrize("M,N,K,out", [(1024, 32768, 512, tl.TL_OUT_BF16), (1024, 40960, 512, tl.TL_OUT_BF16),
+                                        (2048, 10240, 2048, tl.TL_OUT_F32), (512, 1024, 1024, tl.TL_OUT_BF16)])
+def test_prefill_issued_weight_bytes_equal_read_amp(M, N, K, out):
+    """Construction check for the prefill kernels on a tile-major weight
+    (persistent 256 x 256, 256 x 320, the K-split remainder, 128 x 128): the
+    TL_FETCH_COUNT tally of the weight loads issued equals tl_read_amp's
+    fetched bytes for the plan's tile and the oracle's count -- every m-tile
+    loads the weight once, whole memory tiles."""
+    d = tl.layout(out_dtype=out)
+    p = tl.tl_gemm_plan(M, N, K, d, tl.TL_FETCH_BLOCK)
+    banner(f"prefill fetch tally M={M} N={N} K={K} plan={p}")
+    A = synth.normal_bf16((M, K), seed=150)
+    W = synth.normal_bf16((N, K), seed=151, sigma=synth.W_SIGMA)
+    tl.tl_fetch_counter_read()   # reset
+    run_gemm(A, W, d, fetch=tl.TL_FETCH_BLOCK | tl.TL_FETCH_COUNT)
+    got = tl.tl_fetch_counter_read()
+    amp = tl.tl_read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], d, 4096)
+    want = oracle.read_amp(M, N, K, p["tile_m"], p["tile_n"], p["tile_k"], oracle.TILE, 4096, block_rows=32)
+    assert got == amp["fetched_bytes"] == want["fetched_bytes"] == -(-M // p["tile_m"]) * N * K * 2, (got, amp, want)
+
+
 def test_prefill_exact_inputs():
     M, N, K = 256, 256, 1024
     banner("prefill one-hot / small-int")
