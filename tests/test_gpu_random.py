@@ -84,6 +84,43 @@ def test_random_gemm_cases(decode):
     assert ran >= (40 if decode else 12) * SCALE, (ran, skipped)
 
 
+def draw_whole_tiles(rng):
+    """Prefill shapes of whole 256-row tiles and an even number of 64-wide K
+    steps, bf16 out (mostly): the persistent four-wave kernel -- more tiles
+    than CUs (several per workgroup), 256 x 320 tiles that fill whole rounds,
+    or fewer tiles than CUs -- on random memory tiles or a row-major weight."""
+    mt = int(rng.choice([4, 8]))                  # M = 1024 or 2048: 256-row tiles
+    kind_n = int(rng.integers(0, 3))
+    if kind_n == 0:      # 256 x 256, more tiles than CUs
+        N = 256 * int(rng.integers(256 // mt + 1, 384 // mt + 1))
+    elif kind_n == 1:    # 256 x 320 filling one or two rounds
+        N = 320 * 256 * int(rng.integers(1, 3)) // mt
+    else:                # fewer tiles than CUs
+        N = 256 * int(rng.integers(1, 256 // mt))
+    K = 128 * int(rng.integers(1, 5))
+    if rng.random() < 0.75:
+        G = int(rng.choice([1024, 2048, 4096, 8192]))
+        br = int(rng.choice([b for b in (8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
+        kind, fetch = tl.TL_LAYOUT_TILE, tl.TL_FETCH_BLOCK
+    else:
+        G, br, kind, fetch = 4096, 32, tl.TL_LAYOUT_NK_ROW, tl.TL_FETCH_NATIVE
+    out = tl.TL_OUT_BF16 if rng.random() < 0.85 else tl.TL_OUT_F32
+    pin = 256 if rng.random() < 0.2 else 0
+    d = tl.layout(kind=kind, G=G, block_rows=br, out_dtype=out, tile_m=pin, tile_n=pin)
+    return 256 * mt, N, K, d, fetch
+
+
+@pytest.mark.parametrize("case", range(8 * SCALE))
+def test_random_whole_tile_prefill_cases(case):
+    rng = np.random.default_rng(4000 + case)
+    M, N, K, d, fetch = draw_whole_tiles(rng)
+    p = tl.tl_gemm_plan(M, N, K, d, fetch)
+    banner(f"random whole-tile prefill case {case}: M={M} N={N} K={K} G={d.G} br={d.block_rows} "
+           f"kind={d.kind} out={d.out_dtype} plan={p}")
+    assert p["kernel"] == 2 and p["tile_m"] == 256
+    run_case(M, N, K, d, fetch, seed=9000 + case)
+
+
 @pytest.mark.parametrize("case", range(6 * SCALE))
 def test_random_lds_staged_cases(case):
     """17 <= M <= 32 on weights whose 32-row tiles fill the CUs in whole rounds
