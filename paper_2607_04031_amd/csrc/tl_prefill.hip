@@ -64,6 +64,15 @@ __device__ inline uint16_t f32_to_bf16_rne(float f) {
     return uint16_t((u & 0x7fffffffu) > 0x7f800000u ? quiet : rounded);
 }
 
+// two fp32 -> packed bf16 (lo in bits 0-15), round to nearest even: gfx950's
+// v_cvt_pk_bf16_f32, one instruction where the bit arithmetic above takes
+// about seven per value
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ inline uint32_t bf16x2_rne(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+
 // LDS byte offset of 16-byte chunk 'chunk' (0..7) of 128-byte row 'row'.
 // gfx950 serves a 16-byte-per-lane LDS read 16 lanes at a time across 64
 // four-byte banks (256 B): rows r and r + 1 fall in different halves, so the
@@ -511,10 +520,16 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     const int qd = lane & 3;
     const int qrow = ((qd & 1) << 1) | ((qd & 2) >> 1);
     const int cquad = (lane & 31) & ~3;
-    // lane-select masks (all ones on odd lanes / on lanes 2 and 3 of a quad):
-    // the swaps below pick with masks, so the unrolled code has no branches
-    const uint32_t odd = 0u - uint32_t(qd & 1), hi2 = 0u - uint32_t((qd >> 1) & 1);
-    auto pick = [](uint32_t mask, uint32_t a, uint32_t b) { return b ^ ((a ^ b) & mask); };   // mask ? a : b
+    // lane selects (odd lanes / lanes 2 and 3 of a quad): per-lane
+    // conditions fixed for the kernel, so each pick below is one v_cndmask
+    // on a lane mask and the unrolled code has no branches
+    const bool odd = (qd & 1) != 0, hi2 = (qd & 2) != 0;
+    auto pick = [](bool c, uint32_t a, uint32_t b) { return c ? a : b; };
+    // v_perm_b32 byte selectors (bytes 0-3: the kept pair, 4-7: the received
+    // one) that merge the first swap's halves into two rows of two columns:
+    // an even lane's own column comes first, an odd lane's second
+    const uint32_t sel_first = (qd & 1) ? 0x01000504u : 0x05040100u;
+    const uint32_t sel_second = (qd & 1) ? 0x03020706u : 0x07060302u;
     // before the first quad_pack after the MFMAs: 24 wait states, more than
     // any MFMA-result read hazard needs (the reads below are inline assembly,
     // which the compiler's hazard check does not see into; the other tiles'
@@ -537,16 +552,17 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             f2 = acc[i][j][4 * g + 2];
             f3 = acc[i][j][4 * g + 3];
         }
-        const uint32_t h0 = f32_to_bf16_rne(f0), h1 = f32_to_bf16_rne(f1);
-        const uint32_t h2 = f32_to_bf16_rne(f2), h3 = f32_to_bf16_rne(f3);
-        // swap with lane ^ 1: even lanes keep rows 0-1, odd lanes rows 2-3
-        const uint32_t send1 = pick(odd, h0 | (h1 << 16), h2 | (h3 << 16));
-        const uint32_t recv1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send1), 0xB1, 0xf, 0xf, false));
-        const uint32_t x_first = pick(odd, (recv1 & 0xffffu) | (h2 << 16), h0 | (recv1 << 16));
-        const uint32_t x_second = pick(odd, (recv1 >> 16) | (h3 << 16), h1 | (recv1 & 0xffff0000u));
+        const uint32_t h01 = bf16x2_rne(f0, f1), h23 = bf16x2_rne(f2, f3);
+        // swap with lane ^ 1: even lanes keep rows 0-1, odd lanes rows 2-3;
+        // x_first / x_second: rows 0 and 1 (even) or 2 and 3 (odd) of the
+        // two columns
+        const uint32_t send1 = pick(odd, h01, h23), keep1 = pick(odd, h23, h01);
+        const uint32_t recv1 = uint32_t(__builtin_amdgcn_mov_dpp(int(send1), 0xB1, 0xf, 0xf, true));
+        const uint32_t x_first = __builtin_amdgcn_perm(recv1, keep1, sel_first);
+        const uint32_t x_second = __builtin_amdgcn_perm(recv1, keep1, sel_second);
         // swap with lane ^ 2: one row's four columns per lane
         const uint32_t send2 = pick(hi2, x_first, x_second);
-        const uint32_t recv2 = uint32_t(__builtin_amdgcn_update_dpp(0, int(send2), 0x4E, 0xf, 0xf, false));
+        const uint32_t recv2 = uint32_t(__builtin_amdgcn_mov_dpp(int(send2), 0x4E, 0xf, 0xf, true));
         uint2 r;
         r.x = pick(hi2, recv2, x_first);
         r.y = pick(hi2, x_second, recv2);

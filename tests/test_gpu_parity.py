@@ -410,12 +410,34 @@ def test_prefill_persistent_grid(M, N, K, pin):
     parity_bf16_out(host_bits(run_gemm(A, W, d)), oracle.gemm_f64(A, W), f"persistent M={M} N={N}")
 
 
-def test_prefill_persistent_exact():
+# The persistent grid at more K steps (10 and 18) with several units per
+# workgroup: M, N, K, pinned tile, row-major [N][K] weight.  Four units per
+# workgroup; 384 units (half the workgroups take two); a row-major weight.
+PERSIST_DEEP_CASES = [(2048, 32768, 640, 0, False), (768, 32768, 1152, 256, False), (1024, 32768, 640, 0, True)]
+
+
+@pytest.mark.parametrize("M,N,K,pin,row_major", PERSIST_DEEP_CASES)
+def test_prefill_persistent_deeper_k(M, N, K, pin, row_major):
+    kind = tl.TL_LAYOUT_NK_ROW if row_major else tl.TL_LAYOUT_TILE
+    fetch = tl.TL_FETCH_NATIVE if row_major else tl.TL_FETCH_BLOCK
+    d = tl.layout(kind=kind, tile_m=pin, tile_n=pin, out_dtype=tl.TL_OUT_BF16)
+    plan = tl.tl_gemm_plan(M, N, K, d, fetch)
+    banner(f"prefill persistent M={M} N={N} K={K} row_major={row_major} plan={plan}")
+    assert (plan["tile_m"], plan["tile_n"], plan["workgroups"], plan["split_k"]) == (256, 256, 256, 1)
+    assert (M // 256) * (N // 256) > 256
+    A = synth.normal_bf16((M, K), seed=160 + K // 128)
+    W = synth.normal_bf16((N, K), seed=161, sigma=synth.W_SIGMA)
+    C = run_gemm(A, W, d, fetch=fetch, tile_major=not row_major)
+    parity_bf16_out(host_bits(C), oracle.gemm_f64(A, W), f"persistent M={M} N={N} K={K}")
+
+
+@pytest.mark.parametrize("K", [512, 640])
+def test_prefill_persistent_exact(K):
     """Small-integer inputs through the persistent grid: every fp32 sum is
     exact, so the bf16 output equals the oracle's exact result rounded to
     bf16 (nearest even) bit for bit, and two calls are identical."""
-    M, N, K = 1024, 32768, 512
-    banner("prefill persistent exact")
+    M, N = 1024, 32768
+    banner(f"prefill persistent exact K={K}")
     A = synth.small_int_bf16((M, K), seed=132)
     W = synth.small_int_bf16((N, K), seed=133)
     d = tl.layout(out_dtype=tl.TL_OUT_BF16)
@@ -463,6 +485,34 @@ def test_prefill_tiles_256x320_exact():
     C2 = host_bits(run_gemm(A, W, d))
     assert np.array_equal(C1, C2)
     assert np.array_equal(C1, oracle.round_bf16(oracle.gemm_f64(A, W)))
+
+
+# The bf16 epilogues round on the GPU (the persistent 256 x 256 and 256 x 320
+# grids and the LDS-staged 256 x 256 epilogue with the hardware's packed
+# conversion).  A consistency property on top of the oracle parity: the bf16
+# output equals, bit for bit, the round-to-nearest-even (the oracle's
+# round_bf16) of the fp32 output of a plan whose per-element sums run in the
+# same order (256 x 256 tiles, no K split).  M, N, K, the bf16 plan's pinned
+# tile (0: the library's) and the kernel it takes.
+BF16_OF_F32_CASES = [(1024, 32768, 512, 0, "persistent 256x256"), (1024, 40960, 512, 0, "persistent 256x320"),
+                     (300, 1024, 256, 256, "LDS epilogue, ragged M")]
+
+
+@pytest.mark.parametrize("M,N,K,pin,what", BF16_OF_F32_CASES)
+def test_prefill_bf16_out_rounds_the_fp32_sums(M, N, K, pin, what):
+    d16 = tl.layout(tile_m=pin, tile_n=pin, out_dtype=tl.TL_OUT_BF16)
+    d32 = tl.layout(tile_m=256, tile_n=256, out_dtype=tl.TL_OUT_F32)
+    p16, p32 = tl.tl_gemm_plan(M, N, K, d16), tl.tl_gemm_plan(M, N, K, d32)
+    banner(f"prefill bf16 = rne(fp32) M={M} N={N} K={K} ({what}) bf16 plan={p16} fp32 plan={p32}")
+    assert p16["tile_m"] == 256 and p16["split_k"] == 1 and p32["split_k"] == 1
+    assert p16["tile_n"] == (320 if "320" in what else 256)
+    assert p16["workgroups"] == (256 if "persistent" in what else -(-M // 256) * (N // 256))
+    A = synth.normal_bf16((M, K), seed=150 + M % 7)
+    W = synth.normal_bf16((N, K), seed=151, sigma=synth.W_SIGMA)
+    C16 = host_bits(run_gemm(A, W, d16))
+    C32 = host_f32(run_gemm(A, W, d32))
+    assert np.array_equal(C16, oracle.round_bf16(C32.astype(np.float64))), what
+    parity_bf16_out(C16, oracle.gemm_f64(A, W), what)
 
 
 @pytest.mark.parametrize("M,N,K,out", [(1024, 32768, 512, tl.TL_OUT_BF16), (1024, 40960, 512, tl.TL_OUT_BF16),

@@ -85,10 +85,11 @@ def test_random_gemm_cases(decode):
 
 
 def draw_whole_tiles(rng):
-    """Prefill shapes of whole 256-row tiles and an even number of 64-wide K
-    steps, bf16 out (mostly): the persistent four-wave kernel -- more tiles
-    than CUs (several per workgroup), 256 x 320 tiles that fill whole rounds,
-    or fewer tiles than CUs -- on random memory tiles or a row-major weight."""
+    """Prefill shapes of whole 256-row tiles and an even number (2 to 16) of
+    64-wide K steps, bf16 out (mostly): the persistent four-wave kernel --
+    more tiles than CUs (several per workgroup), 256 x 320 tiles that fill
+    whole rounds, or fewer tiles than CUs -- on random memory tiles or a
+    row-major weight."""
     mt = int(rng.choice([4, 8]))                  # M = 1024 or 2048: 256-row tiles
     kind_n = int(rng.integers(0, 3))
     if kind_n == 0:      # 256 x 256, more tiles than CUs
@@ -97,7 +98,7 @@ def draw_whole_tiles(rng):
         N = 320 * 256 * int(rng.integers(1, 3)) // mt
     else:                # fewer tiles than CUs
         N = 256 * int(rng.integers(1, 256 // mt))
-    K = 128 * int(rng.integers(1, 5))
+    K = 128 * int(rng.integers(1, 9))
     if rng.random() < 0.75:
         G = int(rng.choice([1024, 2048, 4096, 8192]))
         br = int(rng.choice([b for b in (8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
