@@ -329,7 +329,8 @@ __device__ inline void load_lds16(const uint8_t* base, uint32_t voff, uint8_t* l
 
 // PERSIST (bf16 output, no K split, whole 256 x 256 tiles, an even number of
 // K steps): a grid of at most one workgroup per CU walks p.units tiles.  The
-// next tile's first K step is loaded during this tile's last two steps, and
+// next tile's first K step (with three weight stages, also its second step's
+// weight tile) is loaded during this tile's last two steps, and
 // this tile's C is stored straight from registers (bf16, quad-transposed: 8
 // bytes of one row per lane), so no workgroup ends and starts between tiles
 // and the next tile's first loads are not waited for.  (With one tile per
@@ -347,13 +348,17 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     constexpr int BM = 256, BN = 64 * NJ, BK = 64;
     constexpr int HALF = BM * BK * 2;            // A tile of a step: 32 KB
     constexpr int WHALF = BN * BK * 2;           // W tile of a step: 32 or 40 KB
-    constexpr int STAGE = HALF + WHALF;
+    // LDS: two A stages, then WST weight stages -- three for 256 x 256 tiles
+    // (step s + 2's weight tile loads during step s, so its latency has two
+    // steps to hide in), two for 256 x 320 (the LDS budget)
+    constexpr int WST = NJ == 4 ? 3 : 2;
+    constexpr int LDS_OPS = 2 * HALF + WST * WHALF;
     constexpr int WROWS = BN / 4;                // W rows each wave loads per step
     constexpr int NWL = WROWS / 8;               // ... in loads of 8 rows: 8 or 10
     constexpr int NLOAD = 8 + NWL;               // loads per step and wave
     constexpr int NREAD = 4 + NJ;                // fragment reads per sub-step
     constexpr int C_STAGE = BM * 576;            // bf16 epilogue: the C tile with 576-byte rows
-    constexpr int LDS_BYTES = (OUT_BF16 && !PERSIST && C_STAGE > 2 * STAGE) ? C_STAGE : 2 * STAGE;
+    constexpr int LDS_BYTES = (OUT_BF16 && !PERSIST && C_STAGE > LDS_OPS) ? C_STAGE : LDS_OPS;
     static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
 
@@ -402,7 +407,7 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     // per-lane load offsets, fixed over the K loop: the A row and chunk; the
     // weight row and Eq. 1's offset of the chunk (the step's share is a
     // uniform base, so a load needs no vector arithmetic)
-    auto set_rows = [&](int um0, int un0) {
+    auto set_a_rows = [&](int um0) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int r = 64 * wave + 8 * i + lrow;
@@ -410,6 +415,8 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             const uint32_t m = uint32_t(min(um0 + r, p.M - 1));
             a_off[i] = (m * uint32_t(p.K) + uint32_t(c * 8)) * 2u;
         }
+    };
+    auto set_w_rows = [&](int un0) {
 #pragma unroll
         for (int i = 0; i < NWL; ++i) {
             const int r = WROWS * wave + 8 * i + lrow;
@@ -420,14 +427,23 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             w_row[i] += w_koff(c * 8);
         }
     };
-    set_rows(m0, n0);
+    set_a_rows(m0);
+    set_w_rows(n0);
+    // step s's A stage is s mod 2 and its weight stage (g + s) mod WST, g
+    // the K steps of the workgroup's earlier units (a multiple of KT, even
+    // in a persistent grid, so the A stages alternate across units too);
+    // g_ld is the g of the weight loads in flight, which run ahead into the
+    // next unit during a unit's last two steps
+    int g_rd = 0, g_ld = 0;
+    auto w_stage = [&](int g, int s) -> uint8_t* {
+        return smem + 2 * HALF + (WST == 3 ? (g + s) % 3 : (s & 1)) * WHALF;
+    };
     // load q (0 .. NLOAD - 1) of step s: q < 8 the A rows 8 q .. of this
     // wave's 64-row share, q >= 8 the W rows 8 (q - 8) .. of its WROWS-row share
     auto issue_one = [&](int s, int q) {
-        uint8_t* buf = smem + (s & 1) * STAGE;
         const int k0 = (kt0 + s) * BK;
-        if (q < 8) load_lds16(Ab + size_t(k0) * 2, a_off[q], buf + wave * 8192 + q * 1024);
-        else load_lds16(p.W + w_koff(k0), w_row[q - 8], buf + HALF + wave * (WROWS * 128) + (q - 8) * 1024);
+        if (q < 8) load_lds16(Ab + size_t(k0) * 2, a_off[q], smem + (s & 1) * HALF + wave * 8192 + q * 1024);
+        else load_lds16(p.W + w_koff(k0), w_row[q - 8], w_stage(g_ld, s) + wave * (WROWS * 128) + (q - 8) * 1024);
     };
     // fragments: lane reads row lane % 32 of its 32-row tile at K chunk
     // 2 * sub-step + lane / 32; offsets of sub-step 0 (a sub-step adds 2
@@ -443,7 +459,7 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int rb = wn * (32 * NJ) + j * 32 + (lane & 31);
-        fb_row[j] = HALF + rb * 128;
+        fb_row[j] = rb * 128;
         fb_sw[j] = (rb >> 1) & 7;
     }
     const int khalf = lane >> 5;
@@ -451,10 +467,9 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
     // else A tile q - NJ (the next sub-step's first MFMAs take A tile 0 with
     // every W tile, so the W tiles are read first)
     auto fread_one = [&](int s, int ss, int q, bf16x8 (&fa)[4], bf16x8 (&fb)[NJ]) {
-        const uint8_t* buf = smem + (s & 1) * STAGE;
         const int c = 2 * ss + khalf;
-        if (q < NJ) fb[q] = *reinterpret_cast<const bf16x8*>(buf + fb_row[q] + ((c ^ fb_sw[q]) << 4));
-        else fa[q - NJ] = *reinterpret_cast<const bf16x8*>(buf + fa_row[q - NJ] + ((c ^ fa_sw[q - NJ]) << 4));
+        if (q < NJ) fb[q] = *reinterpret_cast<const bf16x8*>(w_stage(g_rd, s) + fb_row[q] + ((c ^ fb_sw[q]) << 4));
+        else fa[q - NJ] = *reinterpret_cast<const bf16x8*>(smem + (s & 1) * HALF + fa_row[q - NJ] + ((c ^ fa_sw[q - NJ]) << 4));
     };
     f32x16 acc[4][NJ];
     auto zero_acc = [&]() {
@@ -569,13 +584,19 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
         return r;
     };
 
-    // first step of the first unit in flight
+    // first step of the first unit in flight (three weight stages: step 1's
+    // weight tile too)
 #pragma unroll
     for (int q = 0; q < NLOAD; ++q) issue_one(0, q);
+    if (WST == 3 && KT > 1)
+#pragma unroll
+        for (int q = 8; q < NLOAD; ++q) issue_one(1, q);
     for (;;) {
-        // step 0 loaded and visible, its first fragments read, the first
-        // half of step 1's loads in flight
-        TL_WAIT_VMCNT(0);
+        // step 0 loaded and visible (three weight stages: step 1's weight
+        // tile, issued after it, may stay in flight), its first fragments
+        // read, the A half of step 1 in flight
+        if (WST == 3 && KT > 1) TL_WAIT_VMCNT(NWL);
+        else TL_WAIT_VMCNT(0);
         lds_barrier();
 #pragma unroll
         for (int q = 0; q < NREAD; ++q) fread_one(0, 0, q, fa0, fb0);
@@ -584,10 +605,15 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
             for (int q = 0; q < 8; ++q) issue_one(1, q);
         int s = 0;
         for (; s + 2 < KT; ++s) {            // steady state: every load present
-            substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);   // rest of step s + 1's loads
+            // the weight tile of step s + WST - 1 (two stages: the rest of
+            // step s + 1; three: step s + 2, into the stage step s - 1 read)
+            substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + WST - 1, 8);
             substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
             substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
-            TL_WAIT_VMCNT(0);                // step s + 1 landed
+            // step s + 1 landed (three stages: step s + 2's weight tile,
+            // issued last, stays in flight)
+            if constexpr (WST == 3) TL_WAIT_VMCNT(NWL);
+            else TL_WAIT_VMCNT(0);
             lds_barrier();
             // first fragments of step s + 1, first half of step s + 2's loads
             // (into the stage step s has finished reading)
@@ -597,28 +623,44 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
         // loads nothing reads) and its tile origin
         int nv = v, nm0 = m0, nn0 = n0;
         if (s + 1 < KT) {                    // step KT - 2: no step KT to load
-            substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);
-            substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
-            substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
-            TL_WAIT_VMCNT(0);
-            lds_barrier();
             if constexpr (PERSIST) {
-                // the next unit's first step goes into the stage step KT - 2
-                // has just finished reading (stage 0: KT is even) -- its A
-                // half now, its W half during the last step -- so it lands
-                // under this tile's last MFMAs
                 nv = v + int(gridDim.x);
                 int ns;
                 if (nv < T) unit_of(nv, nm0, nn0, ns);
-                set_rows(nm0, nn0);
+            }
+            if constexpr (PERSIST && WST == 3) {
+                // the next unit's step 0 weight tile, into the stage step
+                // KT - 3 read (g_ld: the next unit's g)
+                set_w_rows(nn0);
+                g_ld = g_rd + KT;
+                substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, 0, 8);
+            } else if constexpr (WST == 3) {
+                substep(Y, N, fa0, fb0, s, 1, fa1, fb1, 0, 0);   // step KT - 1's weight is in flight already
+            } else {
+                substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, s + 1, 8);
+            }
+            substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
+            substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
+            if constexpr (PERSIST && WST == 3) TL_WAIT_VMCNT(NWL);
+            else TL_WAIT_VMCNT(0);
+            lds_barrier();
+            if constexpr (PERSIST) {
+                // the next unit's step 0 A tile goes into the stage step
+                // KT - 2 has just finished reading (stage 0: KT is even),
+                // and (two weight stages) its weight tile during the last
+                // step, so they land under this tile's last MFMAs
+                set_a_rows(nm0);
+                if constexpr (WST == 2) set_w_rows(nn0);
                 substep(Y, Y, fa1, fb1, s + 1, 0, fa0, fb0, 0, 0);
             } else {
                 substep(Y, N, fa1, fb1, s + 1, 0, fa0, fb0, 0, 0);
             }
             ++s;
         }
-        // the last step
-        if constexpr (PERSIST) substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, 0, 8);
+        // the last step (PERSIST: the next unit's weight tile of step 1 with
+        // three stages, of step 0 with two; a persistent unit has at least
+        // two K steps, so step KT - 2 above ran)
+        if constexpr (PERSIST) substep(Y, Y, fa0, fb0, s, 1, fa1, fb1, WST == 3 ? 1 : 0, 8);
         else substep(Y, N, fa0, fb0, s, 1, fa1, fb1, 0, 0);
         substep(Y, N, fa1, fb1, s, 2, fa0, fb0, 0, 0);
         substep(Y, N, fa0, fb0, s, 3, fa1, fb1, 0, 0);
@@ -653,6 +695,8 @@ __global__ __launch_bounds__(256) void prefill_w4_kernel(PrefillParams p) {
                 TL_WAIT_VMCNT(0);        // the reloads land before the workgroup's LDS is released
                 break;
             }
+            g_rd += KT;
+            g_ld = g_rd;
             v = nv;
             m0 = nm0;
             n0 = nn0;
