@@ -309,6 +309,10 @@ PREFILL_SHAPES = [
     (300, 768, 1024, 256, 256),
     (65, 256, 512, 128, 128),                                  # just above the decode limit
     (512, 1056, 512, 256, 128), (512, 1056, 512, 256, 256),    # ragged N tail (N % 128 = 32)
+    # 256 x 256 tiles (the four-wave kernel with three weight stages) at 1, 3
+    # and 5 K steps: one step (no second weight tile to prefetch) and odd
+    # counts, outside the persistent grid
+    (300, 768, 64, 256, 256), (512, 1024, 192, 256, 256), (300, 768, 320, 256, 256),
 ]
 
 
