@@ -34,7 +34,12 @@ def draw(rng, decode):
     br = int(rng.choice([b for b in (4, 8, 16, 32, 64) if G // (2 * b) >= 8]))
     M = int(rng.integers(1, 65)) if decode else int(rng.integers(65, 1500))
     N = int(rng.integers(1, 3000))
-    K = 8 * int(rng.integers(1, 600))
+    # prefill: half the draws take K % 64 = 0, which the four-wave 256 x 256
+    # kernel needs (1 to 75 K steps)
+    if not decode and rng.random() < 0.5:
+        K = 64 * int(rng.integers(1, 76))
+    else:
+        K = 8 * int(rng.integers(1, 600))
     kind = tl.TL_LAYOUT_TILE if rng.random() < 0.8 else tl.TL_LAYOUT_NK_ROW
     fetch = tl.TL_FETCH_BLOCK if rng.random() < 0.7 else tl.TL_FETCH_NATIVE
     out = tl.TL_OUT_BF16 if rng.random() < 0.3 else tl.TL_OUT_F32
@@ -109,6 +114,34 @@ def draw_whole_tiles(rng):
     pin = 256 if rng.random() < 0.2 else 0
     d = tl.layout(kind=kind, G=G, block_rows=br, out_dtype=out, tile_m=pin, tile_n=pin)
     return 256 * mt, N, K, d, fetch
+
+
+def draw_w4_ragged(rng):
+    """Ragged prefill shapes pinned to 256 x 256 tiles with K % 64 = 0: the
+    four-wave kernel outside the persistent grid (partial tiles clamp their
+    loads and guard their stores) at 1 to 40 K steps, on random memory
+    tiles or a row-major weight, both output types."""
+    M, N, K = int(rng.integers(65, 1500)), int(rng.integers(1, 3000)), 64 * int(rng.integers(1, 41))
+    if rng.random() < 0.75:
+        G = int(rng.choice([1024, 2048, 4096, 8192]))
+        br = int(rng.choice([b for b in (8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
+        kind, fetch = tl.TL_LAYOUT_TILE, tl.TL_FETCH_BLOCK
+    else:
+        G, br, kind, fetch = 4096, 32, tl.TL_LAYOUT_NK_ROW, tl.TL_FETCH_NATIVE
+    out = tl.TL_OUT_BF16 if rng.random() < 0.5 else tl.TL_OUT_F32
+    d = tl.layout(kind=kind, G=G, block_rows=br, out_dtype=out, tile_m=256, tile_n=256)
+    return M, N, K, d, fetch
+
+
+@pytest.mark.parametrize("case", range(10 * SCALE))
+def test_random_w4_ragged_prefill_cases(case):
+    rng = np.random.default_rng(5000 + case)
+    M, N, K, d, fetch = draw_w4_ragged(rng)
+    p = tl.tl_gemm_plan(M, N, K, d, fetch)
+    banner(f"random ragged 256x256 prefill case {case}: M={M} N={N} K={K} G={d.G} br={d.block_rows} "
+           f"kind={d.kind} out={d.out_dtype} plan={p}")
+    assert p["kernel"] == 2 and (p["tile_m"], p["tile_n"], p["split_k"]) == (256, 256, 1)
+    run_case(M, N, K, d, fetch, seed=11000 + case)
 
 
 @pytest.mark.parametrize("case", range(8 * SCALE))
