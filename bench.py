@@ -746,8 +746,10 @@ def granularity_sweep(ctx, W=None):
     rows = []
     tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
     settle(ctx, lambda: tl.tl_gemm(A32, Wt, C32, 32, N, K, tl.layout(G=4096, block_rows=32), tl.TL_FETCH_BLOCK))
+    # block_rows 4 to 64: at 4 KB, memory tiles 512 down to 32 elements wide
+    # (the paper's tile-shape sensitivity sweeps 512 down to 64)
     for Gs in (512, 1024, 4096, 16384):
-        for br in (8, 16, 32, 64):
+        for br in (4, 8, 16, 32, 64):
             d = tl.layout(G=Gs, block_rows=br)
             dp = tl.layout(G=Gs, block_rows=br, out_dtype=tl.TL_OUT_BF16)
             row = {"G": Gs, "block_rows": br, "block_cols": Gs // (2 * br),

@@ -36,9 +36,10 @@ REPACK_SMALL = [
     # rows, cols, elem_bytes, G, block_rows
     (1024, 1024, 2, 4096, 32),       # tiny config
     (256, 2048, 2, 512, 8), (256, 2048, 2, 512, 16), (256, 2048, 2, 512, 32), (256, 2048, 2, 512, 64),
-    (256, 2048, 2, 1024, 8), (256, 2048, 2, 1024, 64),
-    (256, 2048, 2, 4096, 8), (256, 2048, 2, 4096, 16), (256, 2048, 2, 4096, 64),
+    (256, 2048, 2, 1024, 8), (256, 2048, 2, 1024, 16), (256, 2048, 2, 1024, 32), (256, 2048, 2, 1024, 64),
+    (256, 2048, 2, 4096, 8), (256, 2048, 2, 4096, 16), (256, 2048, 2, 4096, 32), (256, 2048, 2, 4096, 64),
     (256, 2048, 2, 16384, 8), (256, 2048, 2, 16384, 16), (256, 2048, 2, 16384, 32), (256, 2048, 2, 16384, 64),
+    (256, 2048, 2, 512, 4), (256, 2048, 2, 1024, 4), (256, 2048, 2, 4096, 4), (256, 2048, 2, 16384, 4),   # 4-row tiles
     (192, 768, 1, 4096, 64),         # FP8-sized elements, 64 x 64 memory tile
     (64, 4096, 4, 4096, 8),
     (32, 64, 2, 4096, 32),           # a single memory tile
@@ -228,7 +229,7 @@ def test_decode_bf16_output(M):
 
 
 @pytest.mark.parametrize("G", [512, 1024, 4096, 16384])
-@pytest.mark.parametrize("br", [8, 16, 32, 64])
+@pytest.mark.parametrize("br", [4, 8, 16, 32, 64])
 def test_decode_memory_tile_shapes(G, br):
     """One library binary for every memory-tile shape (runtime descriptor)."""
     M, N, K = 8, 256, 4096
@@ -554,7 +555,7 @@ def test_prefill_exact_inputs():
                               oracle.gemm_f64(A, W))
 
 
-@pytest.mark.parametrize("G,br", [(4096, 8), (16384, 32), (1024, 16), (512, 32)])
+@pytest.mark.parametrize("G,br", [(4096, 8), (16384, 32), (1024, 16), (512, 32), (4096, 4), (16384, 4)])
 def test_prefill_memory_tile_shapes(G, br):
     M, N, K = 256, 256, 2048
     banner(f"prefill G={G} br={br}")

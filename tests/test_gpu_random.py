@@ -106,7 +106,7 @@ def draw_whole_tiles(rng):
     K = 128 * int(rng.integers(1, 9))
     if rng.random() < 0.75:
         G = int(rng.choice([1024, 2048, 4096, 8192]))
-        br = int(rng.choice([b for b in (8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
+        br = int(rng.choice([b for b in (4, 8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
         kind, fetch = tl.TL_LAYOUT_TILE, tl.TL_FETCH_BLOCK
     else:
         G, br, kind, fetch = 4096, 32, tl.TL_LAYOUT_NK_ROW, tl.TL_FETCH_NATIVE
@@ -124,7 +124,7 @@ def draw_w4_ragged(rng):
     M, N, K = int(rng.integers(65, 1500)), int(rng.integers(1, 3000)), 64 * int(rng.integers(1, 41))
     if rng.random() < 0.75:
         G = int(rng.choice([1024, 2048, 4096, 8192]))
-        br = int(rng.choice([b for b in (8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
+        br = int(rng.choice([b for b in (4, 8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
         kind, fetch = tl.TL_LAYOUT_TILE, tl.TL_FETCH_BLOCK
     else:
         G, br, kind, fetch = 4096, 32, tl.TL_LAYOUT_NK_ROW, tl.TL_FETCH_NATIVE

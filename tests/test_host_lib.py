@@ -78,7 +78,7 @@ def test_read_amp_matches_oracle_random_shapes():
 
 
 @pytest.mark.parametrize("G", [512, 1024, 4096, 16384])
-@pytest.mark.parametrize("br", [8, 16, 32, 64])
+@pytest.mark.parametrize("br", [4, 8, 16, 32, 64])
 def test_read_amp_granularity_sweep_slice_matches_oracle(G, br):
     """Down-projection [8192, 28672] (256-row slice), tiles 64..256: the
     library's closed forms equal the oracle's enumeration exactly."""
