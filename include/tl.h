@@ -210,12 +210,13 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * on tile-major weights whose 32-row tiles and 512-column K chunks fill the
  * CUs in whole rounds, a variant that stages the activations in LDS and
  * shares them across several tiles); larger M runs the prefill kernels (bf16
- * MFMA tiles 256x256x64, 256x128x64 or 128x128x64, MFMA-bound; with bf16
- * output, whole 256x256 tiles and K % 128 == 0 a persistent grid of at most
- * 256 workgroups walks the tiles; when 256x256 tiles would leave the last
- * round of workgroups part-empty, the columns past the whole rounds take
- * 256x256 tiles with K split across workgroups, or 128x128 tiles; see
- * tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
+ * MFMA tiles 256x256x64, 256x320x64, 256x128x64 or 128x128x64, MFMA-bound;
+ * with bf16 output, whole 256x256 tiles and K % 128 == 0 a persistent grid of
+ * at most 256 workgroups walks the tiles, and 256x320 tiles replace them
+ * where those fill the CUs in whole rounds and 256x256 tiles do not; when
+ * 256x256 tiles would leave the last round of workgroups part-empty, the
+ * columns past the whole rounds take 256x256 tiles with K split across
+ * workgroups, or 128x128 tiles; see tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
  * byte per element, e.g. 64 x 64 memory tiles of 4 KB, Section 3.1): decode
  * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
  * per-channel scales).
