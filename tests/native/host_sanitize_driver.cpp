@@ -2,7 +2,7 @@
 // calls the library's pure-host entry points -- planning, the exact
 // read-amplification count, the view address generator, Eq. 6 and argument
 // validation -- in a build with AddressSanitizer and UndefinedBehaviorSanitizer.
-// The kernel launchers live in the .hip sources, which this build leaves out;
+// The kernel launchers live in the .hip sources, which the sanitizer build leaves out;
 // the stubs below stand in for them and abort if anything reaches them.
 #include <cstdio>
 #include <cstdlib>
