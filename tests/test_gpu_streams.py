@@ -133,3 +133,54 @@ def test_graph_replay_after_workspace_growth():
         del g
     parity(host_f32(eager_small), oracle.gemm_f64(As, Ws), "captured call")
     parity(host_f32(eager_big), oracle.gemm_f64(Ab, Wb), "growing call")
+
+
+def test_prefill_ksplit_on_separate_streams():
+    """The prefill plan whose columns past the whole rounds split K (fp32
+    partials in the calling stream's workspace, then the split-order reduce):
+    three host threads, each on its own stream, run it repeatedly at the same
+    time; every result equals the call made alone bit for bit (fp32 and bf16
+    out), and that result meets the oracle."""
+    import torch
+    M, N, K = 2000, 12288, 1024
+    banner("prefill K-split plan from 3 host threads on 3 streams")
+    A = synth.normal_bf16((M, K), seed=700)
+    W = synth.normal_bf16((N, K), seed=701, sigma=synth.W_SIGMA)
+    Ad = dev_bf16(A)
+    Wd = dev_bf16(W)
+    Wt = torch.empty_like(Wd)
+    tl.tl_repack(Wd, Wt, N, K, 2, 4096, 32)
+    y_ref = oracle.gemm_f64(A, W)
+    for out, dt in ((tl.TL_OUT_F32, torch.float32), (tl.TL_OUT_BF16, torch.bfloat16)):
+        d = tl.layout(out_dtype=out)
+        plan = tl.tl_gemm_plan(M, N, K, d)
+        assert plan["split_k"] == 2 and plan["workspace_bytes"] > 0, plan
+        alone = torch.empty((M, N), dtype=dt, device="cuda")
+        tl.tl_gemm(Ad, Wt, alone, M, N, K, d, tl.TL_FETCH_BLOCK)
+        torch.cuda.synchronize()
+        alone = alone.view(torch.int16 if out == tl.TL_OUT_BF16 else torch.int32).cpu().numpy()
+        if out == tl.TL_OUT_F32:
+            parity(alone.view(np.float32), y_ref, "K-split plan alone")
+        outs = [None] * 3
+        errors = []
+
+        def worker(i):
+            try:
+                s = torch.cuda.Stream()
+                C = torch.full((M, N), float("nan"), dtype=dt, device="cuda")
+                with torch.cuda.stream(s):
+                    for _ in range(5):
+                        tl.tl_gemm(Ad, Wt, C, M, N, K, d, tl.TL_FETCH_BLOCK, stream=s)
+                s.synchronize()
+                outs[i] = C.view(torch.int16 if out == tl.TL_OUT_BF16 else torch.int32).cpu().numpy()
+            except Exception as e:                      # reported on the main thread
+                errors.append(e)
+
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(3)]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join()
+        assert not errors, errors
+        for i in range(3):
+            assert np.array_equal(outs[i], alone), (out, i)
