@@ -710,18 +710,22 @@ def test_graph_replay_matches_eager():
     import torch
     banner("graph capture / replay")
     side = torch.cuda.Stream()
-    # the last two take the LDS-staged decode kernel (split-K 4 with its reduce, and unsplit)
-    cases = [(8, 1024, 2048, 1), (8, 1024, 2048, 4), (32, 512, 4096, 3), (256, 512, 1024, 0),
-             (32, 8192, 16384, 0), (24, 32768, 2048, 0)]
+    # M, N, K, split_k, bf16 out: decode (split or not); the LDS-staged decode
+    # kernel (split-K 4 with its reduce, and unsplit); prefill through 128 x 128
+    # tiles, the persistent 256 x 256 and 256 x 320 grids, and the plan whose
+    # remaining columns split K (main launch, partials and reduce)
+    cases = [(8, 1024, 2048, 1, False), (8, 1024, 2048, 4, False), (32, 512, 4096, 3, False),
+             (256, 512, 1024, 0, False), (32, 8192, 16384, 0, False), (24, 32768, 2048, 0, False),
+             (1024, 32768, 512, 0, True), (1024, 40960, 512, 0, True), (2000, 12288, 1024, 0, False)]
     with torch.cuda.stream(side):
         tensors = []
-        for i, (M, N, K, S) in enumerate(cases):
+        for i, (M, N, K, S, bf16) in enumerate(cases):
             A = dev_bf16(synth.normal_bf16((M, K), seed=40 + i))
             W = dev_bf16(synth.normal_bf16((N, K), seed=50 + i, sigma=synth.W_SIGMA))
             Wt = torch.empty_like(W)
             tl.tl_repack(W, Wt, N, K, 2, 4096, 32)
-            C = torch.zeros((M, N), dtype=torch.float32, device="cuda")
-            d = tl.layout(split_k=S)
+            C = torch.zeros((M, N), dtype=torch.bfloat16 if bf16 else torch.float32, device="cuda")
+            d = tl.layout(split_k=S, out_dtype=tl.TL_OUT_BF16 if bf16 else tl.TL_OUT_F32)
             tl.tl_gemm(A, Wt, C, M, N, K, d, tl.TL_FETCH_BLOCK)       # eager; creates the workspace
             tensors.append((A, Wt, C, d, M, N, K))
         side.synchronize()
