@@ -428,6 +428,39 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                 return TL_OK;
             }
         }
+        // Medium M (no tile requested): when 256 x 256 tiles are fewer than
+        // the CUs, the same tiles with K split S ways over all the columns
+        // (S = CUs / tiles, up to 8, each split >= 8 of the 64-wide K steps;
+        // fp32 partials, at most 256 tiles x 64 K elements x S <= 64 MiB, summed
+        // in split order by the reduce kernel); when they fill at least half
+        // the CUs, 256 x 256 tiles rather than 128 x 128.  Llama-70B-shaped
+        // layer, bf16 out, on one box: M = 256 851 -> 495 us, 512 1133 -> 786,
+        // 768 1638 -> 1140, 1024 1571 -> 1409 (down at M = 1024: 535 -> 388).
+        if (!d->tile_m && !d->tile_n && M >= 256 && K % 64 == 0 && N % 256 == 0 && !p.block_row &&
+            (!tile || 256 % p.L.br == 0)) {
+            const int64_t t256 = ((M + 255) / 256) * (N / 256);
+            if (t256 < kCUs) {
+                const int64_t S = std::min<int64_t>({kCUs / t256, 8, K / 64 / 8});
+                if (S >= 2) {
+                    p.n_main = 0;                // no main launch: every column splits K
+                    p.split_rest = int(S);
+                    p.persist = false;
+                    p.pub.tile_m = 256;
+                    p.pub.tile_n = 256;
+                    p.pub.tile_k = int(p.k_unit);
+                    p.pub.split_k = int(S);
+                    p.pub.waves = 4;
+                    p.pub.workgroups = t256 * S;
+                    p.pub.workspace_bytes = S * M * N * 4;
+                    *P = p;
+                    return TL_OK;
+                }
+            }
+            if (tm == 128 && 2 * t256 >= kCUs) {
+                tm = 256;
+                tn = 256;
+            }
+        }
         // Quantisation: 256 x 256 tiles that leave the last round of
         // workgroups part-empty (QKV at M = 2048: 320 tiles on 256 CUs) cover
         // the widest column range whose tile count is a multiple of the CU

@@ -878,7 +878,8 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
 }  // namespace
 
 hipError_t launch_prefill(const PrefillLaunch& q, hipStream_t stream) {
-    hipError_t e = launch_range(q, 0, q.n_main, q.tile_m, q.tile_n, stream);
+    // (n_main == 0: every column takes the K-split launch below)
+    hipError_t e = q.n_main > 0 ? launch_range(q, 0, q.n_main, q.tile_m, q.tile_n, stream) : hipSuccess;
     if (e != hipSuccess || q.n_main == q.N) return e;
     if (q.split_rest <= 1) return launch_range(q, q.n_main, q.N - q.n_main, 128, 128, stream);
     // the remaining columns: 256 x 256 tiles of prefill_w4_kernel, K split

@@ -415,6 +415,41 @@ def test_prefill_persistent_grid(M, N, K, pin):
     parity_bf16_out(host_bits(run_gemm(A, W, d)), oracle.gemm_f64(A, W), f"persistent M={M} N={N}")
 
 
+# Medium M, no tile requested: fewer 256 x 256 tiles than CUs, so the plan
+# splits K over all the columns (S = CUs / tiles, at most 8, each split >= 8
+# K steps; fp32 partials, then the split-order reduce).  M, N, K, row-major
+# [N][K] weight: ragged M with S = 8, S = 4, and a row-major weight with S = 2.
+KSPLIT_ALL = [(300, 2048, 4096, False), (512, 4096, 2048, False), (256, 1024, 1024, True)]
+
+
+@pytest.mark.parametrize("M,N,K,row_major", KSPLIT_ALL)
+def test_prefill_ksplit_all_columns(M, N, K, row_major):
+    kind = tl.TL_LAYOUT_NK_ROW if row_major else tl.TL_LAYOUT_TILE
+    fetch = tl.TL_FETCH_NATIVE if row_major else tl.TL_FETCH_BLOCK
+    d = tl.layout(kind=kind)
+    plan = tl.tl_gemm_plan(M, N, K, d, fetch)
+    banner(f"prefill K split over all columns M={M} N={N} K={K} row_major={row_major} plan={plan}")
+    t256 = -(-M // 256) * (N // 256)
+    S = min(256 // t256, 8, K // 512)
+    assert S >= 2 and (plan["tile_m"], plan["tile_n"], plan["split_k"]) == (256, 256, S)
+    assert plan["workgroups"] == t256 * S and plan["workspace_bytes"] == S * M * N * 4
+    A = synth.normal_bf16((M, K), seed=170 + S)
+    W = synth.normal_bf16((N, K), seed=171, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    C1 = host_f32(run_gemm(A, W, d, fetch=fetch, tile_major=not row_major))
+    C2 = host_f32(run_gemm(A, W, d, fetch=fetch, tile_major=not row_major))
+    parity(C1, y_ref, f"K split all S={S} f32")
+    assert np.array_equal(C1, C2)                      # fixed-order reduce: bitwise reproducible
+    db = tl.layout(kind=kind, out_dtype=tl.TL_OUT_BF16)
+    assert tl.tl_gemm_plan(M, N, K, db, fetch)["split_k"] == S
+    parity_bf16_out(host_bits(run_gemm(A, W, db, fetch=fetch, tile_major=not row_major)), y_ref,
+                    f"K split all S={S} bf16")
+    Ai = synth.small_int_bf16((M, K), seed=172)
+    Wi = synth.small_int_bf16((N, K), seed=173)
+    assert np.array_equal(host_f32(run_gemm(Ai, Wi, d, fetch=fetch, tile_major=not row_major)).astype(np.float64),
+                          oracle.gemm_f64(Ai, Wi))
+
+
 # The persistent grid at more K steps (10 and 18) with several units per
 # workgroup: M, N, K, pinned tile, row-major [N][K] weight.  Four units per
 # workgroup; 384 units (half the workgroups take two); a row-major weight.
@@ -521,10 +556,12 @@ def test_prefill_bf16_out_rounds_the_fp32_sums(M, N, K, pin, what):
 
 
 @pytest.mark.parametrize("M,N,K,out", [(1024, 32768, 512, tl.TL_OUT_BF16), (1024, 40960, 512, tl.TL_OUT_BF16),
-                                        (2048, 10240, 2048, tl.TL_OUT_F32), (512, 1024, 1024, tl.TL_OUT_BF16)])
+                                        (2048, 10240, 2048, tl.TL_OUT_F32), (512, 1024, 1024, tl.TL_OUT_BF16),
+                                        (512, 1024, 512, tl.TL_OUT_BF16)])
 def test_prefill_issued_weight_bytes_equal_read_amp(M, N, K, out):
     """Construction check for the prefill kernels on a tile-major weight
-    (persistent 256 x 256, 256 x 320, the K-split remainder, 128 x 128): the
+    (persistent 256 x 256, 256 x 320, the K-split remainder, K split over all
+    columns, 128 x 128): the
     TL_FETCH_COUNT tally of the weight loads issued equals tl_read_amp's
     fetched bytes for the plan's tile and the oracle's count -- every m-tile
     loads the weight once, whole memory tiles."""

@@ -144,6 +144,35 @@ def test_random_w4_ragged_prefill_cases(case):
     run_case(M, N, K, d, fetch, seed=11000 + case)
 
 
+def draw_medium_m(rng):
+    """Medium-M prefill with the library's plan (no tile requested): M 256 to
+    1023 (ragged), N a multiple of 256, K 1024 to 6080, so the plan takes
+    256 x 256 tiles, with K split over all the columns when they are fewer
+    than the CUs, or 128 x 128 tiles; random memory tiles or a row-major
+    weight, both output types."""
+    M, N, K = int(rng.integers(256, 1024)), 256 * int(rng.integers(1, 49)), 64 * int(rng.integers(16, 96))
+    if rng.random() < 0.75:
+        G = int(rng.choice([1024, 2048, 4096, 8192]))
+        br = int(rng.choice([b for b in (4, 8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
+        kind, fetch = tl.TL_LAYOUT_TILE, tl.TL_FETCH_BLOCK
+    else:
+        G, br, kind, fetch = 4096, 32, tl.TL_LAYOUT_NK_ROW, tl.TL_FETCH_NATIVE
+    out = tl.TL_OUT_BF16 if rng.random() < 0.5 else tl.TL_OUT_F32
+    d = tl.layout(kind=kind, G=G, block_rows=br, out_dtype=out)
+    return M, N, K, d, fetch
+
+
+@pytest.mark.parametrize("case", range(10 * SCALE))
+def test_random_medium_m_prefill_cases(case):
+    rng = np.random.default_rng(6000 + case)
+    M, N, K, d, fetch = draw_medium_m(rng)
+    p = tl.tl_gemm_plan(M, N, K, d, fetch)
+    banner(f"random medium-M prefill case {case}: M={M} N={N} K={K} G={d.G} br={d.block_rows} "
+           f"kind={d.kind} out={d.out_dtype} plan={p}")
+    assert p["kernel"] == 2
+    run_case(M, N, K, d, fetch, seed=13000 + case)
+
+
 @pytest.mark.parametrize("case", range(8 * SCALE))
 def test_random_whole_tile_prefill_cases(case):
     rng = np.random.default_rng(4000 + case)

@@ -5,7 +5,8 @@ equal tl_gemm's results on the same inputs bit for bit -- same plan, same
 kernels, same fixed-order reduce -- and the fp64 oracle within the gate.
 Covered plans: the streaming decode kernel with K splits, the LDS-staged
 decode kernel with K splits, an FP8 weight with K splits, prefill without
-scratch, and prefill whose remaining columns run with a K split.  Errors: partials beyond the scratch, and the per-stream tally."""
+scratch, prefill whose columns all run with a K split (medium M), and prefill
+whose remaining columns run with a K split.  Errors: partials beyond the scratch, and the per-stream tally."""
 import numpy as np
 import pytest
 
@@ -52,7 +53,8 @@ def _both(A, Wt, M, N, K, d):
 CASES = [
     ("streaming decode, split-K", (8, 10240, 8192, 0), (5, 2048, 4096, 3)),
     ("LDS-staged decode, split-K", (32, 10240, 8192, 0), (20, 4096, 4096, 0)),
-    ("prefill (no scratch), then split-K decode", (256, 1024, 2048, 0), (3, 1024, 2048, 4)),
+    ("prefill (no scratch), then split-K decode", (256, 1024, 512, 0), (3, 1024, 2048, 4)),
+    ("prefill with K split over all columns, then split-K decode", (256, 1024, 2048, 0), (3, 1024, 2048, 4)),
     ("prefill with K-split remaining columns, then split-K decode", (2000, 10240, 2048, 0), (6, 4096, 4096, 2)),
 ]
 
@@ -69,7 +71,8 @@ def test_noalloc_matches_tl_gemm(what, first, second):
         assert np.array_equal(host_f32(C_na), host_f32(C_ref)), f"{what} {call}: differs from tl_gemm"
         parity(host_f32(C_na), oracle.gemm_f64(A_bits, W_bits), f"{what} {call}")
     # the plans the test names really use the scratch where they say so
-    assert tl.tl_gemm_plan(*first[:3], tl.layout(split_k=first[3]))["split_k"] > 1 or first[0] == 256
+    first_plan = tl.tl_gemm_plan(*first[:3], tl.layout(split_k=first[3]))
+    assert (first_plan["workspace_bytes"] == 0) == ("no scratch" in what), first_plan
 
 
 def test_noalloc_fp8_split_k_twice():
