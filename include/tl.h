@@ -217,9 +217,9 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * where those fill the CUs in whole rounds and 256x256 tiles do not; when
  * 256x256 tiles would leave the last round of workgroups part-empty, the
  * columns past the whole rounds take 256x256 tiles with K split across
- * workgroups, or 128x128 tiles; from M = 256 up, when 256x256 tiles are
- * fewer than the CUs, every column takes them with K split, up to 8 ways;
- * see tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
+ * workgroups, or 128x128 tiles; when 256x256 tiles are fewer than the CUs
+ * (and K % 64 == 0, N % 256 == 0), every column takes them with K split, up
+ * to 8 ways; see tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
  * byte per element, e.g. 64 x 64 memory tiles of 4 KB, Section 3.1): decode
  * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
  * per-channel scales).

@@ -428,15 +428,18 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                 return TL_OK;
             }
         }
-        // Medium M (no tile requested): when 256 x 256 tiles are fewer than
-        // the CUs, the same tiles with K split S ways over all the columns
-        // (S = CUs / tiles, up to 8, each split >= 8 of the 64-wide K steps;
-        // fp32 partials, at most 256 tiles x 64 K elements x S <= 64 MiB, summed
-        // in split order by the reduce kernel); when they fill at least half
-        // the CUs, 256 x 256 tiles rather than 128 x 128.  Llama-70B-shaped
-        // layer, bf16 out, on one box: M = 256 851 -> 495 us, 512 1133 -> 786,
+        // Small and medium M (no tile requested): when 256 x 256 tiles are
+        // fewer than the CUs, the same tiles with K split S ways over all the
+        // columns (S = CUs / tiles, up to 8, each split >= 8 of the 64-wide K
+        // steps; fp32 partials, at most 256 tiles x 64 K elements x S <= 64
+        // MiB, summed in split order by the reduce kernel); above M = 128,
+        // when they fill at least half the CUs, 256 x 256 tiles rather than
+        // 128 x 128 (at M <= 128 those waste half their rows: gate+up at
+        // M = 128, 224 tiles, 193 us as 128 x 128, 224 as 256 x 256).
+        // Llama-70B-shaped layer, bf16 out, on one box: M = 96 710 -> 440 us,
+        // 128 725 -> 450, 192 837 -> 467, 256 851 -> 495, 512 1133 -> 786,
         // 768 1638 -> 1140, 1024 1571 -> 1409 (down at M = 1024: 535 -> 388).
-        if (!d->tile_m && !d->tile_n && M >= 256 && K % 64 == 0 && N % 256 == 0 && !p.block_row &&
+        if (!d->tile_m && !d->tile_n && M > kDecodeMaxM && K % 64 == 0 && N % 256 == 0 && !p.block_row &&
             (!tile || 256 % p.L.br == 0)) {
             const int64_t t256 = ((M + 255) / 256) * (N / 256);
             if (t256 < kCUs) {
@@ -456,7 +459,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                     return TL_OK;
                 }
             }
-            if (tm == 128 && 2 * t256 >= kCUs) {
+            if (tm == 128 && M > 128 && 2 * t256 >= kCUs) {
                 tm = 256;
                 tn = 256;
             }

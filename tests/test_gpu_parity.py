@@ -415,11 +415,13 @@ def test_prefill_persistent_grid(M, N, K, pin):
     parity_bf16_out(host_bits(run_gemm(A, W, d)), oracle.gemm_f64(A, W), f"persistent M={M} N={N}")
 
 
-# Medium M, no tile requested: fewer 256 x 256 tiles than CUs, so the plan
-# splits K over all the columns (S = CUs / tiles, at most 8, each split >= 8
-# K steps; fp32 partials, then the split-order reduce).  M, N, K, row-major
-# [N][K] weight: ragged M with S = 8, S = 4, and a row-major weight with S = 2.
-KSPLIT_ALL = [(300, 2048, 4096, False), (512, 4096, 2048, False), (256, 1024, 1024, True)]
+# Small and medium M, no tile requested: fewer 256 x 256 tiles than CUs, so
+# the plan splits K over all the columns (S = CUs / tiles, at most 8, each
+# split >= 8 K steps; fp32 partials, then the split-order reduce).  M, N, K,
+# row-major [N][K] weight: ragged M with S = 8, S = 4, a row-major weight with
+# S = 2, and M = 96 (S = 8) and 65 (S = 4) in one 256-row tile.
+KSPLIT_ALL = [(300, 2048, 4096, False), (512, 4096, 2048, False), (256, 1024, 1024, True),
+              (96, 2048, 4096, False), (65, 1024, 2048, False)]
 
 
 @pytest.mark.parametrize("M,N,K,row_major", KSPLIT_ALL)

@@ -145,12 +145,12 @@ def test_random_w4_ragged_prefill_cases(case):
 
 
 def draw_medium_m(rng):
-    """Medium-M prefill with the library's plan (no tile requested): M 256 to
-    1023 (ragged), N a multiple of 256, K 1024 to 6080, so the plan takes
-    256 x 256 tiles, with K split over all the columns when they are fewer
-    than the CUs, or 128 x 128 tiles; random memory tiles or a row-major
-    weight, both output types."""
-    M, N, K = int(rng.integers(256, 1024)), 256 * int(rng.integers(1, 49)), 64 * int(rng.integers(16, 96))
+    """Small and medium-M prefill with the library's plan (no tile
+    requested): M 65 to 1023 (ragged), N a multiple of 256, K 1024 to 6080, so
+    the plan takes 256 x 256 tiles, with K split over all the columns when
+    they are fewer than the CUs, or 128 x 128 tiles; random memory tiles or a
+    row-major weight, both output types."""
+    M, N, K = int(rng.integers(65, 1024)), 256 * int(rng.integers(1, 49)), 64 * int(rng.integers(16, 96))
     if rng.random() < 0.75:
         G = int(rng.choice([1024, 2048, 4096, 8192]))
         br = int(rng.choice([b for b in (4, 8, 16, 32, 64) if 8 <= G // (2 * b) <= 512]))
