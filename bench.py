@@ -363,6 +363,43 @@ def prefill_layer(ctx, weights):
     return out
 
 
+def prefill_small_medium_m(ctx, weights, Ms=(128, 256, 512, 1024)):
+    """The Llama-shaped prefill layer (bf16 out, the library's plan) at smaller
+    batches, where 256 x 256 tiles are fewer than the CUs for some or all
+    shapes and the plan splits K over all their columns: per M, a settle, 2
+    untimed and 3 event-timed layers, and each shape's tile and split."""
+    tl, torch, synth = ctx.tl, ctx.torch, ctx.synth
+    pd = tl.layout(G=G, block_rows=BR, out_dtype=tl.TL_OUT_BF16)
+    res = {}
+    for M in Ms:
+        acts = [ctx.to_dev(synth.normal_bf16((M, K), seed=synth.llama_prefill_act_seed(i, M)))
+                for i, (_, N, K, _) in enumerate(weights)]
+        outs = [torch.empty((M, N), dtype=torch.bfloat16, device=ctx.dev) for (_, N, _, _) in weights]
+
+        def layer():
+            for (_, N, K, W), A, C in zip(weights, acts, outs):
+                tl.tl_gemm(A, W, C, M, N, K, pd, tl.TL_FETCH_BLOCK)
+        settle(ctx, layer)          # (the activations above leave the GPU idle)
+        for _ in range(2):
+            layer()
+        torch.cuda.synchronize()
+        ev = ctx.event_pairs(1)[0]
+        ev[0].record(ctx.stream)
+        for _ in range(3):
+            layer()
+        ev[1].record(ctx.stream)
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / 3
+        flops = sum(2.0 * M * N * K for (_, N, K, _) in weights)
+        plans = {name: tl.tl_gemm_plan(M, N, K, pd) for (name, N, K, _) in weights}
+        res[f"M{M}"] = {"layer_ms": round(ms, 3), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
+                        "plan": {name: f"{p['tile_m']}x{p['tile_n']}, split_k {p['split_k']}" for name, p in plans.items()}}
+        log(f"prefill M={M}: {res[f'M{M}']}")
+    res["workload"] = ("llama-3.1-70b-shaped prefill layer (qkv, o, gate_up, down), bf16 out, tile-major G=4096 B "
+                       "32x64 memory tiles; the library's tile plan")
+    return res
+
+
 def moe_layer(ctx, steps, warmup):
     """Qwen-3-30B-A3B-shaped layer at 64 tokens: attention q, k, v (one call
     over the stacked [q; k; v] weight) and o at M = 64 and, for every expert
@@ -1004,6 +1041,8 @@ def main():
         extras["view_load"] = view_load(ctx, weights)
         extras["lgms_emulation"] = lgms_sweep(ctx, weights)
         extras["tp_shard_decode_M8"] = tp_shard_layers(ctx, weights, args.steps, args.warmup)
+        if not args.no_prefill:
+            extras["prefill_layer_small_medium_M"] = prefill_small_medium_m(ctx, weights)
 
     # ---------------- read amplification ----------------
     plan = tl.tl_gemm_plan(DECODE_M, 8192, 8192, desc, tl.TL_FETCH_BLOCK)

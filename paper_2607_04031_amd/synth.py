@@ -91,8 +91,8 @@ def llama_decode_act_seed(i: int, M: int) -> int:
     return 20 + i + 100 * M
 
 
-def llama_prefill_act_seed(i: int) -> int:
-    return 30 + i
+def llama_prefill_act_seed(i: int, M: int = LLAMA_PREFILL_M) -> int:
+    return 30 + i if M == LLAMA_PREFILL_M else 30 + i + 100 * M
 
 
 # Qwen-3-30B-A3B-class MoE layer.
