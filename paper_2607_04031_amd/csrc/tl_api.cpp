@@ -436,9 +436,9 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         // when they fill at least half the CUs, 256 x 256 tiles rather than
         // 128 x 128 (at M <= 128 those waste half their rows: gate+up at
         // M = 128, 224 tiles, 193 us as 128 x 128, 224 as 256 x 256).
-        // Llama-70B-shaped layer, bf16 out, on one box: M = 96 710 -> 440 us,
-        // 128 725 -> 450, 192 837 -> 467, 256 851 -> 495, 512 1133 -> 786,
-        // 768 1638 -> 1140, 1024 1571 -> 1409 (down at M = 1024: 535 -> 388).
+        // Llama-70B-shaped layer, bf16 out, whole layers on one box: M = 128
+        // 730 -> 464 us, 256 851 -> 514, 512 1132 -> 779, 1024 1667 -> 1419
+        // (down alone at M = 1024: 535 -> 388).
         if (!d->tile_m && !d->tile_n && M > kDecodeMaxM && K % 64 == 0 && N % 256 == 0 && !p.block_row &&
             (!tile || 256 % p.L.br == 0)) {
             const int64_t t256 = ((M + 255) / 256) * (N / 256);
