@@ -123,7 +123,7 @@ typedef struct tl_amp {
 
 /* What tl_gemm will launch for given arguments (tl_gemm_plan). */
 typedef struct tl_plan {
-    int32_t kernel;      /* 1 = decode (skinny, M <= 64), 2 = prefill (MFMA tiles) */
+    int32_t kernel;      /* 1 = decode (skinny, M <= 64), 2 = prefill (MFMA tiles; also 33 <= M <= 64 on wide weights) */
     int32_t tile_m;      /* compute tile used by the kernel; with tile_k it is  */
     int32_t tile_n;      /* the tile to pass to tl_read_amp to account for the  */
     int32_t tile_k;      /* kernel's fetches                                     */
@@ -210,7 +210,10 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound; at 17 <= M <= 32
  * on tile-major weights whose 32-row tiles and 512-column K chunks fill the
  * CUs in whole rounds, a variant that stages the activations in LDS and
- * shares them across several tiles); larger M runs the prefill kernels (bf16
+ * shares them across several tiles) -- except that at 33 <= M <= 64 a bf16
+ * weight read natively with N >= 32768 (its 128x128 tiles fill the CUs), no
+ * tile or split requested and the prefill kernel's limits met, takes the
+ * prefill kernel's 128x128 tiles; larger M runs the prefill kernels (bf16
  * MFMA tiles 256x256x64, 256x320x64, 256x128x64 or 128x128x64, MFMA-bound;
  * with bf16 output, whole 256x256 tiles and K % 128 == 0 a persistent grid of
  * at most 256 workgroups walks the tiles, and 256x320 tiles replace them

@@ -233,6 +233,16 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
     p.k_unit = tile ? std::max<int64_t>(64, p.L.bc) : 64;
 
     if (p.fp8 && !(M <= kDecodeMaxM && d->tile_m <= 64)) return TL_EUNSUPPORTED;        // FP8: decode kernel only
+    // 33 <= M <= 64 on a wide bf16 weight (128 x 128 tiles fill the CUs at
+    // least once: N >= 32768), no tile or split requested, within the
+    // prefill kernel's limits (whole memory-tile strips per 128-row tile,
+    // weights under 4 GB): its 128 x 128 tiles stream the weight faster than
+    // the decode kernel's 64-row tiles at four 16-row M tiles, whose
+    // activation reloads from L2 match the weight bytes (Llama gate+up, bf16
+    // out, one box, M = 33 / 48 / 64: 187 / 211 / 240 -> 169 / 171 / 172 us)
+    const bool wide_mid_m = M > 32 && M <= kDecodeMaxM && !d->tile_m && !d->tile_n && !d->split_k && !p.fp8 &&
+                            !p.kn_row && !p.block_row && N / 128 >= kCUs && (!tile || 128 % p.L.br == 0) &&
+                            (tile ? packed_bytes(p.L, N, K) : N * K * 2) < (int64_t(1) << 32);
     if (p.kn_row) {
         // 64-column tiles (128-byte row segments), K split until there are
         // about 1024 workgroups with >= 1024 K per split; 8 waves when the
@@ -261,7 +271,7 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         p.pub.waves = p.waves;
         p.pub.workgroups = wgs;
         p.pub.workspace_bytes = S > 1 ? S * ((M * N + 3) / 4 * 4) * 4 : 0;
-    } else if (M <= kDecodeMaxM && d->tile_m <= 64) {
+    } else if (M <= kDecodeMaxM && d->tile_m <= 64 && !wide_mid_m) {
         p.pub.kernel = 1;
         p.m_tiles16 = int((M + 15) / 16);
         if (p.m_tiles16 == 3) p.m_tiles16 = 4;
@@ -350,10 +360,12 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         const int ns = tn / 16;
         int waves = wgs <= kCUs ? 16 : (wgs <= 2 * kCUs ? 8 : 4);
         // registers: 16 waves (4 per SIMD, <= 128 VGPRs) only fit one 16-row
-        // M tile x 32 rows of N; 8 waves (<= 256 VGPRs) fit up to 8 of those
+        // M tile x 32 rows of N; 8 waves (<= 256 VGPRs) fit up to 8 of those,
+        // and the 64-row tile at four M tiles, which keeps one K step in
+        // flight (bf16 weights read natively)
         const int mn = p.m_tiles16 * ns / 2;
         if (waves == 16 && mn > 1) waves = 8;
-        if (waves == 8 && mn > 4) waves = 4;
+        if (waves == 8 && mn > 4 && !(mn == 8 && !p.fp8 && !p.block_row)) waves = 4;
         p.waves = waves;
         // 17 <= M <= 32 on whole tile-major strips: stage the activations in
         // LDS, one 8-wave workgroup per CU taking T of the 32-row tiles and

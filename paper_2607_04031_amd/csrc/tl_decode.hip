@@ -284,7 +284,7 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeParams p) {
     }
 
     // ---- reduce the waves (an in-workgroup K split) in a fixed order ----
-    static_assert(WAVES * MT * NS <= 64, "reduction buffer exceeds 64 KB");
+    static_assert(WAVES * MT * NS <= 128, "reduction buffer exceeds 128 KB");
     __shared__ f32x4 red[kWaves][MT][NS][64];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -384,8 +384,13 @@ template <int MT, int NS, int WAVES, bool TILE, bool GROUPED, bool SWIGLU = fals
 hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
     // steps in flight per wave: fewer for larger M, and for the grouped
     // 64-row tile (4 steps there take all 256 VGPRs: one wave per SIMD; with
-    // 2 the kernel fits three -- Qwen expert down projection 66.5 -> 61.3 us)
-    constexpr int U = (MT >= 2 || (GROUPED && NS == 4 && !SWIGLU)) ? 2 : 4;
+    // 2 the kernel fits three -- Qwen expert down projection 66.5 -> 61.3 us).
+    // Four 16-row M tiles on a 64-row tile take one step: with two its ~290
+    // registers leave one wave per SIMD, with one two (Llama shapes, bf16
+    // out, one box, M = 33 / 48 / 64: QKV 66 / 70 / 77 -> 50 / 53 / 58 us;
+    // with 8 waves, O 38 / 38 / 41 -> 33 / 35 / 39, down 103 / 100 / 112 ->
+    // 91 / 100 / 111).
+    constexpr int U = (MT >= 4 && NS == 4 && !GROUPED) ? 1 : (MT >= 2 || (GROUPED && NS == 4 && !SWIGLU)) ? 2 : 4;
     if constexpr (!TILE && !GROUPED) {
         if (p.log2_fetch > 0) {   // block emulation: fewer steps in flight leave room for the block loop
             hipLaunchKernelGGL((decode_kernel<MT, NS, 2, WAVES, false, true, false>), dim3(grid), dim3(64 * WAVES), 0,
@@ -410,7 +415,7 @@ hipError_t launch_w(const DecodeParams& p, int grid, int waves, bool grouped, hi
     if constexpr (MT * NS <= 2) {
         if (waves == 16) return launch_t<MT, NS, 16, TILE, false>(p, grid, stream);
     }
-    if constexpr (MT * NS <= 8) {
+    if constexpr (MT * NS <= 16) {   // 4 x 4: one step in flight, 128 KB of LDS for the wave sums
         if (waves == 8) return launch_t<MT, NS, 8, TILE, false>(p, grid, stream);
     }
     return launch_t<MT, NS, 4, TILE, false>(p, grid, stream);

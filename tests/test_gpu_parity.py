@@ -142,6 +142,59 @@ def test_decode_in_workgroup_k_split(M, N):
     assert np.array_equal(host_f32(run_gemm(Ai, Wi, d)).astype(np.float64), oracle.gemm_f64(Ai, Wi))
 
 
+# 33 <= M <= 64 on 64-row tiles (four 16-row M tiles, one K step in flight
+# per wave): M, N, K, waves, split_k of the plan.  One 8-wave workgroup per
+# CU with split_k 2 and 1, a 320-tile grid with 8 waves, and 4-wave
+# workgroups (768 of them).
+MID_M_DECODE = [(33, 8192, 2048, 8, 2), (64, 16384, 2048, 8, 1), (48, 10240, 2048, 8, 2), (40, 24576, 2048, 4, 2)]
+
+
+@pytest.mark.parametrize("M,N,K,waves,S", MID_M_DECODE)
+def test_decode_four_m_tiles(M, N, K, waves, S):
+    d = tl.layout()
+    p = tl.tl_gemm_plan(M, N, K, d)
+    banner(f"decode four M tiles M={M} N={N} K={K} plan={p}")
+    assert (p["kernel"], p["tile_m"], p["tile_n"], p["waves"], p["split_k"]) == (1, 64, 64, waves, S)
+    A = synth.normal_bf16((M, K), seed=180 + M)
+    W = synth.normal_bf16((N, K), seed=181, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    C1 = host_f32(run_gemm(A, W, d))
+    parity(C1, y_ref, f"four M tiles M={M}")
+    assert np.array_equal(C1, host_f32(run_gemm(A, W, d)))       # fixed-order sums: bitwise reproducible
+    db = tl.layout(out_dtype=tl.TL_OUT_BF16)
+    parity_bf16_out(host_bits(run_gemm(A, W, db)), y_ref, f"four M tiles M={M} bf16")
+    Ai = synth.small_int_bf16((M, K), seed=182)
+    Wi = synth.small_int_bf16((N, K), seed=183)
+    assert np.array_equal(host_f32(run_gemm(Ai, Wi, d)).astype(np.float64), oracle.gemm_f64(Ai, Wi))
+
+
+# 33 <= M <= 64 on a wide weight (N >= 32768): the prefill kernel's 128 x 128
+# tiles.  M, N, K, row-major [N][K] weight; a ragged N (N % 128 = 96).
+MID_M_WIDE = [(33, 32768, 512, False), (48, 32768 + 96, 1024, False), (64, 40960, 512, True), (40, 57344, 256, False)]
+
+
+@pytest.mark.parametrize("M,N,K,row_major", MID_M_WIDE)
+def test_mid_m_wide_weight_on_prefill_tiles(M, N, K, row_major):
+    kind = tl.TL_LAYOUT_NK_ROW if row_major else tl.TL_LAYOUT_TILE
+    fetch = tl.TL_FETCH_NATIVE if row_major else tl.TL_FETCH_BLOCK
+    d = tl.layout(kind=kind)
+    p = tl.tl_gemm_plan(M, N, K, d, fetch)
+    banner(f"mid-M wide weight M={M} N={N} K={K} row_major={row_major} plan={p}")
+    assert (p["kernel"], p["tile_m"], p["tile_n"], p["split_k"]) == (2, 128, 128, 1)
+    assert p["workgroups"] == -(-N // 128) and p["workspace_bytes"] == 0
+    A = synth.normal_bf16((M, K), seed=190 + M)
+    W = synth.normal_bf16((N, K), seed=191, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    parity(host_f32(run_gemm(A, W, d, fetch=fetch, tile_major=not row_major)), y_ref, f"mid-M wide M={M}")
+    db = tl.layout(kind=kind, out_dtype=tl.TL_OUT_BF16)
+    parity_bf16_out(host_bits(run_gemm(A, W, db, fetch=fetch, tile_major=not row_major)), y_ref,
+                    f"mid-M wide M={M} bf16")
+    Ai = synth.small_int_bf16((M, K), seed=192)
+    Wi = synth.small_int_bf16((N, K), seed=193)
+    assert np.array_equal(host_f32(run_gemm(Ai, Wi, d, fetch=fetch, tile_major=not row_major)).astype(np.float64),
+                          oracle.gemm_f64(Ai, Wi))
+
+
 @pytest.mark.parametrize("split_k", [1, 2, 3, 7, 16])
 def test_decode_split_k_parity_and_reproducible(split_k):
     M, N, K = 8, 512, 4096

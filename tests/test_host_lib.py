@@ -193,7 +193,29 @@ def test_gemm_plan_decode_and_prefill_shapes():
     assert tl.tl_gemm_plan(32, 8192, 1024, d)["tile_n"] == 32          # 16 MB: small
     assert tl.tl_gemm_plan(32, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=32))["waves"] == 8
-    assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64))["waves"] == 4
+    # four 16-row M tiles on 64-row tiles keep one K step in flight per wave,
+    # which fits two waves per SIMD: 8 waves (bf16, read natively)
+    assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64))["waves"] == 8
+    assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64, elem_bytes=1))["waves"] == 4
+    # 33 <= M <= 64: Llama QKV, O and down stay on the decode kernel; a weight
+    # whose 128 x 128 tiles fill the CUs (N >= 32768, gate+up) takes the
+    # prefill kernel's, unless a tile or split is requested, the weight is
+    # FP8, or the fetch emulates whole blocks
+    for M in (33, 48, 64):
+        for N, K, S, waves in [(10240, 8192, 7, 4), (8192, 8192, 2, 8), (8192, 28672, 2, 8)]:
+            p = tl.tl_gemm_plan(M, N, K, d)
+            assert (p["kernel"], p["tile_n"], p["split_k"], p["waves"]) == (1, 64, S, waves), (M, N, K, p)
+        p = tl.tl_gemm_plan(M, 57344, 8192, d)
+        assert (p["kernel"], p["tile_m"], p["tile_n"], p["split_k"], p["workgroups"]) == (2, 128, 128, 1, 448)
+        assert tl.tl_gemm_plan(M, 32768, 8192, d)["kernel"] == 2
+        assert tl.tl_gemm_plan(M, 32768 - 128, 8192, d)["kernel"] == 1
+        assert tl.tl_gemm_plan(M, 57344, 8192, tl.layout(tile_n=64))["kernel"] == 1
+        assert tl.tl_gemm_plan(M, 57344, 8192, tl.layout(split_k=1))["kernel"] == 1
+        assert tl.tl_gemm_plan(M, 57344, 8192, tl.layout(elem_bytes=1))["kernel"] == 1
+        rm = tl.layout(kind=tl.TL_LAYOUT_NK_ROW)
+        assert tl.tl_gemm_plan(M, 57344, 8192, rm, tl.TL_FETCH_BLOCK)["kernel"] == 1
+        assert tl.tl_gemm_plan(M, 57344, 8192, rm, tl.TL_FETCH_NATIVE)["kernel"] == 2
+    assert tl.tl_gemm_plan(32, 57344, 8192, d)["kernel"] == 1
     p = tl.tl_gemm_plan(2048, 57344, 8192, d)
     assert p["kernel"] == 2 and p["tile_m"] == 256 and p["tile_n"] == 256
     assert tl.tl_gemm_plan(2048, 57344 + 128, 8192, d)["tile_n"] == 128
