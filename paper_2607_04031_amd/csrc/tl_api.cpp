@@ -398,6 +398,28 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                 p.waves = 8;
             }
         }
+        // 33 <= M <= 64 (four M tiles) on whole tile-major strips: the same
+        // staging with T = 4 tiles per workgroup (64 KB chunks of A; at T = 5
+        // the registers spill) and the largest S (K ranges of >= 4 chunks)
+        // whose grid fits one round of the CUs, when that fills at least 7/8
+        // of it (or S = 1 when the tile groups fill a round by themselves):
+        // a 64-row streaming tile reloads as many activation bytes from L2 as
+        // it streams weight bytes (Llama shapes, bf16 out, one box, M = 33 /
+        // 48 / 64: QKV (S = 3, 240 workgroups) 50 / 54 / 58 -> 41 / 42 / 44 us,
+        // O 33 / 35 / 39 -> 32 / 33 / 35, down 93 / 100 / 112 -> 88 / 90 / 92)
+        if (tile && !p.fp8 && p.m_tiles16 == 4 && !d->tile_n && !d->split_k && N % 128 == 0 && K % 512 == 0 &&
+            p.L.br <= 32 && 512 % p.k_unit == 0) {
+            const int64_t groups = N / 128, chunks = K / 512;
+            int64_t s_fit = groups >= kCUs ? 1 : 0;
+            for (int64_t s2 = 1; s2 <= 8 && chunks / s2 >= 4 && groups < kCUs; ++s2)
+                if (groups * s2 <= kCUs) s_fit = s2;
+            if (s_fit && 8 * groups * s_fit >= 7 * kCUs) {
+                p.lds_tiles = 4;
+                S = s_fit;
+                tn = 32;
+                p.waves = 8;
+            }
+        }
         const int64_t wgs_final = p.lds_tiles ? N / 32 / p.lds_tiles * S : wgs;
         p.pub.tile_m = 16 * p.m_tiles16;
         p.pub.tile_n = tn;

@@ -88,9 +88,9 @@ hipError_t launch_fp8_decode(const DecodeParams& p, int grid, int m_tiles16, int
 // fetch when p.log2_fetch > 0.
 hipError_t launch_kn_decode(const DecodeParams& p, int grid, int m_tiles16, int waves, hipStream_t stream);
 
-// Decode with activations staged in LDS (tl_decode_lds.hip): M <= 32,
-// tile-major, tiles_per_wg (4..7) 32-row tiles per workgroup, p.units
-// chunks of 512 columns split p.split_k ways.
+// Decode with activations staged in LDS (tl_decode_lds.hip): 17 <= M <= 64,
+// tile-major, tiles_per_wg 32-row tiles per workgroup (4..7 for M <= 32, 4
+// above), p.units chunks of 512 columns split p.split_k ways.
 hipError_t launch_lds_decode(const DecodeParams& p, int tiles_per_wg, int grid, hipStream_t stream);
 
 }  // namespace tl

@@ -80,7 +80,7 @@ struct DecodeLaunch {
     bool fp8 = false;
     const float* scales = nullptr;
     // > 0: the LDS-staged activation kernel with this many 32-row tiles per
-    // workgroup (17 <= M <= 32, tile-major, N % 32 == 0, K % 512 == 0)
+    // workgroup (17 <= M <= 64, tile-major, N % (32 lds_tiles) == 0, K % 512 == 0)
     int lds_tiles = 0;
 };
 

@@ -1,6 +1,7 @@
-"""Parity of the decode kernel that stages the activations in LDS (17 <= M <= 32
+"""Parity of the decode kernel that stages the activations in LDS (17 <= M <= 64
 on whole tile-major strips; the planner's default when its T tiles x S K
-ranges per workgroup cover the CUs in whole rounds) against the oracle:
+ranges per workgroup cover the CUs in whole rounds, or at least 7/8 of one
+round above 32 rows) against the oracle:
 every (T, S) the Llama-70B shapes use, ragged M, bf16 output, memory-tile
 shapes, exact inputs (bit-exact), reproducibility and the fetch tally."""
 import numpy as np
@@ -123,4 +124,49 @@ def test_lds_decode_fetch_tally_equals_read_amp():
     got = tl.tl_fetch_counter_read()
     amp = tl.tl_read_amp(16, N, K, 16, p["tile_n"], p["tile_k"], d, 4096)
     assert got == amp["fetched_bytes"] == 2 * N * K
+    torch.cuda.synchronize()
+
+
+# 33 <= M <= 64: four M tiles, T = 4 tiles per workgroup, 64 KB chunks of A
+# (M, N, K, G, block_rows, split_k, workgroups): 64 groups x 4 K ranges,
+# 80 groups x 3 uneven ranges (13 chunks: 4, 4, 5), 224 groups unsplit, a
+# ragged M with 16-row memory tiles of 1 KB (block_cols 32: a step spans two)
+# and one with 256-column memory tiles.
+LDS64_SHAPES = [(33, 8192, 8192, 4096, 32, 4, 256), (64, 10240, 6656, 4096, 32, 3, 240),
+                (48, 28672, 2048, 4096, 32, 1, 224), (37, 8192, 8192, 1024, 16, 4, 256),
+                (57, 16384, 4096, 16384, 32, 2, 256)]
+
+
+@pytest.mark.parametrize("M,N,K,G,br,S,wgs", LDS64_SHAPES)
+def test_lds_decode_four_m_tiles(M, N, K, G, br, S, wgs):
+    d = tl.layout(G=G, block_rows=br)
+    p = tl.tl_gemm_plan(M, N, K, d)
+    banner(f"lds decode four M tiles M={M} N={N} K={K} G={G} br={br} plan={p}")
+    assert (p["kernel"], p["tile_m"], p["tile_n"], p["waves"], p["split_k"], p["workgroups"]) == (1, 64, 32, 8, S, wgs)
+    A = synth.normal_bf16((M, K), seed=350 + M)
+    W = synth.normal_bf16((N, K), seed=351, sigma=synth.W_SIGMA)
+    y_ref = oracle.gemm_f64(A, W)
+    C1 = host_f32(run(A, W, d))
+    parity(C1, y_ref, f"lds four M tiles M={M}")
+    assert np.array_equal(C1, host_f32(run(A, W, d)))       # fixed-order sums: bitwise reproducible
+    db = tl.layout(G=G, block_rows=br, out_dtype=tl.TL_OUT_BF16)
+    parity_bf16_out(host_bits(run(A, W, db)), y_ref, f"lds four M tiles M={M} bf16")
+    Ai = synth.small_int_bf16((M, K), seed=352 + M)
+    Wi = synth.small_int_bf16((N, K), seed=353)
+    assert np.array_equal(host_f32(run(Ai, Wi, d)).astype(np.float64), oracle.gemm_f64(Ai, Wi))
+
+
+def test_lds_decode_four_m_tiles_fetch_tally():
+    import torch
+    M, N, K = 64, 8192, 8192
+    d = tl.layout()
+    p = tl.tl_gemm_plan(M, N, K, d)
+    assert p["tile_n"] == 32 and p["waves"] == 8
+    banner("lds decode four M tiles fetch tally")
+    A = synth.normal_bf16((M, K), seed=360)
+    W = synth.normal_bf16((N, K), seed=361, sigma=synth.W_SIGMA)
+    tl.tl_fetch_counter_read()
+    run(A, W, d, tl.TL_FETCH_BLOCK | tl.TL_FETCH_COUNT)
+    got = tl.tl_fetch_counter_read()
+    assert got == 2 * N * K
     torch.cuda.synchronize()

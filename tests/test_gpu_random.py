@@ -200,6 +200,23 @@ def test_random_lds_staged_cases(case):
     run_case(M, N, K, d, tl.TL_FETCH_BLOCK, seed=8000 + case)
 
 
+@pytest.mark.parametrize("case", range(4 * SCALE))
+def test_random_lds_staged_four_m_tile_cases(case):
+    """33 <= M <= 64 on weights whose groups of four 32-row tiles and K ranges
+    fill at least 7/8 of the CUs (the LDS-staged kernel with four M tiles),
+    random M, memory tile and output type."""
+    rng = np.random.default_rng(3100 + case)
+    M = int(rng.integers(33, 65))
+    N, K = [(8192, 16384), (10240, 8192), (8192, 4096 * 7), (16384, 4096)][case % 4]
+    G = int(rng.choice([1024, 4096, 16384]))
+    br = int(rng.choice([b for b in (8, 16, 32) if G // (2 * b) <= 512]))
+    d = tl.layout(G=G, block_rows=br, out_dtype=tl.TL_OUT_BF16 if case % 3 == 2 else tl.TL_OUT_F32)
+    p = tl.tl_gemm_plan(M, N, K, d)
+    assert p["waves"] == 8 and p["tile_n"] == 32 and p["tile_m"] == 64, p
+    banner(f"random lds four-M-tile case {case}: M={M} N={N} K={K} G={G} br={br} plan={p}")
+    run_case(M, N, K, d, tl.TL_FETCH_BLOCK, seed=8100 + case)
+
+
 def dev_i32(a):
     import torch
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()

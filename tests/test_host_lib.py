@@ -197,14 +197,20 @@ def test_gemm_plan_decode_and_prefill_shapes():
     # which fits two waves per SIMD: 8 waves (bf16, read natively)
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64))["waves"] == 8
     assert tl.tl_gemm_plan(64, 8192, 1024, tl.layout(tile_n=64, elem_bytes=1))["waves"] == 4
-    # 33 <= M <= 64: Llama QKV, O and down stay on the decode kernel; a weight
-    # whose 128 x 128 tiles fill the CUs (N >= 32768, gate+up) takes the
-    # prefill kernel's, unless a tile or split is requested, the weight is
-    # FP8, or the fetch emulates whole blocks
+    # 33 <= M <= 64: Llama QKV, O and down stay on the decode kernel, with the
+    # activations staged in LDS for T = 4 tiles per workgroup and the largest
+    # S whose grid fits one round of the CUs, filling >= 7/8 of it (QKV: 80
+    # groups x 3); a weight whose 128 x 128 tiles fill the CUs (N >= 32768,
+    # gate+up) takes the prefill kernel's, unless a tile or split is
+    # requested, the weight is FP8, or the fetch emulates whole blocks
     for M in (33, 48, 64):
-        for N, K, S, waves in [(10240, 8192, 7, 4), (8192, 8192, 2, 8), (8192, 28672, 2, 8)]:
+        for N, K, S, wgs in [(10240, 8192, 3, 240), (8192, 8192, 4, 256), (8192, 28672, 4, 256)]:
             p = tl.tl_gemm_plan(M, N, K, d)
-            assert (p["kernel"], p["tile_n"], p["split_k"], p["waves"]) == (1, 64, S, waves), (M, N, K, p)
+            assert (p["kernel"], p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (1, 32, S, 8, wgs), p
+        # too few groups x K ranges to fill 7/8 of the CUs: 64-row streaming tiles
+        p = tl.tl_gemm_plan(M, 8192, 2048, d)
+        assert (p["kernel"], p["tile_n"], p["split_k"], p["waves"]) == (1, 64, 2, 8), (M, p)
+        assert tl.tl_gemm_plan(M, 8192, 8192, tl.layout(tile_n=64))["tile_n"] == 64
         p = tl.tl_gemm_plan(M, 57344, 8192, d)
         assert (p["kernel"], p["tile_m"], p["tile_n"], p["split_k"], p["workgroups"]) == (2, 128, 128, 1, 448)
         assert tl.tl_gemm_plan(M, 32768, 8192, d)["kernel"] == 2
