@@ -1020,7 +1020,7 @@ def main():
     extras, sweep = None, None
     if not args.no_extras:
         extras = {}
-        for M in (1, 32):
+        for M in (1, 32, 64):
             r = decode_layer(ctx, weights, M, args.steps, args.warmup, desc, event_pass=True)
             extras[f"decode_layer_M{M}_GB/s"] = round(r["GB/s"], 1)
             extras[f"decode_layer_M{M}_event_GB/s"] = round(r["event_GB/s"], 1)
