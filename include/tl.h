@@ -209,8 +209,10 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * BLOCK) and N < 2^27.
  * M <= 64 runs the decode kernel (skinny GEMM, HBM-bound; at 17 <= M <= 32
  * on tile-major weights whose 32-row tiles and 512-column K chunks fill the
- * CUs in whole rounds, a variant that stages the activations in LDS and
- * shares them across several tiles) -- except that at 33 <= M <= 64 a bf16
+ * CUs in whole rounds, and at 33 <= M <= 64 where groups of four such tiles
+ * and the K ranges fill at least 7/8 of one round, a variant that stages the
+ * activations in LDS and shares them across several tiles) -- except that
+ * at 33 <= M <= 64 a bf16
  * weight read natively with N >= 32768 (its 128x128 tiles fill the CUs), no
  * tile or split requested and the prefill kernel's limits met, takes the
  * prefill kernel's 128x128 tiles; larger M runs the prefill kernels (bf16
