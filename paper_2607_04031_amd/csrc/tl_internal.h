@@ -147,6 +147,14 @@ struct ViewProgram {
     int64_t elements;
     int32_t elem_bytes;
     int32_t permute, row_bits, col_bits, sub_bits, log2_G;
+    // Element indices below 2^32 (fast32): the division of an index by
+    // count[c] as a multiplication (Granlund and Montgomery, "Division by
+    // invariant integers using multiplication", 1994, Section 4): for every
+    // 32-bit x, x / count[c] = (umulhi(x, magic[c]) + x) >> shift[c], with
+    // shift = ceil(log2 count) and magic = floor(2^32 (2^shift - count) / count) + 1.
+    int32_t fast32;
+    uint32_t magic[kViewMaxCounters];
+    int32_t shift[kViewMaxCounters];
 };
 
 int make_view_program(const tl_view* v, int64_t K, int64_t N, int32_t elem_bytes, int64_t G,
@@ -155,10 +163,20 @@ int make_view_program(const tl_view* v, int64_t K, int64_t N, int32_t elem_bytes
 // Host and device: byte offset of element e under the program.
 __host__ __device__ inline int64_t view_offset(const ViewProgram& P, int64_t e) {
     int64_t off = P.tile_base;
-    for (int c = 0; c < P.n_counters; ++c) {
-        const int64_t n = P.count[c];
-        off += (e % n) * P.stride[c];
-        e /= n;
+    if (P.fast32) {
+        uint32_t x = uint32_t(e);
+        for (int c = 0; c < P.n_counters; ++c) {
+            const uint32_t hi = uint32_t((uint64_t(x) * P.magic[c]) >> 32);
+            const uint32_t q = uint32_t((uint64_t(hi) + x) >> P.shift[c]);
+            off += int64_t(x - q * uint32_t(P.count[c])) * P.stride[c];
+            x = q;
+        }
+    } else {
+        for (int c = 0; c < P.n_counters; ++c) {
+            const int64_t n = P.count[c];
+            off += (e % n) * P.stride[c];
+            e /= n;
+        }
     }
     if (P.permute) {
         const int64_t G = int64_t(1) << P.log2_G;

@@ -83,6 +83,18 @@ int make_view_program(const tl_view* v, int64_t K, int64_t N, int32_t s, int64_t
         }
     }
     P.n_counters = nc;
+    // every index below 2^32 (so every count too, the counts multiplying to
+    // the element count): divisions by multiplication
+    P.fast32 = elements < (int64_t(1) << 32);
+    if (P.fast32) {
+        for (int c = 0; c < nc; ++c) {
+            const uint64_t d = uint64_t(P.count[c]);
+            int l = 0;
+            while ((uint64_t(1) << l) < d) ++l;
+            P.shift[c] = l;
+            P.magic[c] = uint32_t(((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1);
+        }
+    }
     if (u < a) {                                           // Case 2 bit permutation
         P.permute = 1;
         P.row_bits = ilog2(u * s);
