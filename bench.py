@@ -497,6 +497,7 @@ def moe_layer(ctx, steps, warmup):
                    + 2 * total * I_act + 4 * total * Nd)
     res = {"tokens": Mt, "experts_touched": touched, "expert_rows": total, "weight_bytes": wbytes,
            "step_bytes": step_bytes}
+    settle(ctx, step_grouped)       # (the weights above leave the GPU idle)
     for name, fn, byts in (("per_expert_eager", step_per_expert, step_bytes),
                            ("grouped_eager", step_grouped, step_bytes),
                            ("grouped_swiglu_fused_eager", step_fused, fused_bytes)):
@@ -567,6 +568,7 @@ def fp8_layer(ctx, steps, warmup):
             if ev is not None:
                 ev[j][1].record(ctx.stream)
 
+    settle(ctx, step)               # (the weights above leave the GPU idle)
     for _ in range(warmup):
         step()
     wall = wall_time(ctx, step, steps)
@@ -686,6 +688,7 @@ def tp_shard_layers(ctx, weights, steps, warmup):
                     tl.tl_stream_read(parts[r], 2 * Nr * Kr, ck)
 
         rounds = max(1, steps // tp)
+        settle(ctx, round_all, SETTLE_MS / 2)
         for _ in range(max(1, warmup // tp)):
             round_all()
         wall = wall_time(ctx, round_all, rounds)
