@@ -386,10 +386,11 @@ hipError_t launch_t(const DecodeParams& p, int grid, hipStream_t stream) {
     // 64-row tile (4 steps there take all 256 VGPRs: one wave per SIMD; with
     // 2 the kernel fits three -- Qwen expert down projection 66.5 -> 61.3 us).
     // Four 16-row M tiles on a 64-row tile take one step: with two its ~290
-    // registers leave one wave per SIMD, with one two (Llama shapes, bf16
-    // out, one box, M = 33 / 48 / 64: QKV 66 / 70 / 77 -> 50 / 53 / 58 us;
-    // with 8 waves, O 38 / 38 / 41 -> 33 / 35 / 39, down 103 / 100 / 112 ->
-    // 91 / 100 / 111).
+    // registers leave one wave per SIMD, with one two (this kernel on the
+    // Llama shapes, bf16 out, one box, M = 33 / 48 / 64: QKV 66 / 70 / 77 ->
+    // 50 / 53 / 58 us; with 8 waves, O 38 / 38 / 41 -> 33 / 35 / 39, down
+    // 103 / 100 / 112 -> 91 / 100 / 111; the planner now gives those three
+    // shapes to the LDS-staged kernel).
     constexpr int U = (MT >= 4 && NS == 4 && !GROUPED) ? 1 : (MT >= 2 || (GROUPED && NS == 4 && !SWIGLU)) ? 2 : 4;
     if constexpr (!TILE && !GROUPED) {
         if (p.log2_fetch > 0) {   // block emulation: fewer steps in flight leave room for the block loop
