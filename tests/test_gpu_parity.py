@@ -803,11 +803,14 @@ def test_graph_replay_matches_eager():
     banner("graph capture / replay")
     side = torch.cuda.Stream()
     # M, N, K, split_k, bf16 out: decode (split or not); the LDS-staged decode
-    # kernel (split-K 4 with its reduce, and unsplit); prefill through 128 x 128
-    # tiles, the persistent 256 x 256 and 256 x 320 grids, and the plan whose
-    # remaining columns split K (main launch, partials and reduce)
+    # kernel (split-K 4 with its reduce, and unsplit; four M tiles with
+    # split-K 4); 64-row streaming tiles at four M tiles (8 waves, split-K 2);
+    # a wide weight at M = 48 on 128 x 128 prefill tiles; prefill through
+    # 128 x 128 tiles, the persistent 256 x 256 and 256 x 320 grids, and the
+    # plan whose remaining columns split K (main launch, partials and reduce)
     cases = [(8, 1024, 2048, 1, False), (8, 1024, 2048, 4, False), (32, 512, 4096, 3, False),
              (256, 512, 1024, 0, False), (32, 8192, 16384, 0, False), (24, 32768, 2048, 0, False),
+             (48, 8192, 8192, 0, True), (40, 8192, 2048, 0, False), (48, 32768, 512, 0, True),
              (1024, 32768, 512, 0, True), (1024, 40960, 512, 0, True), (2000, 12288, 1024, 0, False)]
     with torch.cuda.stream(side):
         tensors = []

@@ -53,6 +53,7 @@ def _both(A, Wt, M, N, K, d):
 CASES = [
     ("streaming decode, split-K", (8, 10240, 8192, 0), (5, 2048, 4096, 3)),
     ("LDS-staged decode, split-K", (32, 10240, 8192, 0), (20, 4096, 4096, 0)),
+    ("LDS-staged decode with four M tiles, split-K", (64, 10240, 8192, 0), (40, 8192, 2048, 0)),
     ("prefill (no scratch), then split-K decode", (256, 1024, 512, 0), (3, 1024, 2048, 4)),
     ("prefill with K split over all columns, then split-K decode", (256, 1024, 2048, 0), (3, 1024, 2048, 4)),
     ("prefill with K-split remaining columns, then split-K decode", (2000, 10240, 2048, 0), (6, 4096, 4096, 2)),
