@@ -346,6 +346,13 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
                     tn = best_tn;
                     n_tiles = (N + tn - 1) / tn;
                     S = best_s;
+                } else if (p.fp8) {
+                    // one-byte weights: splits for about 1024 workgroups are
+                    // short (Llama QKV: 7 of 1170 K, 75 KB each) and pay their
+                    // start and drain more than they gain; at most two
+                    // rounds of 8-wave workgroups instead (QKV at M = 8,
+                    // rotated weights, one box: 20.3 -> 18.8 us)
+                    S = std::max<int64_t>(1, std::min(2 * kCUs / n_tiles, max_s));
                 } else {
                     S = std::min((kTargetWorkgroups + n_tiles - 1) / n_tiles, max_s);
                 }

@@ -237,6 +237,10 @@ def test_fp8_plans():
     p = tl.tl_gemm_plan(8, 8192, 8192, fp8)
     assert p["kernel"] == 1 and p["tile_n"] == 64 and p["tile_k"] == 64
     assert tl.tl_read_amp(8, 8192, 8192, p["tile_m"], p["tile_n"], p["tile_k"], fp8, 4096)["amp"] == 1.0
+    # tiles that neither fill two rounds nor divide the CUs (Llama QKV, 160
+    # tiles): at most two rounds of 8-wave workgroups, not ~1024 short splits
+    p = tl.tl_gemm_plan(8, 10240, 8192, fp8)
+    assert (p["tile_n"], p["split_k"], p["waves"], p["workgroups"]) == (64, 3, 8, 480), p
     for args, status in (((128, 8192, 8192, fp8), tl.TL_EUNSUPPORTED),
                          ((8, 8192, 8192, tl.layout(elem_bytes=1, G=512, block_rows=64)), tl.TL_EUNSUPPORTED),
                          ((8, 8192, 8192, tl.layout(elem_bytes=3)), tl.TL_EUNSUPPORTED),
