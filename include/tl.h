@@ -128,8 +128,9 @@ typedef struct tl_plan {
     int32_t tile_n;      /* the tile to pass to tl_read_amp to account for the  */
     int32_t tile_k;      /* kernel's fetches                                     */
     int32_t split_k;     /* workgroups per output tile along K (prefill: > 1
-                            when 256 x 256 tiles are fewer than the CUs and
-                            all columns run with K split, or when the
+                            when 256 x 256 tiles -- 128 x 128 at M <= 128 --
+                            are fewer than the CUs and all columns run with
+                            K split, or when the
                             columns past the whole rounds of 256 x 256 tiles
                             do; fp32 partials summed in a fixed order) */
     int32_t waves;       /* wavefronts per workgroup (decode: 4, 8 or 16; the
@@ -224,7 +225,8 @@ int tl_unpack(const void* src_tm, void* dst, int64_t rows, int64_t cols, int32_t
  * columns past the whole rounds take 256x256 tiles with K split across
  * workgroups, or 128x128 tiles; when 256x256 tiles are fewer than the CUs
  * (and K % 64 == 0, N % 256 == 0), every column takes them with K split, up
- * to 8 ways; see tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
+ * to 8 ways -- at M <= 128, 128x128 tiles with K split when those are fewer
+ * than the CUs (N % 128 == 0); see tl_gemm_plan).  layout->elem_bytes = 1 means an FP8 weight (OCP E4M3, one
  * byte per element, e.g. 64 x 64 memory tiles of 4 KB, Section 3.1): decode
  * kernel only, converted exactly to bf16 in registers (see tl_gemm_w8 for
  * per-channel scales).

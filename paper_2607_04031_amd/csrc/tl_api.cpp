@@ -480,6 +480,29 @@ int plan_gemm(int64_t M, int64_t N, int64_t K, const tl_layout_desc* d, int32_t 
         // Llama-70B-shaped layer, bf16 out, whole layers on one box: M = 128
         // 730 -> 464 us, 256 851 -> 514, 512 1132 -> 779, 1024 1667 -> 1419
         // (down alone at M = 1024: 535 -> 388).
+        // 65 <= M <= 128 (one row of 128-row tiles): 128 x 128 tiles with K
+        // split over all the columns in the same way, when they are fewer
+        // than the CUs -- no padded rows past 128, against half or more of a
+        // 256-row tile's
+        if (!d->tile_m && !d->tile_n && M > kDecodeMaxM && M <= 128 && N % 128 == 0 && !p.block_row &&
+            (!tile || 128 % p.L.br == 0) && N / 128 < kCUs) {
+            const int64_t t128 = N / 128;
+            const int64_t S = std::min<int64_t>({kCUs / t128, 8, (K + 63) / 64 / 8});
+            if (S >= 2) {
+                p.n_main = 0;                // no main launch: every column splits K
+                p.split_rest = int(S);
+                p.persist = false;
+                p.pub.tile_m = 128;
+                p.pub.tile_n = 128;
+                p.pub.tile_k = int(p.k_unit);
+                p.pub.split_k = int(S);
+                p.pub.waves = 4;
+                p.pub.workgroups = t128 * S;
+                p.pub.workspace_bytes = S * M * N * 4;
+                *P = p;
+                return TL_OK;
+            }
+        }
         if (!d->tile_m && !d->tile_n && M > kDecodeMaxM && K % 64 == 0 && N % 256 == 0 && !p.block_row &&
             (!tile || 256 % p.L.br == 0)) {
             const int64_t t256 = ((M + 255) / 256) * (N / 256);

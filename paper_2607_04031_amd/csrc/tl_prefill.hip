@@ -45,9 +45,10 @@ struct PrefillParams {
     bool out_bf16;
     int log2_fetch;          // block-granular emulation on a row-major weight: log2(G), else 0
     int64_t w_bytes;         // bytes of the weight (the block loads stay below it)
-    // prefill_w4_kernel only: K split across workgroups (1 = none); split s
-    // writes its fp32 partial of the M x N range to ws + s * ws_stride
-    // (row stride N), summed by prefill_splitk_reduce
+    // K split across workgroups (1 = none; prefill_w4_kernel, and
+    // prefill_kernel with 128 x 128 tiles): split s writes its fp32 partial
+    // of the M x N range to ws + s * ws_stride (row stride N), summed by
+    // prefill_splitk_reduce
     int split_k = 1;
     float* ws = nullptr;
     int64_t ws_stride = 0;
@@ -107,7 +108,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
     // contiguous range of tiles so neighbouring tiles share that XCD's L2.
     const int T = gridDim.x, b = blockIdx.x;
     const int lb = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
-    const int tm = lb % p.m_tiles, tn = lb / p.m_tiles;
+    // K split (split_k > 1): workgroup lb takes K range lb / tiles of tile
+    // lb % tiles, so the workgroups of one XCD share a K range of A
+    const int tiles = T / p.split_k;
+    const int split = lb / tiles, tix = lb - split * tiles;
+    const int tm = tix % p.m_tiles, tn = tix / p.m_tiles;
     const int m0 = tm * BM, n0 = tn * BN;
 
     // Thread t stages 16-byte chunk c = t % 8 of rows r = t / 8 + ROWS i of
@@ -151,7 +156,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
         if (TILE) return (uint32_t(k >> p.log2_bc) << p.log2_G) + uint32_t((k & p.bc_mask) << 1);
         return uint32_t(k) << 1;
     };
-    const int KT = (p.K + BK - 1) / BK;
+    // this workgroup's 64-wide K steps: [kt0, kt0 + KT)
+    const int kt_all = (p.K + BK - 1) / BK;
+    const int kt0 = int(int64_t(kt_all) * split / p.split_k);
+    const int KT = int(int64_t(kt_all) * (split + 1) / p.split_k) - kt0;
     i32x4p sink = {0, 0, 0, 0};
     uint64_t fetched = 0;
     auto fetch_blocks = [&](int k0) {
@@ -210,9 +218,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
     // issues the loads of step kt + 2, then runs step kt's MFMAs -- so the LDS
     // writes overlap the MFMAs and each global load has a full iteration to
     // arrive.
-    gload(0);
+    gload(kt0);
     sstore(0);
-    if (KT > 1) gload(1);
+    if (KT > 1) gload(kt0 + 1);
     __syncthreads();
 
     // LDS read offsets of this lane's operand rows (chunk added per sub-step)
@@ -226,7 +234,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
     for (int kt = 0; kt < KT; ++kt) {
         const int buf = kt & 1;
         if (kt + 1 < KT) sstore(buf ^ 1);
-        if (kt + 2 < KT) gload(kt + 2);
+        if (kt + 2 < KT) gload(kt0 + kt + 2);
         const uint8_t* As = smem + buf * STAGE;
         const uint8_t* Ws = As + A_BYTES;
         // Operand fragments of the next 16-wide sub-step are read while the
@@ -278,6 +286,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void prefill_kernel(PrefillParams p
     const bool full = m0 + BM <= p.M && n0 + BN <= p.N;
     const int row_base = m0 + wm * WM + 4 * (lane >> 5);
     const int col_base = n0 + wn * WN + (lane & 31);
+    if (p.split_k > 1) {   // this K range's fp32 partial (row stride N), for prefill_splitk_reduce
+        float* P = p.ws + int64_t(split) * p.ws_stride;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = row_base + i * 32 + 8 * (v >> 2) + (v & 3);
+                    const int col = col_base + j * 32;
+                    if (full || (row < p.M && col < p.N)) P[int64_t(row) * p.N + col] = acc[i][j][v];
+                }
+        return;
+    }
     if (p.out_bf16) {
         uint16_t* C = static_cast<uint16_t*>(p.C);
 #pragma unroll
@@ -809,7 +831,7 @@ hipError_t launch_t(const PrefillParams& p, int grid, bool tile, hipStream_t s) 
 // row-major; tile-major strips of block_rows rows are contiguous, and
 // n_begin is a multiple of block_rows).
 hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols, int tile_m, int tile_n,
-                        hipStream_t stream) {
+                        hipStream_t stream, int split = 1) {
     PrefillParams p;
     const int64_t c_elem = q.out_bf16 ? 2 : 4;
     const bool tile = q.L.kind == TL_LAYOUT_TILE;
@@ -872,7 +894,12 @@ hipError_t launch_range(const PrefillLaunch& q, int64_t n_begin, int64_t n_cols,
         return launch_t<256, 256, 2, 4>(p, grid, tile, stream);
     }
     if (tile_m == 256) return launch_t<256, 128, 2, 2>(p, grid, tile, stream);
-    return launch_t<128, 128, 2, 2>(p, grid, tile, stream);
+    // 128 x 128 tiles, optionally with K split 'split' ways (fp32 partials
+    // in ws, M * n_cols floats per split)
+    p.split_k = split;
+    p.ws = q.ws;
+    p.ws_stride = q.M * n_cols;
+    return launch_t<128, 128, 2, 2>(p, grid * split, tile, stream);
 }
 
 }  // namespace
@@ -882,6 +909,20 @@ hipError_t launch_prefill(const PrefillLaunch& q, hipStream_t stream) {
     hipError_t e = q.n_main > 0 ? launch_range(q, 0, q.n_main, q.tile_m, q.tile_n, stream) : hipSuccess;
     if (e != hipSuccess || q.n_main == q.N) return e;
     if (q.split_rest <= 1) return launch_range(q, q.n_main, q.N - q.n_main, 128, 128, stream);
+    if (q.n_main == 0 && q.tile_m == 128) {
+        // every column: 128 x 128 tiles with K split split_rest ways, then the
+        // fixed-order reduce
+        e = launch_range(q, 0, q.N, 128, 128, stream, q.split_rest);
+        if (e != hipSuccess) return e;
+        const int rgrid = int((q.M * q.N / 4 + 255) / 256);
+        if (q.out_bf16)
+            hipLaunchKernelGGL((prefill_splitk_reduce<true>), dim3(rgrid), dim3(256), 0, stream, q.ws, q.split_rest,
+                               q.M * q.N, int(q.M), int(q.N), q.C, int64_t(q.N));
+        else
+            hipLaunchKernelGGL((prefill_splitk_reduce<false>), dim3(rgrid), dim3(256), 0, stream, q.ws, q.split_rest,
+                               q.M * q.N, int(q.M), int(q.N), q.C, int64_t(q.N));
+        return hipGetLastError();
+    }
     // the remaining columns: 256 x 256 tiles of prefill_w4_kernel, K split
     // split_rest ways (fp32 partials in ws), then the fixed-order reduce
     const bool tile = q.L.kind == TL_LAYOUT_TILE;

@@ -472,9 +472,13 @@ def test_prefill_persistent_grid(M, N, K, pin):
 # the plan splits K over all the columns (S = CUs / tiles, at most 8, each
 # split >= 8 K steps; fp32 partials, then the split-order reduce).  M, N, K,
 # row-major [N][K] weight: ragged M with S = 8, S = 4, a row-major weight with
-# S = 2, and M = 96 (S = 8) and 65 (S = 4) in one 256-row tile.
+# S = 2; at M <= 128 the same over 128 x 128 tiles: M = 96 (S = 8) and 65
+# (S = 4), 80 tiles x 3 uneven ranges (10, 11, 11 K steps), a row-major
+# weight whose K has a partial last step (S = 2: 8 and 8 steps, the last 40
+# wide), and a ragged M of 77.
 KSPLIT_ALL = [(300, 2048, 4096, False), (512, 4096, 2048, False), (256, 1024, 1024, True),
-              (96, 2048, 4096, False), (65, 1024, 2048, False)]
+              (96, 2048, 4096, False), (65, 1024, 2048, False), (128, 10240, 2048, False),
+              (100, 1024, 1000, True), (77, 4096, 2048, False)]
 
 
 @pytest.mark.parametrize("M,N,K,row_major", KSPLIT_ALL)
@@ -484,10 +488,11 @@ def test_prefill_ksplit_all_columns(M, N, K, row_major):
     d = tl.layout(kind=kind)
     plan = tl.tl_gemm_plan(M, N, K, d, fetch)
     banner(f"prefill K split over all columns M={M} N={N} K={K} row_major={row_major} plan={plan}")
-    t256 = -(-M // 256) * (N // 256)
-    S = min(256 // t256, 8, K // 512)
-    assert S >= 2 and (plan["tile_m"], plan["tile_n"], plan["split_k"]) == (256, 256, S)
-    assert plan["workgroups"] == t256 * S and plan["workspace_bytes"] == S * M * N * 4
+    tm = 128 if M <= 128 else 256
+    tiles = -(-M // tm) * (N // tm)
+    S = min(256 // tiles, 8, -(-K // 64) // 8)
+    assert S >= 2 and (plan["tile_m"], plan["tile_n"], plan["split_k"]) == (tm, tm, S)
+    assert plan["workgroups"] == tiles * S and plan["workspace_bytes"] == S * M * N * 4
     A = synth.normal_bf16((M, K), seed=170 + S)
     W = synth.normal_bf16((N, K), seed=171, sigma=synth.W_SIGMA)
     y_ref = oracle.gemm_f64(A, W)
