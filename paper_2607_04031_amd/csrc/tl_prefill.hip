@@ -14,7 +14,9 @@
 //    the weight tile through registers into LDS (double buffered, one barrier
 //    per step); 4 waves in a 2 x 2 grid, or 8 in 2 x 4 for 256 x 256.  LDS
 //    rows are 128 B with 16-byte chunks XOR-swizzled (see swz) so operand
-//    reads are free of bank conflicts.
+//    reads are free of bank conflicts.  With 128 x 128 tiles it also takes
+//    a K range per workgroup (the plan for 65 <= M <= 128 when the tiles are
+//    fewer than the CUs) and writes fp32 partials for prefill_splitk_reduce.
 // Padded weights (Section 3.3; strips of ceil(K / bc) memory tiles): rows
 // past M or N are clamped and never stored; in prefill_kernel a last K step
 // partly past K (K % 8 == 0) stages zeros for the chunks past K.
