@@ -296,6 +296,24 @@ def test_prefill_plan_column_split():
     # a memory tile taller than the 128-row remainder tiles keeps one launch
     tall = tl.layout(G=65536, block_rows=256, out_dtype=tl.TL_OUT_BF16)
     assert tl.tl_gemm_plan(2048, 10240, 8192, tall)["workgroups"] == 256
+    # small and medium M: K split over all the columns where the tiles are
+    # fewer than the CUs -- 128 x 128 tiles at M <= 128, 256 x 256 above
+    for M in (65, 96, 128):
+        for N, K, S in [(10240, 8192, 3), (8192, 8192, 4), (8192, 28672, 4)]:
+            p = tl.tl_gemm_plan(M, N, K, bf)
+            assert (p["tile_m"], p["tile_n"], p["split_k"]) == (128, 128, S), (M, N, K, p)
+            assert p["workgroups"] == N // 128 * S and p["workspace_bytes"] == S * M * N * 4
+        g = tl.tl_gemm_plan(M, 57344, 8192, bf)                 # 448 tiles: no split
+        assert (g["tile_m"], g["tile_n"], g["split_k"], g["workgroups"]) == (128, 128, 1, 448)
+    p = tl.tl_gemm_plan(129, 10240, 8192, bf)
+    assert (p["tile_m"], p["tile_n"], p["split_k"], p["workgroups"]) == (256, 256, 6, 240)
+    # a K of 1000: 16 K steps (the last partial) split in two
+    p = tl.tl_gemm_plan(100, 1024, 1000, tl.layout(kind=tl.TL_LAYOUT_NK_ROW), tl.TL_FETCH_NATIVE)
+    assert (p["tile_m"], p["split_k"], p["workgroups"]) == (128, 2, 16)
+    # pinned tiles: no K split
+    assert tl.tl_gemm_plan(96, 10240, 8192, tl.layout(tile_m=128, tile_n=128))["split_k"] == 1
+    tall = tl.layout(G=65536, block_rows=256, tile_m=256, tile_n=256, out_dtype=tl.TL_OUT_BF16)
+    assert tl.tl_gemm_plan(96, 10240, 8192, tall)["split_k"] == 1
 
 
 def test_gemm_plan_error_codes():
